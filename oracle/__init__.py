@@ -1,0 +1,228 @@
+"""CPU oracle of the mini-batch GNN hot path (TEST INFRASTRUCTURE).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg
+may import this package.  The product path (``paper_2010_05337_amd``) never
+imports it and shares no code with it.
+
+The arithmetic lives in ``oracle.c`` (plain C, fp64, single-threaded); this
+module compiles it with gcc, loads it with ctypes and composes the layers.
+Every step follows DistDGL (arXiv 2010.05337) Section II-B (mini-batch
+construction) and Section II-A Eq. (1) (message passing) as read in the
+header of ``oracle.c``.
+
+Parity status per function:
+  philox4x32_10     pinned: published known-answer vectors (tests/golden)
+  bounded_from_word pinned: exhaustive enumeration of all 2^32 words
+  floyd             pinned: brute force over all draw sequences, d <= 8
+  sample_node       pinned: chi-square uniformity, invariants
+  sample_blocks     pinned: relabel invariants that determine it uniquely,
+                    batch-composition independence
+  gather            pinned: numpy fancy indexing
+  mean_aggregate    pinned: dense D^-1 A H with numpy
+  sage_forward      pinned: full-neighbourhood special case == full-graph
+                    dense GraphSAGE (numpy)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+STATUS = {0: "OK", -1: "EINVAL", -4: "ERANGE", -5: "EDUP", -6: "ENOMEM"}
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(f"oracle status {code} ({STATUS.get(code, '?')})")
+        self.code = code
+
+
+def build(force: bool = False) -> str:
+    """Compile liboracle.so: gcc -O2, no fast-math, no SIMD intrinsics."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-Wall", _SRC,
+                               "-o", tmp])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        vp, i64, u32, u64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
+        L.orc_philox4x32_10.restype = None
+        L.orc_philox4x32_10.argtypes = [vp, vp, vp]
+        L.orc_bounded_from_word.restype = ctypes.c_int
+        L.orc_bounded_from_word.argtypes = [u32, u32, ctypes.POINTER(u32)]
+        L.orc_uniform_below.restype = u32
+        L.orc_uniform_below.argtypes = [u64, u32, u32, u32, u32]
+        L.orc_floyd.restype = None
+        L.orc_floyd.argtypes = [u32, u32, vp, vp]
+        L.orc_sample_node.restype = i64
+        L.orc_sample_node.argtypes = [u64, u32, u32, i64, i64, vp]
+        L.orc_sample_blocks.restype = ctypes.c_int
+        L.orc_sample_blocks.argtypes = [i64, vp, vp, vp, i64, vp, ctypes.c_int, u64,
+                                        ctypes.POINTER(vp)]
+        L.orc_free_blocks.restype = None
+        L.orc_free_blocks.argtypes = [vp]
+        L.orc_block_sizes.restype = None
+        L.orc_block_sizes.argtypes = [vp, ctypes.c_int, vp]
+        L.orc_block_copy.restype = None
+        L.orc_block_copy.argtypes = [vp, ctypes.c_int, vp, vp, vp, vp]
+        L.orc_gather.restype = ctypes.c_int
+        L.orc_gather.argtypes = [vp, i64, i64, vp, i64, vp]
+        L.orc_mean_aggregate.restype = None
+        L.orc_mean_aggregate.argtypes = [i64, vp, vp, vp, i64, vp]
+        L.orc_sage_linear.restype = None
+        L.orc_sage_linear.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, ctypes.c_int, vp]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data) if a.size else None
+
+
+# ---------------------------------------------------------------- O1 / O2 / O3
+
+def philox4x32_10(ctr, key) -> np.ndarray:
+    c = np.asarray(ctr, dtype=np.uint32)
+    k = np.asarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().orc_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def bounded_from_word(x: int, m: int):
+    """Lemire's draw from one word: the value in [0, m), or None if rejected."""
+    t = ctypes.c_uint32(0)
+    ok = lib().orc_bounded_from_word(x, m, ctypes.byref(t))
+    return t.value if ok else None
+
+
+def uniform_below(seed: int, v: int, l: int, i: int, m: int) -> int:
+    return lib().orc_uniform_below(seed, v, l, i, m)
+
+
+def floyd(d: int, k: int, draws) -> np.ndarray:
+    t = np.ascontiguousarray(draws, dtype=np.uint32)
+    out = np.zeros(max(k, 1), dtype=np.uint32)
+    lib().orc_floyd(d, k, _p(t), _p(out))
+    return out[:k]
+
+
+def sample_node(seed: int, v: int, l: int, deg: int, fanout: int) -> np.ndarray:
+    """Ascending row slots sampled for node v at layer l."""
+    out = np.zeros(max(min(deg, fanout), 1), dtype=np.uint32)
+    k = lib().orc_sample_node(seed, v, l, deg, fanout, _p(out))
+    return out[:k]
+
+
+# ---------------------------------------------------------------- O4
+
+@dataclass
+class Block:
+    """Bipartite block of model layer l: destinations = src[:n_dst]."""
+    n_dst: int
+    n_src: int
+    nnz: int
+    indptr: np.ndarray   # int64 [n_dst+1]
+    nbr: np.ndarray      # int64 [nnz] global ids of sampled in-neighbours
+    local: np.ndarray    # int64 [nnz] positions in src
+    src: np.ndarray      # int64 [n_src] global ids
+
+
+def sample_blocks(indptr, indices, seeds, fanouts, seed: int):
+    """Blocks for model layers 0..L-1 (index 0 = input layer)."""
+    ip = np.ascontiguousarray(indptr, dtype=np.int64)
+    ix = np.ascontiguousarray(indices, dtype=np.int32)
+    sd = np.ascontiguousarray(seeds, dtype=np.int64)
+    fo = np.ascontiguousarray(fanouts, dtype=np.int64)
+    h = ctypes.c_void_p()
+    st = lib().orc_sample_blocks(len(ip) - 1, _p(ip), _p(ix), _p(sd), len(sd), _p(fo), len(fo),
+                                 seed & 0xFFFFFFFFFFFFFFFF, ctypes.byref(h))
+    if st != 0:
+        raise OracleError(st)
+    try:
+        blocks = []
+        for l in range(len(fo)):
+            sz = np.zeros(3, dtype=np.int64)
+            lib().orc_block_sizes(h, l, _p(sz))
+            n_dst, n_src, nnz = (int(x) for x in sz)
+            b = Block(n_dst, n_src, nnz, np.zeros(n_dst + 1, np.int64), np.zeros(nnz, np.int64),
+                      np.zeros(nnz, np.int64), np.zeros(n_src, np.int64))
+            lib().orc_block_copy(h, l, _p(b.indptr), _p(b.nbr), _p(b.local), _p(b.src))
+            blocks.append(b)
+    finally:
+        lib().orc_free_blocks(h)
+    return blocks
+
+
+# ---------------------------------------------------------------- O5
+
+def gather(feats: np.ndarray, ids) -> np.ndarray:
+    """Rows of `feats` at `ids`, copied bit for bit (any dtype)."""
+    f = np.ascontiguousarray(feats)
+    ii = np.ascontiguousarray(ids, dtype=np.int64)
+    out = np.empty((len(ii),) + f.shape[1:], dtype=f.dtype)
+    row_bytes = f.strides[0] if f.ndim > 1 else f.itemsize
+    st = lib().orc_gather(_p(f), f.shape[0], row_bytes, _p(ii), len(ii), _p(out))
+    if st != 0:
+        raise OracleError(st)
+    return out
+
+
+def widen(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact stored values as float64 (bf16 arrives as uint16 bit patterns)."""
+    if dtype == "bf16":
+        return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return x.astype(np.float64)
+
+
+# ---------------------------------------------------------------- O6
+
+def mean_aggregate(block: Block, H: np.ndarray) -> np.ndarray:
+    H = np.ascontiguousarray(H, dtype=np.float64)
+    d = H.shape[1]
+    m = np.zeros((block.n_dst, d), dtype=np.float64)
+    lib().orc_mean_aggregate(block.n_dst, _p(block.indptr), _p(block.local), _p(H), d, _p(m))
+    return m
+
+
+def sage_linear(H_dst: np.ndarray, m: np.ndarray, w_self, w_neigh, bias, relu: bool) -> np.ndarray:
+    H_dst = np.ascontiguousarray(H_dst, dtype=np.float64)
+    m = np.ascontiguousarray(m, dtype=np.float64)
+    ws = np.ascontiguousarray(w_self, dtype=np.float64)
+    wn = np.ascontiguousarray(w_neigh, dtype=np.float64)
+    b = np.ascontiguousarray(bias, dtype=np.float64)
+    n, d_in = m.shape
+    d_out = ws.shape[1]
+    out = np.zeros((n, d_out), dtype=np.float64)
+    lib().orc_sage_linear(n, d_in, d_out, _p(H_dst), _p(m), _p(ws), _p(wn), _p(b), int(relu),
+                          _p(out))
+    return out
+
+
+def sage_forward(blocks, X: np.ndarray, w_self, w_neigh, bias):
+    """GraphSAGE-mean over the blocks (layer 0 first).  X is the fp64 input
+    of blocks[0]'s sources.  Returns (logits [B, C], [H_1, ..., H_L])."""
+    H = np.ascontiguousarray(X, dtype=np.float64)
+    outs = []
+    L = len(blocks)
+    for l, blk in enumerate(blocks):
+        m = mean_aggregate(blk, H)
+        H = sage_linear(H[:blk.n_dst], m, w_self[l], w_neigh[l], bias[l], relu=(l < L - 1))
+        outs.append(H)
+    return H, outs

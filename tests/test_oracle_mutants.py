@@ -1,0 +1,112 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each case copies the oracle source, plants one mistake, builds it on the CPU
+in a temporary directory and runs the pin meant to catch it against the
+mutant, which must fail.  Nothing here touches the GPU.
+"""
+import ctypes
+import importlib.util
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import test_oracle_blocks as tb
+import test_oracle_rng as tr
+import test_oracle_sampling as ts
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+MUTANTS = {
+    # Philox: multipliers swapped between the two lanes
+    "philox_multipliers_swapped": ("(uint64_t)PHILOX_M0 * c[0]", "(uint64_t)PHILOX_M1 * c[0]"),
+    # Philox: key bumped before the first round as well
+    "philox_key_schedule": ("if (round > 0) {", "if (round >= 0) {"),
+    # Philox: output lanes mixed up
+    "philox_output_order": ("uint32_t n1 = lo1;", "uint32_t n1 = lo0;"),
+    # bounded draw: no rejection (biased modulo-like draw)
+    "bounded_no_rejection": ("if (low < threshold) return 0;", "(void)threshold;"),
+    # Floyd: inserts the draw even when it is already chosen
+    "floyd_insert_wrong": ("chosen[i] = present ? j : t;", "chosen[i] = present ? t : j;"),
+    # Floyd: draw range off by one ([0, j) instead of [0, j])
+    "floyd_draw_range": ("orc_uniform_below(seed, v, l, i, j + 1)", "orc_uniform_below(seed, v, l, i, j)"),
+    # relabel: local ids off by one
+    "relabel_off_by_one": ("B->local[e] = map[u] - 1;", "B->local[e] = map[u];"),
+    # relabel: new nodes not recorded in the map (duplicates in src)
+    "relabel_no_dedup": ("map[u] = n_src + 1;\n", "\n"),
+    # mean: divides by the fan-out instead of the sampled count
+    "mean_divides_by_wrong_count": ("row[c] = row[c] / (double)k;", "row[c] = row[c] / (double)(k + 1);"),
+    # SAGE: neighbour weights applied transposed
+    "sage_transposed_weight": ("m[v * d_in + c] * w_neigh[c * d_out + o]", "m[v * d_in + c] * w_neigh[o * d_in + c]"),
+    # SAGE: bias dropped
+    "sage_no_bias": ("double z = bias[o];", "double z = 0.0;"),
+    # sampling: slots mapped to the row in reverse
+    "sample_slots_reversed": ("int64_t u = indices[indptr[v] + slots[q]];",
+                              "int64_t u = indices[indptr[v] + (d - 1 - slots[q])];"),
+    # sampling: fan-out of the wrong layer (hop index instead of layer index)
+    "sample_wrong_layer_fanout": ("int64_t f = fanouts[l];", "int64_t f = fanouts[hop];"),
+}
+
+
+def _build_mutant(tmpdir, name):
+    old, new = MUTANTS[name]
+    src = open(os.path.join(ROOT, "oracle", "oracle.c")).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    d = os.path.join(tmpdir, name)
+    os.makedirs(d, exist_ok=True)
+    path = os.path.join(d, "oracle.c")
+    with open(path, "w") as fh:
+        fh.write(src.replace(old, new))
+    so = os.path.join(d, "liboracle.so")
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-w", path, "-o", so])
+    spec = importlib.util.spec_from_file_location(f"oracle_mutant_{name}",
+                                                  os.path.join(ROOT, "oracle", "__init__.py"))
+    mod = importlib.util.module_from_spec(spec)
+    sys.modules[spec.name] = mod
+    spec.loader.exec_module(mod)
+    mod._LIB = so
+    mod._lib = None
+    pins_so = os.path.join(d, "libpins.so")
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-pthread",
+                           os.path.join(ROOT, "tests", "native", "pins.c"), "-o", pins_so,
+                           "-L" + d, "-loracle", "-Wl,-rpath," + d])
+    pins = ctypes.CDLL(pins_so)
+    vp, u32, u64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64
+    pins.pin_bounded_exhaustive.restype = ctypes.c_int
+    pins.pin_bounded_exhaustive.argtypes = [u32, vp, ctypes.POINTER(u64), ctypes.c_int]
+    for fn in ("pin_subset_hist", "pin_subset_hist_nodes", "pin_marginals"):
+        getattr(pins, fn).restype = ctypes.c_int
+        getattr(pins, fn).argtypes = [u32, u32, u32, u32, u64, u64, vp]
+    return mod, pins
+
+
+def _fails(fn):
+    """True when the pin rejects the mutant (an assertion fails).  Any other
+    exception does not count as a catch."""
+    try:
+        fn()
+    except AssertionError:
+        return True
+    except Exception:
+        return False
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, tmp_path, dg):
+    mut, pins = _build_mutant(str(tmp_path), name)
+    tiny = dg.er_directed(10000, 10.0, 101)
+    checks = {
+        "philox": lambda: tr.test_philox_known_answers(mut),
+        "bounded": lambda: tr.test_bounded_draw_exhaustive(pins, 7),
+        "floyd": lambda: ts.test_floyd_brute_force_exact_uniformity(mut, 5),
+        "chi2": lambda: ts.test_keyed_subsets_uniform_over_keys(pins, 8, 3, 200000),
+        "blocks": lambda: tb.test_tiny_blocks_invariants(mut, dg, tiny),
+        "rmat": lambda: tb.test_rmat_blocks_invariants_with_hubs(mut, dg),
+        "mean": lambda: tb.test_mean_aggregate_matches_dense(mut, dg, tiny),
+        "dense": lambda: tb.test_full_neighbourhood_equals_dense_sage(mut, dg, 2),
+    }
+    caught = next((k for k, fn in checks.items() if _fails(fn)), None)
+    assert caught is not None, f"mutant {name} passed every pin"
