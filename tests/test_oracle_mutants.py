@@ -59,7 +59,9 @@ def _build_mutant(tmpdir, name):
     path = os.path.join(d, "oracle.c")
     with open(path, "w") as fh:
         fh.write(src.replace(old, new))
-    so = os.path.join(d, "liboracle.so")
+    # a file name of its own: a shared object is matched by name when another
+    # library asks for it, so the mutant must not be called liboracle.so
+    so = os.path.join(d, f"liboracle_{name}.so")
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-w", path, "-o", so])
     spec = importlib.util.spec_from_file_location(f"oracle_mutant_{name}",
                                                   os.path.join(ROOT, "oracle", "__init__.py"))
@@ -71,7 +73,7 @@ def _build_mutant(tmpdir, name):
     pins_so = os.path.join(d, "libpins.so")
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-pthread",
                            os.path.join(ROOT, "tests", "native", "pins.c"), "-o", pins_so,
-                           "-L" + d, "-loracle", "-Wl,-rpath," + d])
+                           "-L" + d, f"-l:liboracle_{name}.so", "-Wl,-rpath," + d])
     pins = ctypes.CDLL(pins_so)
     vp, u32, u64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64
     pins.pin_bounded_exhaustive.restype = ctypes.c_int
