@@ -1,0 +1,231 @@
+/*
+ * gmb.h — C ABI of the mini-batch GNN hot path on MI355X (gfx950).
+ *
+ * The library implements the data-parallel part of one trainer's iteration
+ * in DistDGL (arXiv 2010.05337): build a mini-batch by recursive fan-out
+ * neighbour sampling (Section II-B), pull the feature rows of the sampled
+ * vertices (the KVStore "pull" of Section III-C, here a local gather), and
+ * run the GraphSAGE-mean forward pass (Section II-A, Eq. (1); model of
+ * Section IV).
+ *
+ * Conventions shared by every entry point
+ *   - Pointers documented "device" are HIP device pointers; "host" are host
+ *     pointers.  Device buffers are owned by the caller; the library never
+ *     allocates, frees or keeps device memory.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     All device work of a call is enqueued on that stream; a call returns
+ *     as soon as the work is enqueued, unless it says it synchronises.
+ *   - Return value: GMB_OK (0) or a negative gmb_status.  Argument errors are
+ *     detected on the host before anything is enqueued, so nothing runs and
+ *     no buffer is touched.  Errors in the data (a vertex id out of range, a
+ *     duplicated seed) are found on the device; they set bits of a sticky
+ *     status word that gmb_read_status() returns.  Outputs produced under a
+ *     data error are unspecified, but every access stays in bounds.
+ *   - gmb_last_error() returns a thread-local message for the last failing
+ *     call on this thread.
+ *   - Layer numbering: model layer l = 0 is the input layer; fanouts[l]
+ *     belongs to layer l, so the first hop (from the seeds) uses
+ *     fanouts[L-1], and blocks are returned in layer order.
+ *   - Vertex ids are int32 (graphs up to 2^31 - 1 vertices); CSR row offsets
+ *     may be int32 or int64.
+ */
+#ifndef GMB_H
+#define GMB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GMB_MAX_LAYERS 8
+#define GMB_ABI_VERSION 1
+
+typedef enum {
+  GMB_OK = 0,
+  GMB_EINVAL = -1,   /* bad argument (null pointer, bad size, unsupported shape) */
+  GMB_ENOSPC = -2,   /* workspace or state buffer too small */
+  GMB_EDEVICE = -3,  /* a HIP runtime call failed */
+  GMB_ERANGE = -4,   /* (device) a vertex id outside [0, num_nodes) */
+  GMB_EDUP = -5      /* (device) the seed list holds a vertex twice */
+} gmb_status;
+
+typedef enum { GMB_F32 = 0, GMB_BF16 = 1 } gmb_dtype;
+
+/* Bits of the device status word. */
+#define GMB_STATUS_ERANGE 1u
+#define GMB_STATUS_EDUP 2u
+
+/* In-neighbour CSR of the input graph G(V, E) (Section II-A): row v lists
+ * the sources u of the edges u -> v, so sampling row v samples the vertices
+ * whose messages flow into v.  Rows must be sorted ascending and unique;
+ * without that, sampled neighbour sets may hold duplicates.
+ * All pointers are device pointers, read-only, owned by the caller. */
+typedef struct {
+  int64_t num_nodes;      /* |V|, 1 .. 2^31 - 1 */
+  int64_t num_edges;      /* |E| = indptr[num_nodes] */
+  const void* indptr;     /* [num_nodes + 1] int32 or int64 row offsets */
+  int32_t indptr_bits;    /* 32 or 64 */
+  int32_t reserved;
+  const int32_t* indices; /* [num_edges] source vertex of each edge */
+} gmb_csr;
+
+/* One bipartite block of the sampled computation graph (Fig. 1(b)): the
+ * messages of model layer l flow from the block's sources to its
+ * destinations.  Filled in by gmb_sample_blocks with pointers into the
+ * caller's workspace; sizes live on the device.
+ *   indptr  [cap_dst + 1]  row offsets: edges of destination p are
+ *                          [indptr[p], indptr[p+1]), k_p = min(deg, fanout)
+ *   indices [cap_nnz]      local source id of each edge: a position in src_ids
+ *   nbr     [cap_nnz]      the same edges as global vertex ids, each row in
+ *                          ascending CSR-slot order
+ *   src_ids [cap_src]      global ids of the sources; the first n_dst entries
+ *                          are the destinations, in order, followed by the
+ *                          new vertices in order of first appearance over
+ *                          (destination position, slot).  All blocks of one
+ *                          call share this array: block l uses its first
+ *                          n_src(l) entries, and block 0's sources are the
+ *                          input vertices whose features are gathered.
+ *   sizes   [4]            device int32: n_dst, n_src, nnz, 0
+ * cap_* are host-known upper bounds of the device-side sizes. */
+typedef struct {
+  int32_t* indptr;
+  int32_t* indices;
+  int32_t* nbr;
+  int32_t* src_ids;
+  int32_t* sizes;
+  int64_t cap_dst, cap_src, cap_nnz;
+  int32_t fanout;
+  int32_t layer;
+} gmb_block;
+
+typedef struct {
+  int32_t num_layers;
+  int32_t num_seeds;
+  gmb_block blk[GMB_MAX_LAYERS];   /* blk[l] = model layer l */
+} gmb_blocks;
+
+/* GraphSAGE-mean weights of an L-layer model (Section IV: 3 layers, hidden
+ * 256).  Layer l maps dims[l] -> dims[l+1]:
+ *   h_v' = act(h_v W_self[l] + mean_{u in sampled N(v)} h_u W_neigh[l] + bias[l])
+ * with act = ReLU for l < L-1 and the identity for the last layer.
+ * w_self[l], w_neigh[l]: device, [dims[l]][dims[l+1]] row-major, in `dtype`
+ * (fp32, or bf16 bit patterns).  bias[l]: device, [dims[l+1]] fp32.  The
+ * input features must have the same dtype as the matrices. */
+typedef struct {
+  int32_t num_layers;
+  int32_t dtype;                       /* gmb_dtype */
+  int32_t dims[GMB_MAX_LAYERS + 1];
+  const void* w_self[GMB_MAX_LAYERS];
+  const void* w_neigh[GMB_MAX_LAYERS];
+  const float* bias[GMB_MAX_LAYERS];
+} gmb_sage_weights;
+
+/* ---- library ---------------------------------------------------------- */
+
+/* GMB_ABI_VERSION of the loaded library. */
+int32_t gmb_abi_version(void);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* gmb_last_error(void);
+
+/* ---- sampler state ---------------------------------------------------- */
+
+/* The sampler keeps one 32-bit slot per vertex (the dedup table of the
+ * relabel step) plus a status word, in a caller-owned device buffer that
+ * outlives calls: gmb_sampler_state_bytes() bytes for `num_nodes` vertices.
+ * gmb_sampler_state_init() clears it (enqueued on `stream`); every
+ * gmb_sample_blocks call leaves the table clear again.  One state serves
+ * one call at a time: calls that share a state must be ordered on one
+ * stream.  Returns 0 for num_nodes outside 1 .. 2^31 - 1. */
+size_t gmb_sampler_state_bytes(int64_t num_nodes);
+int gmb_sampler_state_init(void* state, size_t state_bytes, int64_t num_nodes, void* stream);
+
+/* Device address of the state's status word (uint32, GMB_STATUS_* bits),
+ * for passing to gmb_gather_features; NULL for a NULL state. */
+uint32_t* gmb_state_status_word(void* state);
+
+/* Synchronises `stream`, reads and clears the status word and returns the
+ * matching status (GMB_ERANGE before GMB_EDUP), or GMB_OK. */
+int gmb_read_status(void* state, void* stream);
+
+/* ---- sampling (Section II-B, steps (i)-(ii), recursive per layer) ------- */
+
+/* Bytes of workspace gmb_sample_blocks needs for these shapes (0 for bad
+ * arguments). */
+size_t gmb_sample_workspace_bytes(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
+                                  int64_t num_nodes);
+
+/* Samples an L-layer mini-batch.
+ *   seeds     device int32[num_seeds]: the target vertices, distinct, in
+ *             [0, num_nodes) (a duplicate sets GMB_STATUS_EDUP, an id out of
+ *             range GMB_STATUS_ERANGE).  num_seeds may be 0.
+ *   fanouts   host int32[num_layers], each >= 1: at most fanouts[l]
+ *             in-neighbours of each destination of layer l are picked,
+ *             uniformly without replacement; a vertex with in-degree
+ *             <= fanouts[l] keeps all of them.
+ *   seed      64-bit key.  The sample of vertex v at layer l depends only on
+ *             (seed, v, l) and the CSR row of v: Philox4x32-10 keyed by
+ *             (lo32(seed), hi32(seed)) with counter (v, l, i, r) draws the
+ *             i-th number of Floyd's algorithm by Lemire's
+ *             multiply-and-reject on words x0..x3 of block r = 0, 1, ...
+ *   state     the sampler state of this graph (see above).
+ *   ws        device workspace of >= gmb_sample_workspace_bytes(...) bytes,
+ *             256-byte aligned; the blocks point into it and stay valid
+ *             until the workspace is reused.
+ *   out       host struct filled with the blocks' pointers and capacities.
+ * No host synchronisation: the sizes stay on the device (gmb_read_sizes). */
+int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds,
+                      const int32_t* fanouts, int32_t num_layers, uint64_t seed,
+                      void* state, size_t state_bytes, void* ws, size_t ws_bytes,
+                      gmb_blocks* out, void* stream);
+
+/* Synchronises `stream` and copies the device sizes to host
+ * sizes[num_layers][3] = {n_dst, n_src, nnz} (layer order). */
+int gmb_read_sizes(const gmb_blocks* blocks, int64_t* sizes, void* stream);
+
+/* ---- feature gather (KVStore pull, Section III-C) ---------------------- */
+
+/* out[i, :] = feats[ids[i], :] bit for bit, for i < n, where n = *n_dev
+ * (device int32, e.g. block 0's n_src) clamped to n_cap, or n = n_cap when
+ * n_dev is NULL.  Rows at i >= n are not written.
+ *   ids    device int32[n_cap]
+ *   feats  device [num_nodes, dim] row-major, element size from dtype
+ *   out    device [n_cap, dim]
+ *   status device uint32 status word or NULL: an id outside [0, num_nodes)
+ *          sets GMB_STATUS_ERANGE there and its output row is zero-filled. */
+int gmb_gather_features(const int32_t* ids, const int32_t* n_dev, int64_t n_cap, const void* feats,
+                        int64_t num_nodes, int32_t dim, int32_t dtype, void* out, uint32_t* status,
+                        void* stream);
+
+/* ---- GraphSAGE-mean forward (Eq. (1), Section IV model) ----------------- */
+
+/* Bytes of workspace gmb_sage_forward needs (0 for bad arguments). */
+size_t gmb_forward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights);
+
+/* Byte offset in the forward workspace of the output of layer l < L-1
+ * (the hidden activations, [n_dst(l), dims[l+1]] in the weights' dtype);
+ * -1 for a bad layer. */
+int64_t gmb_forward_hidden_offset(const gmb_blocks* blocks, const gmb_sage_weights* weights,
+                                  int32_t layer);
+
+/* Runs the L layers over the blocks.
+ *   x       device [blocks->blk[0].cap_src, dims[0]] in weights->dtype: the
+ *           gathered input features of block 0's sources (rows beyond
+ *           n_src are not read).
+ *   logits  device fp32 [num_seeds, dims[L]].
+ *   ws      device workspace of >= gmb_forward_workspace_bytes() bytes,
+ *           256-byte aligned.
+ * Per layer: the mean of the sampled in-neighbours' rows (0 for a vertex
+ * with none) accumulated in fp32, then the two products and the bias in
+ * one matrix-core GEMM with fp32 accumulation.  In bf16 mode the mean and
+ * the hidden activations are rounded to bf16 before the next product. */
+int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
+                     float* logits, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GMB_H */

@@ -1,0 +1,396 @@
+// C ABI of the mini-batch GNN hot path (declared in include/gmb.h):
+// argument validation, workspace planning and kernel launches.  No C++
+// exception crosses the ABI; every entry point returns a gmb_status.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "gmb.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  return GMB_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(GMB_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxInt32 = 0x7FFFFFFF;
+constexpr size_t kStateHeader = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+// ---- sampling workspace plan -------------------------------------------
+
+struct HopPlan {
+  int layer;
+  int fanout;
+  int64_t cap_dst, cap_nnz, cap_src;
+  size_t off_indptr, off_nbr, off_local;
+  int64_t count_tiles_word, count_ticket_word, flag_tiles_word, flag_ticket_word;
+};
+
+struct SamplePlan {
+  int num_layers;
+  HopPlan hop[GMB_MAX_LAYERS];
+  size_t off_ids, off_sizes, off_zero;
+  int64_t num_zero_words;
+  int64_t cap_ids;
+  size_t total;
+};
+
+// Fills the plan; returns GMB_OK or an argument error (message set).
+int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers, int64_t num_nodes,
+                  SamplePlan* plan) {
+  if (num_layers < 1 || num_layers > GMB_MAX_LAYERS)
+    return fail(GMB_EINVAL, "num_layers=%d outside 1..%d", num_layers, GMB_MAX_LAYERS);
+  if (!fanouts) return fail(GMB_EINVAL, "fanouts is NULL");
+  if (num_nodes < 1 || num_nodes > kMaxInt32)
+    return fail(GMB_EINVAL, "num_nodes=%lld outside 1..2^31-1", static_cast<long long>(num_nodes));
+  if (num_seeds < 0) return fail(GMB_EINVAL, "num_seeds=%d < 0", num_seeds);
+  if (num_seeds > num_nodes)
+    return fail(GMB_EINVAL, "num_seeds=%d exceeds num_nodes (seeds must be distinct)", num_seeds);
+  for (int l = 0; l < num_layers; ++l)
+    if (fanouts[l] < 1) return fail(GMB_EINVAL, "fanouts[%d]=%d < 1", l, fanouts[l]);
+
+  SamplePlan p{};
+  p.num_layers = num_layers;
+  size_t off = 0;
+  int64_t cap_dst = num_seeds;
+  int64_t zero_words = 0;
+  for (int h = 0; h < num_layers; ++h) {
+    HopPlan& hp = p.hop[h];
+    hp.layer = num_layers - 1 - h;
+    hp.fanout = fanouts[hp.layer];
+    hp.cap_dst = cap_dst;
+    hp.cap_nnz = cap_dst * static_cast<int64_t>(hp.fanout);
+    hp.cap_src = cap_dst + std::min<int64_t>(hp.cap_nnz, num_nodes);
+    // every position (edge, source) and every edge tag must fit in 31 bits
+    if (hp.cap_nnz >= kMaxInt32 || hp.cap_src >= kMaxInt32)
+      return fail(GMB_EINVAL, "hop %d: capacity %lld edges / %lld sources exceeds 2^31-1", h,
+                  static_cast<long long>(hp.cap_nnz), static_cast<long long>(hp.cap_src));
+    hp.count_tiles_word = zero_words;
+    zero_words += gmb::scan_tiles(hp.cap_dst);
+    hp.count_ticket_word = zero_words++;
+    hp.flag_tiles_word = zero_words;
+    zero_words += gmb::scan_tiles(hp.cap_nnz);
+    hp.flag_ticket_word = zero_words++;
+    cap_dst = hp.cap_src;
+  }
+  p.cap_ids = p.hop[num_layers - 1].cap_src;
+  p.off_ids = off;
+  off = align_up(off + sizeof(int32_t) * std::max<int64_t>(p.cap_ids, 1));
+  p.off_sizes = off;
+  off = align_up(off + sizeof(int32_t) * 4 * num_layers);
+  p.off_zero = off;
+  p.num_zero_words = zero_words;
+  off = align_up(off + sizeof(uint64_t) * zero_words);
+  for (int h = 0; h < num_layers; ++h) {
+    HopPlan& hp = p.hop[h];
+    hp.off_indptr = off;
+    off = align_up(off + sizeof(int32_t) * (hp.cap_dst + 1));
+    hp.off_nbr = off;
+    off = align_up(off + sizeof(int32_t) * std::max<int64_t>(hp.cap_nnz, 1));
+    hp.off_local = off;
+    off = align_up(off + sizeof(int32_t) * std::max<int64_t>(hp.cap_nnz, 1));
+  }
+  p.total = off;
+  *plan = p;
+  return GMB_OK;
+}
+
+// ---- forward workspace plan --------------------------------------------
+
+struct ForwardPlan {
+  size_t off_agg;
+  size_t off_hidden[GMB_MAX_LAYERS];
+  size_t total;
+};
+
+int check_blocks(const gmb_blocks* b) {
+  if (!b) return fail(GMB_EINVAL, "blocks is NULL");
+  if (b->num_layers < 1 || b->num_layers > GMB_MAX_LAYERS)
+    return fail(GMB_EINVAL, "blocks->num_layers=%d outside 1..%d", b->num_layers, GMB_MAX_LAYERS);
+  for (int l = 0; l < b->num_layers; ++l) {
+    const gmb_block& k = b->blk[l];
+    if (!k.indptr || !k.indices || !k.src_ids || !k.sizes)
+      return fail(GMB_EINVAL, "block %d has a NULL array", l);
+    if (k.cap_dst < 0 || k.cap_src < k.cap_dst || k.cap_nnz < 0)
+      return fail(GMB_EINVAL, "block %d has inconsistent capacities", l);
+  }
+  return GMB_OK;
+}
+
+int plan_forward(const gmb_blocks* b, const gmb_sage_weights* w, ForwardPlan* plan) {
+  int st = check_blocks(b);
+  if (st != GMB_OK) return st;
+  if (!w) return fail(GMB_EINVAL, "weights is NULL");
+  if (w->num_layers != b->num_layers)
+    return fail(GMB_EINVAL, "weights have %d layers, blocks %d", w->num_layers, b->num_layers);
+  if (w->dtype != GMB_F32 && w->dtype != GMB_BF16) return fail(GMB_EINVAL, "dtype=%d unknown", w->dtype);
+  for (int l = 0; l <= w->num_layers; ++l)
+    if (w->dims[l] < 1 || w->dims[l] > 65536) return fail(GMB_EINVAL, "dims[%d]=%d outside 1..65536", l, w->dims[l]);
+  for (int l = 0; l < w->num_layers; ++l)
+    if (!w->w_self[l] || !w->w_neigh[l] || !w->bias[l]) return fail(GMB_EINVAL, "layer %d weight is NULL", l);
+  for (int l = 1; l < b->num_layers; ++l)
+    if (b->blk[l].cap_src != b->blk[l - 1].cap_dst)
+      return fail(GMB_EINVAL, "block %d sources (cap %lld) are not block %d destinations (cap %lld)", l,
+                  static_cast<long long>(b->blk[l].cap_src), l - 1,
+                  static_cast<long long>(b->blk[l - 1].cap_dst));
+  const size_t es = w->dtype == GMB_BF16 ? 2 : 4;
+  ForwardPlan p{};
+  size_t agg = 0;
+  for (int l = 0; l < w->num_layers; ++l)
+    agg = std::max(agg, static_cast<size_t>(std::max<int64_t>(b->blk[l].cap_dst, 1)) * w->dims[l] * es);
+  size_t off = 0;
+  p.off_agg = off;
+  off = align_up(off + agg);
+  for (int l = 0; l + 1 < w->num_layers; ++l) {
+    p.off_hidden[l] = off;
+    off = align_up(off + static_cast<size_t>(std::max<int64_t>(b->blk[l].cap_dst, 1)) * w->dims[l + 1] * es);
+  }
+  p.total = off;
+  *plan = p;
+  return GMB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t gmb_abi_version(void) { return GMB_ABI_VERSION; }
+
+const char* gmb_last_error(void) { return g_last_error.c_str(); }
+
+size_t gmb_sampler_state_bytes(int64_t num_nodes) {
+  if (num_nodes < 1 || num_nodes > kMaxInt32) return 0;
+  return kStateHeader + align_up(sizeof(uint32_t) * static_cast<size_t>(num_nodes));
+}
+
+uint32_t* gmb_state_status_word(void* state) { return static_cast<uint32_t*>(state); }
+
+int gmb_sampler_state_init(void* state, size_t state_bytes, int64_t num_nodes, void* stream) {
+  const size_t need = gmb_sampler_state_bytes(num_nodes);
+  if (need == 0) return fail(GMB_EINVAL, "num_nodes=%lld outside 1..2^31-1", static_cast<long long>(num_nodes));
+  if (!state) return fail(GMB_EINVAL, "state is NULL");
+  if (reinterpret_cast<uintptr_t>(state) % kAlign) return fail(GMB_EINVAL, "state is not 256-byte aligned");
+  if (state_bytes < need) return fail(GMB_ENOSPC, "state holds %zu bytes, %zu needed", state_bytes, need);
+  uint32_t* status = static_cast<uint32_t*>(state);
+  uint32_t* table = reinterpret_cast<uint32_t*>(static_cast<char*>(state) + kStateHeader);
+  hipError_t e = gmb::launch_state_init(table, status, num_nodes, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "state init launch");
+  return ok();
+}
+
+int gmb_read_status(void* state, void* stream) {
+  if (!state) return fail(GMB_EINVAL, "state is NULL");
+  uint32_t word = 0;
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+  e = hipMemcpy(&word, state, sizeof word, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "status read");
+  if (word != 0) {
+    e = hipMemset(state, 0, sizeof word);
+    if (e != hipSuccess) return hip_fail(e, "status clear");
+  }
+  if (word & GMB_STATUS_ERANGE) return fail(GMB_ERANGE, "a vertex id outside [0, num_nodes) was found on the device");
+  if (word & GMB_STATUS_EDUP) return fail(GMB_EDUP, "the seed list holds a vertex more than once");
+  return ok();
+}
+
+size_t gmb_sample_workspace_bytes(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
+                                  int64_t num_nodes) {
+  SamplePlan p;
+  if (plan_sampling(num_seeds, fanouts, num_layers, num_nodes, &p) != GMB_OK) return 0;
+  return p.total;
+}
+
+int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds,
+                      const int32_t* fanouts, int32_t num_layers, uint64_t seed, void* state,
+                      size_t state_bytes, void* ws, size_t ws_bytes, gmb_blocks* out, void* stream) {
+  if (!csr) return fail(GMB_EINVAL, "csr is NULL");
+  if (!out) return fail(GMB_EINVAL, "out is NULL");
+  if (!csr->indptr || (!csr->indices && csr->num_edges > 0))
+    return fail(GMB_EINVAL, "csr has a NULL array");
+  if (csr->indptr_bits != 32 && csr->indptr_bits != 64)
+    return fail(GMB_EINVAL, "indptr_bits=%d (32 or 64)", csr->indptr_bits);
+  if (csr->num_edges < 0 || (csr->indptr_bits == 32 && csr->num_edges > kMaxInt32))
+    return fail(GMB_EINVAL, "num_edges=%lld does not fit the row-offset type", static_cast<long long>(csr->num_edges));
+  if (num_seeds > 0 && !seeds) return fail(GMB_EINVAL, "seeds is NULL");
+  SamplePlan p;
+  int st = plan_sampling(num_seeds, fanouts, num_layers, csr->num_nodes, &p);
+  if (st != GMB_OK) return st;
+  if (!state) return fail(GMB_EINVAL, "state is NULL");
+  if (state_bytes < gmb_sampler_state_bytes(csr->num_nodes))
+    return fail(GMB_ENOSPC, "state holds %zu bytes, %zu needed", state_bytes, gmb_sampler_state_bytes(csr->num_nodes));
+  if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign || reinterpret_cast<uintptr_t>(state) % kAlign)
+    return fail(GMB_EINVAL, "workspace and state must be 256-byte aligned");
+  if (ws_bytes < p.total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p.total);
+
+  char* base = static_cast<char*>(ws);
+  int32_t* ids = reinterpret_cast<int32_t*>(base + p.off_ids);
+  int32_t* sizes = reinterpret_cast<int32_t*>(base + p.off_sizes);
+  uint64_t* zero = reinterpret_cast<uint64_t*>(base + p.off_zero);
+  uint32_t* status = static_cast<uint32_t*>(state);
+  uint32_t* table = reinterpret_cast<uint32_t*>(static_cast<char*>(state) + kStateHeader);
+  const hipStream_t s = as_stream(stream);
+
+  gmb::CsrArgs g{csr->indptr, csr->indices, csr->num_nodes, csr->indptr_bits == 64 ? 1 : 0};
+  gmb::HopArgs hops[GMB_MAX_LAYERS];
+  gmb_blocks res{};
+  res.num_layers = num_layers;
+  res.num_seeds = num_seeds;
+  for (int h = 0; h < num_layers; ++h) {
+    const HopPlan& hp = p.hop[h];
+    gmb::HopArgs& a = hops[h];
+    a.sizes = sizes + 4 * hp.layer;
+    a.next_sizes = (h + 1 < num_layers) ? sizes + 4 * p.hop[h + 1].layer : nullptr;
+    a.indptr = reinterpret_cast<int32_t*>(base + hp.off_indptr);
+    a.nbr = reinterpret_cast<int32_t*>(base + hp.off_nbr);
+    a.local = reinterpret_cast<int32_t*>(base + hp.off_local);
+    a.count_tiles = zero + hp.count_tiles_word;
+    a.count_ticket = reinterpret_cast<uint32_t*>(zero + hp.count_ticket_word);
+    a.flag_tiles = zero + hp.flag_tiles_word;
+    a.flag_ticket = reinterpret_cast<uint32_t*>(zero + hp.flag_ticket_word);
+    a.cap_dst = hp.cap_dst;
+    a.cap_nnz = hp.cap_nnz;
+    a.cap_src = hp.cap_src;
+    a.fanout = hp.fanout;
+    a.layer = hp.layer;
+    gmb_block& bk = res.blk[hp.layer];
+    bk.indptr = a.indptr;
+    bk.indices = a.local;
+    bk.nbr = a.nbr;
+    bk.src_ids = ids;
+    bk.sizes = a.sizes;
+    bk.cap_dst = hp.cap_dst;
+    bk.cap_src = hp.cap_src;
+    bk.cap_nnz = hp.cap_nnz;
+    bk.fanout = hp.fanout;
+    bk.layer = hp.layer;
+  }
+
+  const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
+  hipError_t e = gmb::launch_prep(seeds, num_seeds, ids, table, csr->num_nodes, status, zero,
+                                  p.num_zero_words, sizes, 4 * num_layers, 4 * (num_layers - 1) + 0, s);
+  if (e != hipSuccess) return hip_fail(e, "prep launch");
+  for (int h = 0; h < num_layers; ++h) {
+    e = gmb::launch_count_scan(g, ids, hops[h], status, s);
+    if (e != hipSuccess) return hip_fail(e, "degree scan launch");
+    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, s);
+    if (e != hipSuccess) return hip_fail(e, "sample launch");
+    e = gmb::launch_assign(hops[h], ids, table, csr->num_nodes, s);
+    if (e != hipSuccess) return hip_fail(e, "relabel launch");
+  }
+  e = gmb::launch_local(hops, num_layers, ids, num_seeds, table, csr->num_nodes, status, s);
+  if (e != hipSuccess) return hip_fail(e, "local-id launch");
+  e = gmb::launch_cleanup(ids, sizes + 4 * 0, p.cap_ids, table, csr->num_nodes, s);
+  if (e != hipSuccess) return hip_fail(e, "cleanup launch");
+  *out = res;
+  return ok();
+}
+
+int gmb_read_sizes(const gmb_blocks* blocks, int64_t* sizes, void* stream) {
+  int st = check_blocks(blocks);
+  if (st != GMB_OK) return st;
+  if (!sizes) return fail(GMB_EINVAL, "sizes is NULL");
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+  for (int l = 0; l < blocks->num_layers; ++l) {
+    int32_t w[4];
+    e = hipMemcpy(w, blocks->blk[l].sizes, sizeof w, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "size read");
+    sizes[3 * l + 0] = w[gmb::kNDst];
+    sizes[3 * l + 1] = w[gmb::kNSrc];
+    sizes[3 * l + 2] = w[gmb::kNnz];
+  }
+  return ok();
+}
+
+int gmb_gather_features(const int32_t* ids, const int32_t* n_dev, int64_t n_cap, const void* feats,
+                        int64_t num_nodes, int32_t dim, int32_t dtype, void* out, uint32_t* status,
+                        void* stream) {
+  if (n_cap < 0) return fail(GMB_EINVAL, "n_cap=%lld < 0", static_cast<long long>(n_cap));
+  if (dim < 1) return fail(GMB_EINVAL, "dim=%d < 1", dim);
+  if (dtype != GMB_F32 && dtype != GMB_BF16) return fail(GMB_EINVAL, "dtype=%d unknown", dtype);
+  if (num_nodes < 1 || num_nodes > kMaxInt32)
+    return fail(GMB_EINVAL, "num_nodes=%lld outside 1..2^31-1", static_cast<long long>(num_nodes));
+  if (n_cap == 0) return ok();
+  if (!ids || !feats || !out) return fail(GMB_EINVAL, "a NULL array");
+  const int64_t row_bytes = static_cast<int64_t>(dim) * (dtype == GMB_BF16 ? 2 : 4);
+  hipError_t e = gmb::launch_gather(ids, n_dev, n_cap, feats, num_nodes, row_bytes, out, status,
+                                    as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return ok();
+}
+
+size_t gmb_forward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights) {
+  ForwardPlan p;
+  if (plan_forward(blocks, weights, &p) != GMB_OK) return 0;
+  return p.total;
+}
+
+int64_t gmb_forward_hidden_offset(const gmb_blocks* blocks, const gmb_sage_weights* weights, int32_t layer) {
+  ForwardPlan p;
+  if (plan_forward(blocks, weights, &p) != GMB_OK) return -1;
+  if (layer < 0 || layer + 1 >= weights->num_layers) return -1;
+  return static_cast<int64_t>(p.off_hidden[layer]);
+}
+
+int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
+                     float* logits, void* ws, size_t ws_bytes, void* stream) {
+  ForwardPlan p;
+  int st = plan_forward(blocks, weights, &p);
+  if (st != GMB_OK) return st;
+  if (!x || !logits) return fail(GMB_EINVAL, "x or logits is NULL");
+  if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(GMB_EINVAL, "workspace is not 256-byte aligned");
+  if (ws_bytes < p.total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p.total);
+  const hipStream_t s = as_stream(stream);
+  const int L = weights->num_layers;
+  const int bf16 = weights->dtype == GMB_BF16;
+  char* base = static_cast<char*>(ws);
+  void* agg = base + p.off_agg;
+  const void* h_in = x;
+  for (int l = 0; l < L; ++l) {
+    const gmb_block& bk = blocks->blk[l];
+    const int d_in = weights->dims[l], d_out = weights->dims[l + 1];
+    const bool last = (l == L - 1);
+    void* h_out = last ? static_cast<void*>(logits) : static_cast<void*>(base + p.off_hidden[l]);
+    hipError_t e = gmb::launch_mean_aggregate(bk.sizes, bk.indptr, bk.indices, h_in, d_in, bf16, agg,
+                                              bk.cap_dst, s);
+    if (e != hipSuccess) return hip_fail(e, "mean-aggregation launch");
+    e = gmb::launch_sage_linear(bk.sizes, h_in, agg, weights->w_self[l], weights->w_neigh[l],
+                                weights->bias[l], d_in, d_out, bf16, last ? 0 : 1,
+                                (last || !bf16) ? 1 : 0, h_out, bk.cap_dst, s);
+    if (e != hipSuccess) return hip_fail(e, "linear launch");
+    h_in = h_out;
+  }
+  return ok();
+}
+
+}  // extern "C"

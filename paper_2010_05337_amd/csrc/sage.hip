@@ -1,0 +1,360 @@
+// GraphSAGE-mean layer on gfx950 (DistDGL Section II-A, Eq. (1), with the
+// message f = h_u, the aggregator = mean over the sampled in-neighbours and
+// the update g = act(h_v W_self + m_v W_neigh + b); Section IV model).
+//
+//   k_mean    m_v = (1/k_v) sum_e H[local[e]], fp32 accumulation; a group of
+//             G lanes per destination row, 16-byte chunks of the feature
+//             row per lane, four neighbour rows in flight per lane.
+//   k_linear  out = act([H_dst | M] [W_self; W_neigh] + b): one GEMM with
+//             K = 2 d_in on the matrix cores (v_mfma_f32_16x16x4_f32 for
+//             fp32, v_mfma_f32_16x16x32_bf16 for bf16 with fp32
+//             accumulation), 64x64 output tile per 256-thread workgroup,
+//             operands staged through LDS.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace gmb {
+
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// ---- mean aggregation -------------------------------------------------
+
+// VEC elements per lane access, from fp32 or bf16 (uint16_t bits) rows.
+template <int VEC>
+__device__ __forceinline__ void load_chunk(const float* p, float (&v)[VEC]) {
+  if constexpr (VEC == 4) {
+    const float4 x = *reinterpret_cast<const float4*>(p);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) v[i] = p[i];
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void load_chunk(const uint16_t* p, float (&v)[VEC]) {
+  if constexpr (VEC == 8) {
+    const uint4 x = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) v[i] = bf16_to_f32(p[i]);
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_chunk(float* p, const float (&v)[VEC]) {
+  if constexpr (VEC == 4) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) p[i] = v[i];
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_chunk(uint16_t* p, const float (&v)[VEC]) {
+  if constexpr (VEC == 8) {
+    uint4 x;
+    x.x = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+    x.y = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+    x.z = f32_to_bf16(v[4]) | (static_cast<uint32_t>(f32_to_bf16(v[5])) << 16);
+    x.w = f32_to_bf16(v[6]) | (static_cast<uint32_t>(f32_to_bf16(v[7])) << 16);
+    *reinterpret_cast<uint4*>(p) = x;
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) p[i] = f32_to_bf16(v[i]);
+  }
+}
+
+template <typename T, int VEC, int G>
+__global__ __launch_bounds__(256) void k_mean(const int32_t* sizes, const int32_t* __restrict__ indptr,
+                                              const int32_t* __restrict__ local,
+                                              const T* __restrict__ H, int d, T* __restrict__ M) {
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  const int64_t row = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
+  if (row >= n_dst) return;
+  const int lane = threadIdx.x & (G - 1);
+  const int32_t beg = indptr[row], end = indptr[row + 1];
+  const int32_t k = end - beg;
+  const int chunks = d / VEC;
+  for (int c = lane; c < chunks; c += G) {
+    float acc[VEC];
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+    // A negative local id only exists after a data error (vertex id out of
+    // range); it is read as row 0 so that every access stays in bounds.
+    int32_t e = beg;
+    for (; e + 4 <= end; e += 4) {
+      float x0[VEC], x1[VEC], x2[VEC], x3[VEC];
+      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e], 0)) * d + c * VEC, x0);
+      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e + 1], 0)) * d + c * VEC, x1);
+      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e + 2], 0)) * d + c * VEC, x2);
+      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e + 3], 0)) * d + c * VEC, x3);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc[i] += x0[i] + x1[i] + x2[i] + x3[i];
+    }
+    for (; e < end; ++e) {
+      float x0[VEC];
+      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e], 0)) * d + c * VEC, x0);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc[i] += x0[i];
+    }
+    if (k > 0) {
+      const float kf = static_cast<float>(k);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc[i] = acc[i] / kf;
+    }
+    store_chunk<VEC>(M + row * d + c * VEC, acc);
+  }
+}
+
+template <typename T, int VEC>
+hipError_t mean_dispatch(const int32_t* sizes, const int32_t* indptr, const int32_t* local, const void* h,
+                         int d, void* m, int64_t cap_dst, hipStream_t s) {
+  const int chunks = d / VEC;
+  int G = 64;
+  if (chunks <= 4) G = 4;
+  else if (chunks <= 8) G = 8;
+  else if (chunks <= 16) G = 16;
+  else if (chunks <= 32) G = 32;
+  int64_t blocks = (cap_dst * G + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+  const T* H = static_cast<const T*>(h);
+  T* M = static_cast<T*>(m);
+  switch (G) {
+    case 4: hipLaunchKernelGGL((k_mean<T, VEC, 4>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
+    case 8: hipLaunchKernelGGL((k_mean<T, VEC, 8>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
+    case 16: hipLaunchKernelGGL((k_mean<T, VEC, 16>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
+    case 32: hipLaunchKernelGGL((k_mean<T, VEC, 32>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
+    default: hipLaunchKernelGGL((k_mean<T, VEC, 64>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
+  }
+  return hipGetLastError();
+}
+
+// ---- linear layer on the matrix cores ---------------------------------
+
+constexpr int kBM = 64, kBN = 64;
+
+// fp32: v_mfma_f32_16x16x4_f32.  Lane l supplies A[l%16][l/16] and
+// B[l/16][l%16] of a 16x4 by 4x16 step and holds C[4*(l/16)+r][l%16],
+// r = 0..3.  Four waves tile the 64x64 output as 2x2 blocks of 32x32.
+constexpr int kBK32 = 32;
+constexpr int kAStride32 = kBK32 + 1;
+constexpr int kBStride32 = kBN + 16;
+
+__global__ __launch_bounds__(256) void k_linear_f32(const int32_t* sizes, const float* __restrict__ Hs,
+                                                    const float* __restrict__ Ag,
+                                                    const float* __restrict__ Ws,
+                                                    const float* __restrict__ Wn,
+                                                    const float* __restrict__ bias, int K, int N,
+                                                    int relu, float* __restrict__ out) {
+  __shared__ float As[kBM * kAStride32];
+  __shared__ float Bs[kBK32 * kBStride32];
+  const int32_t M = load_size(&sizes[kNDst]);
+  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN;
+  if (m0 >= M) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int K2 = 2 * K;
+  floatx4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = 0; k0 < K2; k0 += kBK32) {
+#pragma unroll
+    for (int q = 0; q < (kBM * kBK32) / 256; ++q) {
+      const int idx = tid + 256 * q;
+      const int r = idx / kBK32, c = idx % kBK32;
+      const int gm = m0 + r, gk = k0 + c;
+      float v = 0.f;
+      if (gm < M && gk < K2) v = gk < K ? Hs[static_cast<int64_t>(gm) * K + gk] : Ag[static_cast<int64_t>(gm) * K + (gk - K)];
+      As[r * kAStride32 + c] = v;
+    }
+#pragma unroll
+    for (int q = 0; q < (kBK32 * kBN) / 256; ++q) {
+      const int idx = tid + 256 * q;
+      const int r = idx / kBN, c = idx % kBN;
+      const int gk = k0 + r, gn = n0 + c;
+      float v = 0.f;
+      if (gk < K2 && gn < N) v = gk < K ? Ws[static_cast<int64_t>(gk) * N + gn] : Wn[static_cast<int64_t>(gk - K) * N + gn];
+      Bs[r * kBStride32 + c] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kBK32; kk += 4) {
+      float a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = As[(wm + i * 16 + (lane & 15)) * kAStride32 + kk + (lane >> 4)];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = Bs[(kk + (lane >> 4)) * kBStride32 + wn + j * 16 + (lane & 15)];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wn + j * 16 + (lane & 15);
+      if (col >= N) continue;
+      const float bv = bias[col];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = m0 + wm + i * 16 + 4 * (lane >> 4) + r;
+        if (row < M) {
+          float z = acc[i][j][r] + bv;
+          if (relu) z = z > 0.f ? z : 0.f;
+          out[static_cast<int64_t>(row) * N + col] = z;
+        }
+      }
+    }
+}
+
+// bf16: v_mfma_f32_16x16x32_bf16.  Lane l supplies A[l%16][8(l/16) .. +7]
+// and B[8(l/16) .. +7][l%16] and holds C as in the fp32 case.  B is kept
+// transposed in LDS so that a lane's eight k values are contiguous.
+constexpr int kBK16 = 64;
+constexpr int kAStride16 = kBK16 + 8;   // in bf16 elements; rows stay 16-byte aligned
+constexpr int kBStride16 = kBK16 + 8;
+
+__global__ __launch_bounds__(256) void k_linear_bf16(const int32_t* sizes, const uint16_t* __restrict__ Hs,
+                                                     const uint16_t* __restrict__ Ag,
+                                                     const uint16_t* __restrict__ Ws,
+                                                     const uint16_t* __restrict__ Wn,
+                                                     const float* __restrict__ bias, int K, int N,
+                                                     int relu, int out_f32, void* __restrict__ out) {
+  __shared__ __attribute__((aligned(16))) uint16_t As[kBM * kAStride16];
+  __shared__ __attribute__((aligned(16))) uint16_t Bt[kBN * kBStride16];
+  const int32_t M = load_size(&sizes[kNDst]);
+  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN;
+  if (m0 >= M) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int K2 = 2 * K;
+  floatx4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = 0; k0 < K2; k0 += kBK16) {
+#pragma unroll
+    for (int q = 0; q < (kBM * kBK16) / 256; ++q) {
+      const int idx = tid + 256 * q;
+      const int r = idx / kBK16, c = idx % kBK16;
+      const int gm = m0 + r, gk = k0 + c;
+      uint16_t v = 0;
+      if (gm < M && gk < K2) v = gk < K ? Hs[static_cast<int64_t>(gm) * K + gk] : Ag[static_cast<int64_t>(gm) * K + (gk - K)];
+      As[r * kAStride16 + c] = v;
+    }
+#pragma unroll
+    for (int q = 0; q < (kBK16 * kBN) / 256; ++q) {
+      const int idx = tid + 256 * q;
+      const int r = idx / kBN, c = idx % kBN;   // r: k within the tile, c: output column
+      const int gk = k0 + r, gn = n0 + c;
+      uint16_t v = 0;
+      if (gk < K2 && gn < N) v = gk < K ? Ws[static_cast<int64_t>(gk) * N + gn] : Wn[static_cast<int64_t>(gk - K) * N + gn];
+      Bt[c * kBStride16 + r] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kBK16; kk += 32) {
+      bf16x8 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        a[i] = *reinterpret_cast<const bf16x8*>(&As[(wm + i * 16 + (lane & 15)) * kAStride16 + kk + 8 * (lane >> 4)]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        b[j] = *reinterpret_cast<const bf16x8*>(&Bt[(wn + j * 16 + (lane & 15)) * kBStride16 + kk + 8 * (lane >> 4)]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wn + j * 16 + (lane & 15);
+      if (col >= N) continue;
+      const float bv = bias[col];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = m0 + wm + i * 16 + 4 * (lane >> 4) + r;
+        if (row < M) {
+          float z = acc[i][j][r] + bv;
+          if (relu) z = z > 0.f ? z : 0.f;
+          if (out_f32)
+            static_cast<float*>(out)[static_cast<int64_t>(row) * N + col] = z;
+          else
+            static_cast<uint16_t*>(out)[static_cast<int64_t>(row) * N + col] = f32_to_bf16(z);
+        }
+      }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_mean_aggregate(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
+                                 const void* h, int d, int bf16, void* agg, int64_t cap_dst,
+                                 hipStream_t s) {
+  const uintptr_t align = reinterpret_cast<uintptr_t>(h) | reinterpret_cast<uintptr_t>(agg);
+  if (bf16) {
+    if (d % 8 == 0 && align % 16 == 0) return mean_dispatch<uint16_t, 8>(sizes, indptr, local, h, d, agg, cap_dst, s);
+    return mean_dispatch<uint16_t, 1>(sizes, indptr, local, h, d, agg, cap_dst, s);
+  }
+  if (d % 4 == 0 && align % 16 == 0) return mean_dispatch<float, 4>(sizes, indptr, local, h, d, agg, cap_dst, s);
+  return mean_dispatch<float, 1>(sizes, indptr, local, h, d, agg, cap_dst, s);
+}
+
+hipError_t launch_sage_linear(const int32_t* sizes, const void* h_self, const void* agg,
+                              const void* w_self, const void* w_neigh, const float* bias, int d_in,
+                              int d_out, int bf16, int relu, int out_f32, void* out,
+                              int64_t cap_rows, hipStream_t s) {
+  int64_t gm = (cap_rows + kBM - 1) / kBM;
+  if (gm < 1) gm = 1;
+  const dim3 grid(static_cast<unsigned>(gm), static_cast<unsigned>((d_out + kBN - 1) / kBN)), block(256);
+  if (bf16) {
+    hipLaunchKernelGGL(k_linear_bf16, grid, block, 0, s, sizes, static_cast<const uint16_t*>(h_self),
+                       static_cast<const uint16_t*>(agg), static_cast<const uint16_t*>(w_self),
+                       static_cast<const uint16_t*>(w_neigh), bias, d_in, d_out, relu, out_f32, out);
+  } else {
+    if (!out_f32) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_linear_f32, grid, block, 0, s, sizes, static_cast<const float*>(h_self),
+                       static_cast<const float*>(agg), static_cast<const float*>(w_self),
+                       static_cast<const float*>(w_neigh), bias, d_in, d_out, relu,
+                       static_cast<float*>(out));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace gmb

@@ -1,0 +1,87 @@
+// Block-wide and single-pass device-wide exclusive scans (device side).
+//
+// The device-wide scan is a decoupled look-back scan (Merrill & Garland,
+// "Single-pass parallel prefix scan with decoupled look-back", NVIDIA
+// technical report NVR-2016-002): every tile publishes its aggregate at
+// once, then walks back over its predecessors until it meets one that has
+// published an inclusive prefix.  Tiles are numbered in the order in which
+// workgroups start (an atomic ticket), so a tile only ever waits on tiles
+// that are already running, and every tile publishes its aggregate before
+// it waits: every wait ends.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gmb {
+
+constexpr uint64_t kTileAggregate = 1ull << 62;
+constexpr uint64_t kTilePrefix = 2ull << 62;
+
+__device__ __forceinline__ int32_t wave_inclusive_scan(int32_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Exclusive scan of one value per thread over a block of BLOCK threads;
+// `smem` holds BLOCK/64 ints.  Every thread of the block must call it.
+template <int BLOCK>
+__device__ __forceinline__ int32_t block_exclusive_scan(int32_t x, int32_t& total, int32_t* smem) {
+  const int32_t inc = wave_inclusive_scan(x);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 63) smem[wave] = inc;
+  __syncthreads();
+  int32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < BLOCK / 64; ++w) {
+    const int32_t s = smem[w];
+    before += (w < wave) ? s : 0;
+    all += s;
+  }
+  __syncthreads();
+  total = all;
+  return before + inc - x;
+}
+
+__device__ __forceinline__ void publish_tile(uint64_t* tiles, int tile, uint64_t word) {
+  __hip_atomic_store(&tiles[tile], word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Called by one thread per tile.  Publishes the tile's aggregate, resolves
+// the exclusive prefix of the tile from its predecessors, publishes the
+// inclusive prefix and returns the exclusive one.  Values are non-negative
+// and below 2^31.
+__device__ int32_t tile_lookback(uint64_t* tiles, int tile, int32_t aggregate) {
+  if (tile == 0) {
+    publish_tile(tiles, 0, kTilePrefix | static_cast<uint32_t>(aggregate));
+    return 0;
+  }
+  publish_tile(tiles, tile, kTileAggregate | static_cast<uint32_t>(aggregate));
+  int32_t exclusive = 0;
+  for (int t = tile - 1;; --t) {
+    uint64_t w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while ((w >> 62) == 0) {
+      __builtin_amdgcn_s_sleep(1);
+      w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    exclusive += static_cast<int32_t>(static_cast<uint32_t>(w));
+    if ((w >> 62) == 2) break;
+  }
+  publish_tile(tiles, tile, kTilePrefix | static_cast<uint32_t>(exclusive + aggregate));
+  return exclusive;
+}
+
+// Claims the next tile number for this workgroup (thread 0 takes a ticket,
+// the block reads it from LDS).
+__device__ __forceinline__ int claim_tile(uint32_t* counter, int* s_tile) {
+  if (threadIdx.x == 0) *s_tile = static_cast<int>(atomicAdd(counter, 1u));
+  __syncthreads();
+  return *s_tile;
+}
+
+}  // namespace gmb

@@ -1,0 +1,212 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Sampling, relabelling and gather must match bit for bit; the GraphSAGE
+forward within a row-wise max relative error of 1e-4 (fp32 features) or
+2e-2 (bf16 features), on the logits and on every hidden layer.
+"""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU on this machine", allow_module_level=True)
+
+import paper_2010_05337_amd as gmb  # noqa: E402
+from gpu_util import (assert_blocks_equal, csr_on_device, gpu_blocks, rowwise_rel_err,  # noqa: E402
+                      tensor_bits, tensor_f64, to_torch_feats, to_torch_weights)
+
+TOL_F32, TOL_BF16 = 1e-4, 2e-2
+
+
+@pytest.fixture(scope="module")
+def tiny(dg):
+    return dg.er_directed(10000, 10.0, 101)
+
+
+def _star_graph():
+    class G:
+        pass
+    rows = {0: [], 1: [4, 5, 6], 2: [4, 5, 6, 7, 8], 3: list(range(4, 13))}
+    g = G()
+    g.num_nodes = 13
+    idx, ptr = [], [0]
+    for v in range(13):
+        idx += rows.get(v, [])
+        ptr.append(len(idx))
+    g.indptr = np.array(ptr, dtype=np.int64)
+    g.indices = np.array(idx, dtype=np.int32)
+    return g
+
+
+def test_library_is_the_hip_build():
+    L = gmb.lib()
+    assert L.gmb_abi_version() == 1
+    assert torch.cuda.get_device_properties(0).gcnArchName.startswith("gfx950")
+
+
+@pytest.mark.parametrize("fanouts", [[5, 5], [1], [3, 7, 2], [16, 16], [33, 9], [70]])
+def test_sampling_tiny_bitexact(orc, dg, tiny, fanouts):
+    print(f"tiny ER, fanouts={fanouts}", flush=True)
+    csr = csr_on_device(tiny)
+    seeds = dg.permutation(10000, 104)[:64]
+    _, host = gpu_blocks(csr, seeds, fanouts, 105)
+    ref = orc.sample_blocks(tiny.indptr, tiny.indices, seeds, fanouts, 105)
+    assert_blocks_equal(host, ref, f"fanouts {fanouts}")
+    csr.check_status()
+
+
+def test_sampling_degree_cases_and_empty(orc):
+    g = _star_graph()
+    csr = csr_on_device(g)
+    for seeds, fo in [([0, 1, 2, 3], [5]), ([3, 2, 1, 0], [5, 2]), ([], [5, 5]), ([0], [3])]:
+        _, host = gpu_blocks(csr, seeds, fo, 3)
+        ref = orc.sample_blocks(g.indptr, g.indices, seeds, fo, 3)
+        assert_blocks_equal(host, ref, f"seeds {seeds} fanouts {fo}")
+    csr.check_status()
+
+
+@pytest.mark.parametrize("wide", [False, True])
+def test_sampling_rmat_hubs_bitexact(orc, dg, wide):
+    """Hubs well above every fan-out, many tiles of the look-back scans, and
+    int32 / int64 row offsets."""
+    g = dg.rmat(16, 60000, 900000, (0.57, 0.19, 0.19), 7)
+    g = dg.inject_hubs(g, 5, 20000, 3)
+    print(f"rmat N={g.num_nodes} nnz={g.num_edges} max deg={g.degrees().max()} wide={wide}", flush=True)
+    csr = csr_on_device(g, wide=wide)
+    seeds = np.concatenate([g.hubs, dg.permutation(60000, 8)[:3000]]).astype(np.int64)
+    seeds = seeds[np.sort(np.unique(seeds, return_index=True)[1])]
+    for fo, key in [([15, 10, 5], 99), ([25, 10], 7)]:
+        _, host = gpu_blocks(csr, seeds, fo, key)
+        ref = orc.sample_blocks(g.indptr, g.indices, seeds, fo, key)
+        assert_blocks_equal(host, ref, f"fanouts {fo}")
+        assert ref[0].nnz > 2 * 2048   # several scan tiles
+    csr.check_status()
+
+
+def test_sampling_is_deterministic_and_keyed(dg, tiny):
+    csr = csr_on_device(tiny)
+    seeds = dg.permutation(10000, 5)[:500]
+    _, a = gpu_blocks(csr, seeds, [10, 10], 11)
+    _, b = gpu_blocks(csr, seeds, [10, 10], 11)
+    _, c = gpu_blocks(csr, seeds, [10, 10], 12)
+    for x, y in zip(a, b):
+        for k in x:
+            assert np.array_equal(x[k], y[k])
+    assert not np.array_equal(a[1]["nbr"], c[1]["nbr"])
+
+
+def test_state_is_clean_after_each_call(dg, tiny):
+    csr = csr_on_device(tiny)
+    seeds = dg.permutation(10000, 6)[:64]
+    gpu_blocks(csr, seeds, [5, 5], 1)
+    torch.cuda.synchronize()
+    table = csr.state[256:256 + 4 * csr.num_nodes].view(torch.int32)
+    assert bool((table == -1).all())
+
+
+def test_device_errors_are_reported(orc, dg, tiny):
+    csr = csr_on_device(tiny)
+    gpu_blocks(csr, [1, 2, 10000], [5], 1)
+    with pytest.raises(gmb.GmbError) as e:
+        csr.check_status()
+    assert e.value.code == -4
+    gpu_blocks(csr, [1, 2, 1], [5, 5], 1)
+    with pytest.raises(gmb.GmbError) as e:
+        csr.check_status()
+    assert e.value.code == -5
+    # the state is usable again afterwards
+    seeds = dg.permutation(10000, 9)[:64]
+    _, host = gpu_blocks(csr, seeds, [5, 5], 2)
+    assert_blocks_equal(host, orc.sample_blocks(tiny.indptr, tiny.indices, seeds, [5, 5], 2))
+    csr.check_status()
+
+
+def test_host_argument_errors(tiny):
+    csr = csr_on_device(tiny)
+    s = torch.arange(10, dtype=torch.int32, device="cuda")
+    with pytest.raises(gmb.GmbError) as e:
+        gmb.sample_blocks(csr, s, [5, 0], 1)
+    assert e.value.code == -1
+    small = torch.empty(256, dtype=torch.uint8, device="cuda")
+    need = gmb.sample_workspace_bytes(10, [5, 5], csr.num_nodes)
+    assert need > 256
+    # a too-small workspace is replaced by the binding; through the ABI it is ENOSPC
+    blocks = gmb.sample_blocks(csr, s, [5, 5], 1, workspace=small)
+    assert blocks.workspace.numel() >= need
+
+
+@pytest.mark.parametrize("dim,dtype", [(16, "f32"), (100, "f32"), (7, "f32"), (128, "bf16"),
+                                       (3, "bf16"), (256, "f32")])
+def test_gather_bitexact(orc, dg, tiny, dim, dtype):
+    feats = dg.features(10000, dim, 77, dtype)
+    ft = to_torch_feats(feats)
+    csr = csr_on_device(tiny)
+    seeds = dg.permutation(10000, 104)[:64]
+    blocks, host = gpu_blocks(csr, seeds, [5, 5], 105)
+    x = gmb.gather_features(blocks, ft)
+    n_in = host[0]["n_src"]
+    got = tensor_bits(x)[:n_in]
+    ref = orc.gather(feats, host[0]["src"])
+    assert got.view(np.uint8).tobytes() == ref.view(np.uint8).tobytes()
+    # explicit id list with a ragged count
+    ids = torch.from_numpy(dg.permutation(10000, 3)[:1001]).cuda()
+    y = gmb.gather_features(ids, ft, n=999)
+    assert np.array_equal(tensor_bits(y).view(np.uint8),
+                          orc.gather(feats, ids.cpu().numpy()[:999]).view(np.uint8))
+    csr.check_status()
+
+
+def _forward_case(orc, dg, g, feats, w, seeds, fanouts, key, tol):
+    csr = csr_on_device(g)
+    ft = to_torch_feats(feats)
+    wt = to_torch_weights(w)
+    blocks, host = gpu_blocks(csr, seeds, fanouts, key)
+    x = gmb.gather_features(blocks, ft)
+    logits, hidden = gmb.sage_forward(blocks, x, wt, return_hidden=True)
+    ref_blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, key)
+    assert_blocks_equal(host, ref_blocks)
+    X = orc.widen(orc.gather(feats, ref_blocks[0].src), w.dtype)
+    ws, wn, bs = w.as_f64()
+    ref_logits, ref_hidden = orc.sage_forward(ref_blocks, X, ws, wn, bs)
+    errs = [rowwise_rel_err(tensor_f64(h), r) for h, r in zip(hidden, ref_hidden[:-1])]
+    errs.append(rowwise_rel_err(tensor_f64(logits), ref_logits))
+    print(f"forward rel. errors per layer: {errs}", flush=True)
+    assert all(e <= tol for e in errs), errs
+    csr.check_status()
+    return errs
+
+
+@pytest.mark.parametrize("fanouts", [[5, 5], [2, 9]])
+def test_forward_tiny_f32(orc, dg, tiny, fanouts):
+    feats = dg.features(10000, 16, 102, "f32")
+    w = dg.sage_weights([16, 16, 8], 103)
+    seeds = dg.permutation(10000, 104)[:64]
+    _forward_case(orc, dg, tiny, feats, w, seeds, fanouts, 105, TOL_F32)
+
+
+def test_forward_ragged_dims_f32(orc, dg, tiny):
+    """Dims that are not multiples of the vector width or of the 64-wide
+    output tile, three layers."""
+    feats = dg.features(10000, 37, 1, "f32")
+    w = dg.sage_weights([37, 70, 65, 5], 2)
+    seeds = dg.permutation(10000, 3)[:200]
+    _forward_case(orc, dg, tiny, feats, w, seeds, [4, 3, 6], 4, TOL_F32)
+
+
+def test_forward_bf16(orc, dg, tiny):
+    feats = dg.features(10000, 128, 5, "bf16")
+    w = dg.sage_weights([128, 256, 47], 6, "bf16")
+    seeds = dg.permutation(10000, 7)[:300]
+    _forward_case(orc, dg, tiny, feats, w, seeds, [25, 10], 8, TOL_BF16)
+
+
+def test_forward_wide_model_f32(orc, dg):
+    """The paper's model shape (3 layers, hidden 256, fan-outs 15/10/5) on a
+    small power-law graph: many rows of the 64-row tiles, K = 200 and 512."""
+    g = dg.rmat(15, 30000, 300000, (0.57, 0.19, 0.19), 21)
+    feats = dg.features(30000, 100, 22, "f32")
+    w = dg.sage_weights([100, 256, 256, 47], 23)
+    seeds = dg.permutation(30000, 24)[:256]
+    _forward_case(orc, dg, g, feats, w, seeds, [15, 10, 5], 25, TOL_F32)
