@@ -1,0 +1,280 @@
+"""Throughput of the mini-batch GNN hot path on one MI355X.
+
+A step is one mini-batch through the whole path: sample_blocks (fan-out
+sampling + dedup/relabel into blocks), gather_features (input rows) and
+sage_forward (GraphSAGE-mean, 3 layers), all on one stream.  Default
+workload: the 2.4M-node power-law graph (shape of Table I's product graph),
+fp32 features of dim 100, model 100-256-256-47, fan-outs 15/10/5, batch 1000,
+one epoch over a random 8% training set (196 batches).
+
+Prints one JSON line.  value = seeds/s over the timed steps; sampled edges/s
+and gather GB/s ride along; `roofline` covers the dominant kernel, measured
+with HIP events on the stream the kernels run on; `cpu_baseline` times the
+CPU oracle on a bounded sample of the same batches (single thread).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=196)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="products2m")
+    ap.add_argument("--cpu-batches", type=int, default=4,
+                    help="batches the CPU oracle runs for the baseline (0 = skip)")
+    ap.add_argument("--no-stage-events", action="store_true",
+                    help="time the steps without per-stage events")
+    return ap.parse_args()
+
+
+def alg_sample_bytes(sizes, wide: bool) -> int:
+    """Algorithmic bytes of sampling + relabel for one batch: per hop, the
+    destination ids, their row-offset pairs, the sampled neighbour ids, the
+    block row offsets, the local ids and the source ids."""
+    w = 8 if wide else 4
+    total = 0
+    for n_dst, n_src, nnz in sizes:
+        total += 4 * n_dst + 2 * w * n_dst + 4 * nnz + 4 * (n_dst + 1) + 4 * nnz + 4 * n_src
+    return total
+
+
+def alg_gather_bytes(n_in: int, dim: int, es: int) -> int:
+    """Rows read + rows written + ids read."""
+    return n_in * (2 * dim * es + 4)
+
+
+def alg_forward_bytes(sizes, dims, es: int) -> int:
+    """Per layer: each source row read once, block CSR, mean rows written
+    and read, weight matrices, output rows."""
+    total = 0
+    for l, (n_dst, n_src, nnz) in enumerate(sizes):
+        d, o = dims[l], dims[l + 1]
+        total += n_src * d * es + 4 * nnz + 4 * (n_dst + 1) + 2 * n_dst * d * es
+        total += 2 * d * o * es + 4 * o + n_dst * o * (4 if l == len(sizes) - 1 else es)
+    return total
+
+
+def linear_flops(sizes, dims) -> int:
+    return sum(2 * n_dst * 2 * dims[l] * dims[l + 1] for l, (n_dst, _, _) in enumerate(sizes))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(the path has no multi-GPU sharding; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2010_05337_amd as gmb
+    from datagen.configs import CONFIGS, make_workload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    cfg = CONFIGS[args.workload]
+    t_gen = time.perf_counter()
+    wl = make_workload(args.workload)
+    t_gen = time.perf_counter() - t_gen
+    g = wl.graph
+    wide = g.num_edges > 0x7FFFFFFF
+    dev = torch.device("cuda:0")
+    ip = torch.from_numpy(g.indptr if wide else g.indptr.astype(np.int32)).to(dev)
+    ix = torch.from_numpy(g.indices).to(dev)
+    csr = gmb.CSRGraph(ip, ix)
+    bf16 = cfg.feat_dtype == "bf16"
+    es = 2 if bf16 else 4
+    if bf16:
+        feats = torch.from_numpy(wl.feats.view(np.int16)).to(dev).view(torch.bfloat16)
+    else:
+        feats = torch.from_numpy(wl.feats).to(dev)
+
+    def mat(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(a).to(dev)
+    w = wl.weights
+    weights = gmb.SageWeights([mat(a) for a in w.w_self], [mat(a) for a in w.w_neigh],
+                              [torch.from_numpy(b).to(dev) for b in w.bias])
+    fanouts = list(cfg.fanouts)
+    batches = [torch.from_numpy(b).to(dev) for b in wl.batches]
+    nb = len(batches)
+
+    # workspaces sized for a full batch, reused by every step
+    ws_sample = gmb._aligned_bytes(gmb.sample_workspace_bytes(cfg.batch, fanouts, g.num_nodes), dev)[1]
+    probe = gmb.sample_blocks(csr, batches[0], fanouts, wl.batch_key(0), workspace=ws_sample)
+    x_buf = torch.empty((probe.input_capacity, cfg.feat_dim), dtype=feats.dtype, device=dev)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1]
+    logits_buf = torch.empty((cfg.batch, cfg.dims[-1]), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    csr.check_status()
+
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        b = i % nb
+        if ev is not None:
+            ev[0].record(stream)
+        blocks = gmb.sample_blocks(csr, batches[b], fanouts, wl.batch_key(b), workspace=ws_sample)
+        if ev is not None:
+            ev[1].record(stream)
+        x = gmb.gather_features(blocks, feats, out=x_buf)
+        if ev is not None:
+            ev[2].record(stream)
+        lg = logits_buf[:batches[b].numel()]
+        gmb.sage_forward(blocks, x, weights, workspace=ws_fwd, logits=lg)
+        if ev is not None:
+            ev[3].record(stream)
+        return blocks
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = None if args.no_stage_events else [[torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                                             for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        step(i, evs[i] if evs else None)
+    torch.cuda.synchronize()
+    T = time.perf_counter() - t0
+    csr.check_status()
+
+    stage = {"sample": 0.0, "gather": 0.0, "forward": 0.0}
+    if evs:
+        for e in evs:
+            stage["sample"] += e[0].elapsed_time(e[1])
+            stage["gather"] += e[1].elapsed_time(e[2])
+            stage["forward"] += e[2].elapsed_time(e[3])
+
+    # sizes per batch (sampling is a pure function of the batch and its key)
+    seeds_total = edges_total = 0
+    b_sample = b_gather = b_fwd = flops = 0
+    for i in range(K):
+        b = i % nb
+        blocks = gmb.sample_blocks(csr, batches[b], fanouts, wl.batch_key(b), workspace=ws_sample)
+        sizes = blocks.sizes()
+        seeds_total += batches[b].numel()
+        edges_total += sum(s[2] for s in sizes)
+        b_sample += alg_sample_bytes(sizes, wide)
+        b_gather += alg_gather_bytes(sizes[0][1], cfg.feat_dim, es)
+        b_fwd += alg_forward_bytes(sizes, cfg.dims, es)
+        flops += linear_flops(sizes, cfg.dims)
+
+    seeds_per_s = seeds_total / T
+    res = {
+        "metric": "sampled edges/s + seeds/s (sample+gather+SAGE fwd); gather GB/s vs HBM peak",
+        "value": seeds_per_s,
+        "unit": "seeds/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * T / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {cfg.num_nodes}-node "
+                               f"{'R-MAT' if 'rmat' in cfg.graph else 'ER'} graph, {g.num_edges} edges, "
+                               f"feats {cfg.feat_dtype} x{cfg.feat_dim}, SAGE {'-'.join(map(str, cfg.dims))}, "
+                               f"fanouts {fanouts}, batch {cfg.batch}, {nb} batches per epoch",
+                   "batch": cfg.batch, "fanouts": fanouts, "num_nodes": cfg.num_nodes,
+                   "num_edges": g.num_edges, "dims": list(cfg.dims), "batches_per_epoch": nb},
+        "sampled_edges_per_s": edges_total / T,
+        "seeds": seeds_total,
+        "sampled_edges": edges_total,
+        "datagen_s": t_gen,
+    }
+    if evs:
+        ts, tg, tf = stage["sample"] / 1e3, stage["gather"] / 1e3, stage["forward"] / 1e3
+        res["stage_ms_per_step"] = {k: v / K for k, v in stage.items()}
+        res["gather_GBps"] = b_gather / tg / 1e9
+        res["sampling_edges_per_s"] = edges_total / ts
+        res["sample_gather_hbm"] = {"alg_bytes": b_sample + b_gather,
+                                    "GBps": (b_sample + b_gather) / (ts + tg) / 1e9,
+                                    "frac_of_peak": (b_sample + b_gather) / (ts + tg) / 1e9 / HBM_PEAK_GBPS}
+        peak = BF16_MFMA_PEAK_TFLOPS if bf16 else FP32_MFMA_PEAK_TFLOPS
+        res["forward"] = {"alg_bytes": b_fwd, "linear_flops": flops,
+                          "linear_TFLOPs_lower_bound": flops / tf / 1e12,
+                          "mfma_peak_TFLOPs": peak}
+        # dominant kernel of the path: the feature gather (one launch per step)
+        res["roofline"] = {"kernel": "k_gather", "bound": "hbm",
+                           "achieved": b_gather / tg / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                           "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": None,
+                           "alg_bytes_per_launch": b_gather / K,
+                           "avg_launch_ms": 1e3 * tg / K}
+
+    if args.cpu_batches > 0:
+        res["cpu_baseline"], res["parity"] = cpu_baseline(args, wl, csr, batches, fanouts, feats,
+                                                          weights, ws_sample, x_buf, ws_fwd)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(args, wl, csr, batches, fanouts, feats, weights, ws_sample, x_buf, ws_fwd):
+    """The oracle (plain C, fp64, one thread) on the first batches of the
+    same epoch, timed end to end; its results double as a parity check of
+    the GPU run on those batches."""
+    import torch
+    import oracle
+    import paper_2010_05337_amd as gmb
+    g, w, cfg = wl.graph, wl.weights, wl.cfg
+    ws64, wn64, b64 = w.as_f64()
+    n = min(args.cpu_batches, len(batches))
+    seeds_done = 0
+    t = 0.0
+    bitexact = True
+    max_err = 0.0
+    for b in range(n):
+        seeds_np = wl.batches[b]
+        key = wl.batch_key(b)
+        t0 = time.perf_counter()
+        ref = oracle.sample_blocks(g.indptr, g.indices, seeds_np, fanouts, key)
+        X = oracle.gather(wl.feats, ref[0].src)
+        logits, _ = oracle.sage_forward(ref, oracle.widen(X, cfg.feat_dtype), ws64, wn64, b64)
+        t += time.perf_counter() - t0
+        seeds_done += len(seeds_np)
+        # the GPU result of the same batch
+        blocks = gmb.sample_blocks(csr, batches[b], fanouts, key, workspace=ws_sample)
+        x = gmb.gather_features(blocks, feats, out=x_buf)
+        lg = gmb.sage_forward(blocks, x, weights, workspace=ws_fwd)
+        got = blocks.blocks()
+        for a, r in zip(got, ref):
+            bitexact &= (a.n_dst, a.n_src, a.nnz) == (r.n_dst, r.n_src, r.nnz)
+            bitexact &= bool(np.array_equal(a.nbr.cpu().numpy(), r.nbr))
+            bitexact &= bool(np.array_equal(a.indices.cpu().numpy(), r.local))
+            bitexact &= bool(np.array_equal(a.src_ids.cpu().numpy(), r.src))
+        xb = x[:ref[0].n_src]
+        xb = xb.view(torch.int16).cpu().numpy().view(np.uint16) if xb.dtype == torch.bfloat16 \
+            else xb.cpu().numpy()
+        bitexact &= xb.tobytes() == X.tobytes()
+        out = lg.float().cpu().numpy().astype(np.float64)
+        err = (np.abs(out - logits).max(axis=1) / np.maximum(np.abs(logits).max(axis=1), 1e-30)).max()
+        max_err = max(max_err, float(err))
+    base = {"value": seeds_done / t, "unit": "seeds/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} of {len(batches)} batches of the epoch ({seeds_done} seeds), "
+                      f"sample+gather+forward in fp64 plain C, {t:.1f} s"}
+    par = {"batches": n, "sample_relabel_gather_bitexact": bitexact, "logits_max_rel_err": max_err}
+    return base, par
+
+
+if __name__ == "__main__":
+    main()

@@ -13,6 +13,22 @@ namespace gmb {
 
 namespace {
 
+template <typename V>
+__device__ __forceinline__ void opaque_vec(V& x) {
+  static_assert(sizeof(V) % 4 == 0 || sizeof(V) == 2, "element size");
+  if constexpr (sizeof(V) == 16) {
+    asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+  } else if constexpr (sizeof(V) == 8) {
+    asm volatile("" : "+v"(x.x), "+v"(x.y));
+  } else {
+    asm volatile("" : "+v"(x));
+  }
+}
+
+// Every load is unconditional from a clamped address (row 0 for a lane
+// without a row, an out-of-range id reads row 0 and is zeroed after the
+// whole batch has been issued): a load under a divergent branch makes the
+// compiler drain every outstanding load before the next one.
 template <typename V, int G, int U>
 __global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ ids, const int32_t* n_dev,
                                                 int64_t n_cap, const V* __restrict__ feats,
@@ -26,30 +42,39 @@ __global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ ids,
   constexpr int kGroups = 256 / G;
   const int lane = threadIdx.x & (G - 1);
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kGroups;
+  bool bad = false;
   for (int64_t row = static_cast<int64_t>(blockIdx.x) * kGroups + threadIdx.x / G; row < n;
        row += stride * U) {
     int32_t id[U];
+    bool in[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t r = row + u * stride;
-      id[u] = r < n ? ids[r] : 0;
-      if (r < n && lane == 0 && !valid_vertex(id[u], num_nodes)) raise_status(status, GMB_STATUS_ERANGE);
+      id[u] = ids[r < n ? r : 0];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t r = row + u * stride;
+      const bool ok = valid_vertex(id[u], num_nodes);
+      bad |= (r < n) & !ok;
+      in[u] = (r < n) & ok;
+      id[u] = in[u] ? id[u] : 0;
     }
     for (int c = lane; c < cpr; c += G) {
       V val[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t r = row + u * stride;
-        val[u] = V{};
-        if (r < n && valid_vertex(id[u], num_nodes)) val[u] = feats[static_cast<int64_t>(id[u]) * cpr + c];
-      }
+      for (int u = 0; u < U; ++u) val[u] = feats[static_cast<int64_t>(id[u]) * cpr + c];
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
+        opaque_vec(val[u]);
         const int64_t r = row + u * stride;
-        if (r < n) out[r * cpr + c] = val[u];
+        if (r < n) out[r * cpr + c] = in[u] ? val[u] : V{};
       }
     }
   }
+  if (bad) raise_status(status, GMB_STATUS_ERANGE);
 }
 
 template <typename V>

@@ -32,6 +32,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
+// Makes a loaded value opaque to the optimiser, so that a later select on
+// it cannot turn the load itself into a conditional (branched) load.
+__device__ __forceinline__ void opaque(float& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void opaque(float4& x) {
+  asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+}
+
 // ---- mean aggregation -------------------------------------------------
 
 // VEC elements per lane access, from fp32 or bf16 (uint16_t bits) rows.
@@ -322,6 +329,166 @@ __global__ __launch_bounds__(256) void k_linear_bf16(const int32_t* sizes, const
     }
 }
 
+// fp32 with the weight slab resident in LDS.  A workgroup owns 64 output
+// columns and keeps those columns of [W_self; W_neigh] (all 2 d_in rows,
+// zero-padded to NCH chunks of 16) in LDS for its whole life, walking over
+// row tiles of 64 rows (persistent), so the weights are read once per
+// workgroup.  The slab is stored in MFMA operand order: for chunk c of k,
+// lane l (q = l/16) of a wave reads W[16c + 4q + s][col], s = 0..3, with one
+// 16-byte LDS read and feeds the four values to four consecutive
+// v_mfma_f32_16x16x4_f32 steps; its A operand is the matching float4
+// A[row][16c + 4q .. +3], one 16-byte global read.  The MFMA sums over its
+// four k slots, so any assignment of k to slots that A and B share gives
+// the same product.  Each wave computes 16 rows x 64 columns; it issues
+// all NCH A reads of its row tile before the first MFMA (at this LDS-bound
+// occupancy registers are plentiful), then runs the 16 NCH MFMAs.
+//
+// Loads are unconditional from clamped addresses: rows past M read row
+// M-1 and are never stored, k past 2 d_in reads the row's first elements
+// and meets zero rows of the slab.  (A load under a divergent branch makes
+// the compiler drain every outstanding load before the next one.)
+__device__ __forceinline__ const float* pick(bool c, const float* a, const float* b) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return reinterpret_cast<const float*>(c ? x : y);
+}
+
+template <int NCH>
+__global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
+                                                         const float* __restrict__ Hs,
+                                                         const float* __restrict__ Ag,
+                                                         const float* __restrict__ Ws,
+                                                         const float* __restrict__ Wn,
+                                                         const float* __restrict__ bias, int K,
+                                                         int N, int relu, int vec4,
+                                                         float* __restrict__ out) {
+  __shared__ __attribute__((aligned(16))) float Bp[NCH * 16 * 64];
+  const int32_t M = load_size(&sizes[kNDst]);
+  const int row_tiles = (M + 63) / 64;
+  if (static_cast<int>(blockIdx.x) >= row_tiles) return;
+  const int n0 = blockIdx.y * 64;
+  const int K2 = 2 * K;
+  auto slab_at = [&](int k, int n) -> float& {
+    return Bp[((((k >> 4) * 4 + ((k >> 2) & 3)) * 64) + n) * 4 + (k & 3)];
+  };
+  // Slab fill: a batch of independent loads per thread, made opaque only
+  // after the whole batch is issued, then the zero-padding select.
+  if (vec4) {   // N % 4 == 0 and 16-byte aligned weights: float4 along n
+    constexpr int total = NCH * 16 * 16;
+    for (int base = 0; base < total; base += 256 * 8) {
+      float4 v[8];
+      bool in[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int idx = base + u * 256 + threadIdx.x;
+        const int k = idx >> 4, n = (idx & 15) * 4;
+        in[u] = (idx < total) & (k < K2) & (n0 + n < N);
+        const int kr = in[u] ? (k < K ? k : k - K) : 0;
+        const float* src = pick(in[u] & (k >= K), Wn, Ws) + static_cast<int64_t>(kr) * N + (in[u] ? n0 + n : 0);
+        v[u] = *reinterpret_cast<const float4*>(src);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        opaque(v[u]);
+        const int idx = base + u * 256 + threadIdx.x;
+        if (idx < total) {
+          const int k = idx >> 4, n = (idx & 15) * 4;
+          const float4 x = in[u] ? v[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+          slab_at(k, n) = x.x;
+          slab_at(k, n + 1) = x.y;
+          slab_at(k, n + 2) = x.z;
+          slab_at(k, n + 3) = x.w;
+        }
+      }
+    }
+  } else {
+    constexpr int total = NCH * 16 * 64;
+    for (int base = 0; base < total; base += 256 * 16) {
+      float v[16];
+      bool in[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int idx = base + u * 256 + threadIdx.x;
+        const int k = idx >> 6, n = idx & 63;
+        in[u] = (idx < total) & (k < K2) & (n0 + n < N);
+        const int kr = in[u] ? (k < K ? k : k - K) : 0;
+        const float* src = pick(in[u] & (k >= K), Wn, Ws) + static_cast<int64_t>(kr) * N + (in[u] ? n0 + n : 0);
+        v[u] = *src;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        opaque(v[u]);
+        const int idx = base + u * 256 + threadIdx.x;
+        if (idx < total) slab_at(idx >> 6, idx & 63) = in[u] ? v[u] : 0.f;
+      }
+    }
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, r16 = lane & 15;
+  for (int rt = blockIdx.x; rt < row_tiles; rt += gridDim.x) {
+    const int row = rt * 64 + wave * 16 + r16;
+    const int64_t arow = row < M ? row : M - 1;
+    const float* hrow = Hs + arow * K;
+    const float* grow = Ag + arow * K;
+    float4 a[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int k = c * 16 + 4 * q;
+      const int kk = k >= K2 ? 0 : (k < K ? k : k - K);
+      a[c] = *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
+    }
+    // keep the scheduler from sinking each read next to its first use
+    __builtin_amdgcn_sched_barrier(0);
+    floatx4 acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      float4 b[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        b[j] = *reinterpret_cast<const float4*>(&Bp[(((c * 4 + q) * 64) + j * 16 + r16) * 4]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].x, b[j].x, acc[j], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].y, b[j].y, acc[j], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].z, b[j].z, acc[j], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].w, b[j].w, acc[j], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = n0 + j * 16 + r16;
+      const float bv = bias[col < N ? col : N - 1];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int orow = rt * 64 + wave * 16 + 4 * q + r;
+        float z = acc[j][r] + bv;
+        if (relu) z = z > 0.f ? z : 0.f;
+        if (orow < M && col < N) out[static_cast<int64_t>(orow) * N + col] = z;
+      }
+    }
+  }
+}
+
+template <int NCH>
+void launch_slab(const int32_t* sizes, const float* hs, const float* ag, const float* ws, const float* wn,
+                 const float* bias, int K, int N, int relu, float* out, int64_t cap_rows, hipStream_t s) {
+  // LDS bounds the workgroups per CU; size the persistent grid to fill the
+  // 256 CUs about twice over.
+  constexpr int per_cu = (160 * 1024) / (NCH * 16 * 64 * 4);
+  const int col_tiles = (N + 63) / 64;
+  int64_t rows = (cap_rows + 63) / 64;
+  int64_t want = (2 * 256 * (per_cu < 1 ? 1 : per_cu) + col_tiles - 1) / col_tiles;
+  if (rows > want) rows = want;
+  if (rows < 1) rows = 1;
+  const uintptr_t walign = reinterpret_cast<uintptr_t>(ws) | reinterpret_cast<uintptr_t>(wn);
+  const int vec4 = (N % 4 == 0 && walign % 16 == 0) ? 1 : 0;
+  hipLaunchKernelGGL(k_linear_f32_slab<NCH>, dim3(static_cast<unsigned>(rows), col_tiles), dim3(256), 0,
+                     s, sizes, hs, ag, ws, wn, bias, K, N, relu, vec4, out);
+}
+
 }  // namespace
 
 hipError_t launch_mean_aggregate(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
@@ -349,6 +516,26 @@ hipError_t launch_sage_linear(const int32_t* sizes, const void* h_self, const vo
                        static_cast<const uint16_t*>(w_neigh), bias, d_in, d_out, relu, out_f32, out);
   } else {
     if (!out_f32) return hipErrorInvalidValue;
+    const float* hs = static_cast<const float*>(h_self);
+    const float* ag = static_cast<const float*>(agg);
+    const float* ws = static_cast<const float*>(w_self);
+    const float* wn = static_cast<const float*>(w_neigh);
+    const uintptr_t align = reinterpret_cast<uintptr_t>(hs) | reinterpret_cast<uintptr_t>(ag);
+    const int nch = (2 * d_in + 15) / 16;
+    if (d_in % 4 == 0 && align % 16 == 0 && nch <= 40) {
+      float* o = static_cast<float*>(out);
+#define GMB_SLAB(C) launch_slab<C>(sizes, hs, ag, ws, wn, bias, d_in, d_out, relu, o, cap_rows, s)
+      if (nch <= 2) GMB_SLAB(2);
+      else if (nch <= 4) GMB_SLAB(4);
+      else if (nch <= 8) GMB_SLAB(8);
+      else if (nch <= 13) GMB_SLAB(13);
+      else if (nch <= 16) GMB_SLAB(16);
+      else if (nch <= 24) GMB_SLAB(24);
+      else if (nch <= 32) GMB_SLAB(32);
+      else GMB_SLAB(40);
+#undef GMB_SLAB
+      return hipGetLastError();
+    }
     hipLaunchKernelGGL(k_linear_f32, grid, block, 0, s, sizes, static_cast<const float*>(h_self),
                        static_cast<const float*>(agg), static_cast<const float*>(w_self),
                        static_cast<const float*>(w_neigh), bias, d_in, d_out, relu,
