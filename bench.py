@@ -2,7 +2,10 @@
 
 A step is one mini-batch through the whole path: sample_blocks (fan-out
 sampling + dedup/relabel into blocks), gather_features (input rows) and
-sage_forward (GraphSAGE-mean, 3 layers), all on one stream.  Default
+sage_forward (GraphSAGE-mean, 3 layers), in order on one stream.  Like the
+paper's sampling workers that overlap mini-batch production with training
+(Section III-D), consecutive batches run on --streams streams (default 4),
+each with its own sampler state and workspaces.  Default
 workload: the 2.4M-node power-law graph (shape of Table I's product graph),
 fp32 features of dim 100, model 100-256-256-47, fan-outs 15/10/5, batch 1000,
 one epoch over a random 8% training set (196 batches).
@@ -40,6 +43,9 @@ def parse():
                     help="batches the CPU oracle runs for the baseline (0 = skip)")
     ap.add_argument("--no-stage-events", action="store_true",
                     help="time the steps without per-stage events")
+    ap.add_argument("--streams", type=int, default=4,
+                    help="mini-batches in flight: batch i runs on stream i %% streams, each stream "
+                         "with its own sampler state and workspaces")
     return ap.parse_args()
 
 
@@ -116,31 +122,43 @@ def main():
     batches = [torch.from_numpy(b).to(dev) for b in wl.batches]
     nb = len(batches)
 
-    # workspaces sized for a full batch, reused by every step
-    ws_sample = gmb._aligned_bytes(gmb.sample_workspace_bytes(cfg.batch, fanouts, g.num_nodes), dev)[1]
-    probe = gmb.sample_blocks(csr, batches[0], fanouts, wl.batch_key(0), workspace=ws_sample)
-    x_buf = torch.empty((probe.input_capacity, cfg.feat_dim), dtype=feats.dtype, device=dev)
-    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1]
-    logits_buf = torch.empty((cfg.batch, cfg.dims[-1]), dtype=torch.float32, device=dev)
+    # one set of buffers per stream, sized for a full batch and reused by
+    # every step that runs on that stream
+    S = max(1, args.streams)
+    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(S - 1)]
+    lanes = []
+    for k in range(S):
+        c = csr if k == 0 else gmb.CSRGraph(ip, ix)
+        ws_s = gmb._aligned_bytes(gmb.sample_workspace_bytes(cfg.batch, fanouts, g.num_nodes), dev)[1]
+        probe = gmb.sample_blocks(c, batches[0], fanouts, wl.batch_key(0), workspace=ws_s)
+        lanes.append(dict(
+            csr=c, ws_sample=ws_s,
+            x=torch.empty((probe.input_capacity, cfg.feat_dim), dtype=feats.dtype, device=dev),
+            ws_fwd=gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1],
+            logits=torch.empty((cfg.batch, cfg.dims[-1]), dtype=torch.float32, device=dev)))
     torch.cuda.synchronize()
-    csr.check_status()
-
-    stream = torch.cuda.current_stream()
+    for ln in lanes:
+        ln["csr"].check_status()
+    ws_sample, x_buf, ws_fwd = lanes[0]["ws_sample"], lanes[0]["x"], lanes[0]["ws_fwd"]
 
     def step(i, ev=None):
         b = i % nb
-        if ev is not None:
-            ev[0].record(stream)
-        blocks = gmb.sample_blocks(csr, batches[b], fanouts, wl.batch_key(b), workspace=ws_sample)
-        if ev is not None:
-            ev[1].record(stream)
-        x = gmb.gather_features(blocks, feats, out=x_buf)
-        if ev is not None:
-            ev[2].record(stream)
-        lg = logits_buf[:batches[b].numel()]
-        gmb.sage_forward(blocks, x, weights, workspace=ws_fwd, logits=lg)
-        if ev is not None:
-            ev[3].record(stream)
+        ln = lanes[i % S]
+        st = streams[i % S]
+        with torch.cuda.stream(st):
+            if ev is not None:
+                ev[0].record(st)
+            blocks = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b),
+                                       workspace=ln["ws_sample"])
+            if ev is not None:
+                ev[1].record(st)
+            x = gmb.gather_features(blocks, feats, out=ln["x"])
+            if ev is not None:
+                ev[2].record(st)
+            gmb.sage_forward(blocks, x, weights, workspace=ln["ws_fwd"],
+                             logits=ln["logits"][:batches[b].numel()])
+            if ev is not None:
+                ev[3].record(st)
         return blocks
 
     for i in range(args.warmup):
@@ -156,7 +174,8 @@ def main():
         step(i, evs[i] if evs else None)
     torch.cuda.synchronize()
     T = time.perf_counter() - t0
-    csr.check_status()
+    for ln in lanes:
+        ln["csr"].check_status()
 
     stage = {"sample": 0.0, "gather": 0.0, "forward": 0.0}
     if evs:
@@ -200,12 +219,15 @@ def main():
                    "batch": cfg.batch, "fanouts": fanouts, "num_nodes": cfg.num_nodes,
                    "num_edges": g.num_edges, "dims": list(cfg.dims), "batches_per_epoch": nb},
         "sampled_edges_per_s": edges_total / T,
+        "streams": S,
         "seeds": seeds_total,
         "sampled_edges": edges_total,
         "datagen_s": t_gen,
     }
     if evs:
         ts, tg, tf = stage["sample"] / 1e3, stage["gather"] / 1e3, stage["forward"] / 1e3
+        # with several streams the stage intervals of different batches overlap,
+        # so these are per-batch latencies, not shares of the wall time
         res["stage_ms_per_step"] = {k: v / K for k, v in stage.items()}
         res["gather_GBps"] = b_gather / tg / 1e9
         res["sampling_edges_per_s"] = edges_total / ts
