@@ -41,8 +41,10 @@ def parse():
     ap.add_argument("--workload", default="products2m")
     ap.add_argument("--cpu-batches", type=int, default=4,
                     help="batches the CPU oracle runs for the baseline (0 = skip)")
-    ap.add_argument("--no-stage-events", action="store_true",
-                    help="time the steps without per-stage events")
+    ap.add_argument("--summarize-profile", metavar="PREFIX",
+                    help="print a markdown summary of a rocprofv3 CSV run of this script "
+                         "(PREFIX_kernel_stats.csv, PREFIX_kernel_trace.csv) and exit; --steps "
+                         "and --warmup must match that run")
     ap.add_argument("--streams", type=int, default=4,
                     help="mini-batches in flight: batch i runs on stream i %% streams, each stream "
                          "with its own sampler state and workspaces")
@@ -80,8 +82,37 @@ def linear_flops(sizes, dims) -> int:
     return sum(2 * n_dst * 2 * dims[l] * dims[l + 1] for l, (n_dst, _, _) in enumerate(sizes))
 
 
+def summarize_profile(args):
+    """Markdown summary of `rocprofv3 --kernel-trace --stats --output-format
+    csv -- python bench.py ...`: the per-kernel statistics of the whole run,
+    and the gather kernel's average over the launches of pass B (isolated,
+    one stream), which is what `roofline.avg_launch_ms` measures."""
+    import csv
+    pre = args.summarize_profile
+    stats = list(csv.DictReader(open(pre + "_kernel_stats.csv")))
+    trace = list(csv.DictReader(open(pre + "_kernel_trace.csv")))
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    out = ["| kernel | calls | avg us | min us | max us | share % |", "|---|---:|---:|---:|---:|---:|"]
+    for r in stats:
+        name = r["Name"].replace("gmb::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        out.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                   f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                   f"{float(r['Percentage']):.1f} |")
+    g = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace if "k_gather" in r["Kernel_Name"]]
+    lo, hi = args.warmup + args.steps, args.warmup + 2 * args.steps
+    sel = g[lo:hi]
+    out.append("")
+    out.append(f"k_gather launches in the run: {len(g)}; pass B (isolated, launches {lo}..{hi - 1}): "
+               f"{len(sel)} launches, average {sum(sel) / max(len(sel), 1) / 1e3:.2f} us, "
+               f"min {min(sel) / 1e3:.2f} us, max {max(sel) / 1e3:.2f} us" if sel else "no pass-B launches")
+    print("\n".join(out))
+
+
 def main():
     args = parse()
+    if args.summarize_profile:
+        summarize_profile(args)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
               "(the path has no multi-GPU sharding; see the design notes).", file=sys.stderr)
@@ -141,10 +172,10 @@ def main():
         ln["csr"].check_status()
     ws_sample, x_buf, ws_fwd = lanes[0]["ws_sample"], lanes[0]["x"], lanes[0]["ws_fwd"]
 
-    def step(i, ev=None):
+    def step(i, nstreams, ev=None):
         b = i % nb
-        ln = lanes[i % S]
-        st = streams[i % S]
+        ln = lanes[i % nstreams]
+        st = streams[i % nstreams]
         with torch.cuda.stream(st):
             if ev is not None:
                 ev[0].record(st)
@@ -162,27 +193,35 @@ def main():
         return blocks
 
     for i in range(args.warmup):
-        step(i)
+        step(i, S)
     torch.cuda.synchronize()
 
+    # pass A (the headline): K steps, S streams in flight, no events
     K = args.steps
-    evs = None if args.no_stage_events else [[torch.cuda.Event(enable_timing=True) for _ in range(4)]
-                                             for _ in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
-        step(i, evs[i] if evs else None)
+        step(i, S)
     torch.cuda.synchronize()
     T = time.perf_counter() - t0
     for ln in lanes:
         ln["csr"].check_status()
 
+    # pass B (isolated launches): the same K steps on one stream with HIP
+    # events around every stage, for per-stage times and the roofline
     stage = {"sample": 0.0, "gather": 0.0, "forward": 0.0}
-    if evs:
-        for e in evs:
-            stage["sample"] += e[0].elapsed_time(e[1])
-            stage["gather"] += e[1].elapsed_time(e[2])
-            stage["forward"] += e[2].elapsed_time(e[3])
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(K):
+        step(i, 1, evs[i])
+    torch.cuda.synchronize()
+    T1 = time.perf_counter() - t1
+    csr.check_status()
+    for e in evs:
+        stage["sample"] += e[0].elapsed_time(e[1])
+        stage["gather"] += e[1].elapsed_time(e[2])
+        stage["forward"] += e[2].elapsed_time(e[3])
 
     # sizes per batch (sampling is a pure function of the batch and its key)
     seeds_total = edges_total = 0
@@ -224,26 +263,24 @@ def main():
         "sampled_edges": edges_total,
         "datagen_s": t_gen,
     }
-    if evs:
-        ts, tg, tf = stage["sample"] / 1e3, stage["gather"] / 1e3, stage["forward"] / 1e3
-        # with several streams the stage intervals of different batches overlap,
-        # so these are per-batch latencies, not shares of the wall time
-        res["stage_ms_per_step"] = {k: v / K for k, v in stage.items()}
-        res["gather_GBps"] = b_gather / tg / 1e9
-        res["sampling_edges_per_s"] = edges_total / ts
-        res["sample_gather_hbm"] = {"alg_bytes": b_sample + b_gather,
-                                    "GBps": (b_sample + b_gather) / (ts + tg) / 1e9,
-                                    "frac_of_peak": (b_sample + b_gather) / (ts + tg) / 1e9 / HBM_PEAK_GBPS}
-        peak = BF16_MFMA_PEAK_TFLOPS if bf16 else FP32_MFMA_PEAK_TFLOPS
-        res["forward"] = {"alg_bytes": b_fwd, "linear_flops": flops,
-                          "linear_TFLOPs_lower_bound": flops / tf / 1e12,
-                          "mfma_peak_TFLOPs": peak}
-        # dominant kernel of the path: the feature gather (one launch per step)
-        res["roofline"] = {"kernel": "k_gather", "bound": "hbm",
-                           "achieved": b_gather / tg / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                           "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": None,
-                           "alg_bytes_per_launch": b_gather / K,
-                           "avg_launch_ms": 1e3 * tg / K}
+    ts, tg, tf = stage["sample"] / 1e3, stage["gather"] / 1e3, stage["forward"] / 1e3
+    res["single_stream"] = {"seeds_per_s": seeds_total / T1, "ms_per_step": 1e3 * T1 / K,
+                            "stage_ms_per_step": {k: v / K for k, v in stage.items()}}
+    res["gather_GBps"] = b_gather / tg / 1e9
+    res["sampling_edges_per_s"] = edges_total / ts
+    res["sample_gather_hbm"] = {"alg_bytes": b_sample + b_gather,
+                                "GBps": (b_sample + b_gather) / (ts + tg) / 1e9,
+                                "frac_of_peak": (b_sample + b_gather) / (ts + tg) / 1e9 / HBM_PEAK_GBPS}
+    peak = BF16_MFMA_PEAK_TFLOPS if bf16 else FP32_MFMA_PEAK_TFLOPS
+    res["forward"] = {"alg_bytes": b_fwd, "linear_flops": flops,
+                      "linear_TFLOPs_lower_bound": flops / tf / 1e12, "mfma_peak_TFLOPs": peak}
+    # dominant kernel of the path: the feature gather, one launch per step,
+    # timed in the isolated pass (launches W+K .. W+2K-1 of the run)
+    res["roofline"] = {"kernel": "k_gather", "bound": "hbm",
+                       "achieved": b_gather / tg / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                       "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": None,
+                       "alg_bytes_per_launch": b_gather / K, "avg_launch_ms": 1e3 * tg / K,
+                       "launches": f"{args.warmup + K}..{args.warmup + 2 * K - 1} (pass B)"}
 
     if args.cpu_batches > 0:
         res["cpu_baseline"], res["parity"] = cpu_baseline(args, wl, csr, batches, fanouts, feats,

@@ -352,7 +352,12 @@ __device__ __forceinline__ const float* pick(bool c, const float* a, const float
   return reinterpret_cast<const float*>(c ? x : y);
 }
 
-template <int NCH>
+// NCH chunks of 16 k, J column subtiles of 16 (BN = 16 J columns per
+// workgroup), SPLIT = 1: each wave owns 16 rows of a 64-row tile and all
+// chunks; SPLIT = 4: the four waves share one 16-row tile, wave w takes the
+// chunks c = w (mod 4), and the partial sums meet in LDS (for layers with
+// few rows, where one wave per 16 rows would leave most SIMDs idle).
+template <int NCH, int J, int SPLIT>
 __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
                                                          const float* __restrict__ Hs,
                                                          const float* __restrict__ Ag,
@@ -361,26 +366,31 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
                                                          const float* __restrict__ bias, int K,
                                                          int N, int relu, int vec4,
                                                          float* __restrict__ out) {
-  __shared__ __attribute__((aligned(16))) float Bp[NCH * 16 * 64];
+  constexpr int BN = 16 * J;
+  constexpr int ROWS = SPLIT > 1 ? 16 : 64;
+  constexpr int MYCH = SPLIT > 1 ? (NCH + 3) / 4 : NCH;
+  __shared__ __attribute__((aligned(16))) float Bp[NCH * 16 * BN];
+  __shared__ __attribute__((aligned(16))) float Red[SPLIT > 1 ? 4 * J * 64 * 4 : 4];
   const int32_t M = load_size(&sizes[kNDst]);
-  const int row_tiles = (M + 63) / 64;
+  const int row_tiles = (M + ROWS - 1) / ROWS;
   if (static_cast<int>(blockIdx.x) >= row_tiles) return;
-  const int n0 = blockIdx.y * 64;
+  const int n0 = blockIdx.y * BN;
   const int K2 = 2 * K;
   auto slab_at = [&](int k, int n) -> float& {
-    return Bp[((((k >> 4) * 4 + ((k >> 2) & 3)) * 64) + n) * 4 + (k & 3)];
+    return Bp[((((k >> 4) * 4 + ((k >> 2) & 3)) * BN) + n) * 4 + (k & 3)];
   };
   // Slab fill: a batch of independent loads per thread, made opaque only
   // after the whole batch is issued, then the zero-padding select.
   if (vec4) {   // N % 4 == 0 and 16-byte aligned weights: float4 along n
-    constexpr int total = NCH * 16 * 16;
+    constexpr int per_row = BN / 4;
+    constexpr int total = NCH * 16 * per_row;
     for (int base = 0; base < total; base += 256 * 8) {
       float4 v[8];
       bool in[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int idx = base + u * 256 + threadIdx.x;
-        const int k = idx >> 4, n = (idx & 15) * 4;
+        const int k = idx / per_row, n = (idx % per_row) * 4;
         in[u] = (idx < total) & (k < K2) & (n0 + n < N);
         const int kr = in[u] ? (k < K ? k : k - K) : 0;
         const float* src = pick(in[u] & (k >= K), Wn, Ws) + static_cast<int64_t>(kr) * N + (in[u] ? n0 + n : 0);
@@ -391,7 +401,7 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
         opaque(v[u]);
         const int idx = base + u * 256 + threadIdx.x;
         if (idx < total) {
-          const int k = idx >> 4, n = (idx & 15) * 4;
+          const int k = idx / per_row, n = (idx % per_row) * 4;
           const float4 x = in[u] ? v[u] : make_float4(0.f, 0.f, 0.f, 0.f);
           slab_at(k, n) = x.x;
           slab_at(k, n + 1) = x.y;
@@ -401,24 +411,24 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
       }
     }
   } else {
-    constexpr int total = NCH * 16 * 64;
-    for (int base = 0; base < total; base += 256 * 16) {
-      float v[16];
-      bool in[16];
+    constexpr int total = NCH * 16 * BN;
+    for (int base = 0; base < total; base += 256 * 32) {
+      float v[32];
+      bool in[32];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
+      for (int u = 0; u < 32; ++u) {
         const int idx = base + u * 256 + threadIdx.x;
-        const int k = idx >> 6, n = idx & 63;
+        const int k = idx / BN, n = idx % BN;
         in[u] = (idx < total) & (k < K2) & (n0 + n < N);
         const int kr = in[u] ? (k < K ? k : k - K) : 0;
         const float* src = pick(in[u] & (k >= K), Wn, Ws) + static_cast<int64_t>(kr) * N + (in[u] ? n0 + n : 0);
         v[u] = *src;
       }
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
+      for (int u = 0; u < 32; ++u) {
         opaque(v[u]);
         const int idx = base + u * 256 + threadIdx.x;
-        if (idx < total) slab_at(idx >> 6, idx & 63) = in[u] ? v[u] : 0.f;
+        if (idx < total) slab_at(idx / BN, idx % BN) = in[u] ? v[u] : 0.f;
       }
     }
   }
@@ -426,67 +436,113 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, r16 = lane & 15;
   for (int rt = blockIdx.x; rt < row_tiles; rt += gridDim.x) {
-    const int row = rt * 64 + wave * 16 + r16;
+    const int row = SPLIT > 1 ? rt * 16 + r16 : rt * 64 + wave * 16 + r16;
     const int64_t arow = row < M ? row : M - 1;
     const float* hrow = Hs + arow * K;
     const float* grow = Ag + arow * K;
-    float4 a[NCH];
+    float4 a[MYCH];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
+    for (int i = 0; i < MYCH; ++i) {
+      const int c = SPLIT > 1 ? wave + 4 * i : i;
       const int k = c * 16 + 4 * q;
       const int kk = k >= K2 ? 0 : (k < K ? k : k - K);
-      a[c] = *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
+      a[i] = *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
     }
     // keep the scheduler from sinking each read next to its first use
     __builtin_amdgcn_sched_barrier(0);
-    floatx4 acc[4];
+    floatx4 acc[J];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < J; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      float4 b[4];
+    for (int i = 0; i < MYCH; ++i) {
+      const int c = SPLIT > 1 ? wave + 4 * i : i;
+      if (c < NCH) {   // uniform: depends on the wave index only
+        float4 b[J];
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const float4*>(&Bp[(((c * 4 + q) * 64) + j * 16 + r16) * 4]);
+        for (int j = 0; j < J; ++j)
+          b[j] = *reinterpret_cast<const float4*>(&Bp[(((c * 4 + q) * BN) + j * 16 + r16) * 4]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].x, b[j].x, acc[j], 0, 0, 0);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, b[j].x, acc[j], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].y, b[j].y, acc[j], 0, 0, 0);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, b[j].y, acc[j], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].z, b[j].z, acc[j], 0, 0, 0);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, b[j].z, acc[j], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].w, b[j].w, acc[j], 0, 0, 0);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, b[j].w, acc[j], 0, 0, 0);
+      }
     }
+    if constexpr (SPLIT > 1) {
+      // partials of the four waves -> LDS; thread t then owns output entry
+      // (subtile j, lane l) = t and sums the four partials
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = n0 + j * 16 + r16;
-      const float bv = bias[col < N ? col : N - 1];
+      for (int j = 0; j < J; ++j)
+        *reinterpret_cast<floatx4*>(&Red[((wave * J + j) * 64 + lane) * 4]) = acc[j];
+      __syncthreads();
+      if (threadIdx.x < J * 64) {
+        const int j = threadIdx.x >> 6, l = threadIdx.x & 63;
+        floatx4 sum = *reinterpret_cast<const floatx4*>(&Red[((0 * J + j) * 64 + l) * 4]);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int orow = rt * 64 + wave * 16 + 4 * q + r;
-        float z = acc[j][r] + bv;
-        if (relu) z = z > 0.f ? z : 0.f;
-        if (orow < M && col < N) out[static_cast<int64_t>(orow) * N + col] = z;
+        for (int w = 1; w < 4; ++w) sum += *reinterpret_cast<const floatx4*>(&Red[((w * J + j) * 64 + l) * 4]);
+        const int col = n0 + j * 16 + (l & 15);
+        const float bv = bias[col < N ? col : N - 1];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int orow = rt * 16 + 4 * (l >> 4) + r;
+          float z = sum[r] + bv;
+          if (relu) z = z > 0.f ? z : 0.f;
+          if (orow < M && col < N) out[static_cast<int64_t>(orow) * N + col] = z;
+        }
+      }
+      __syncthreads();
+    } else {
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int col = n0 + j * 16 + r16;
+        const float bv = bias[col < N ? col : N - 1];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int orow = rt * 64 + wave * 16 + 4 * q + r;
+          float z = acc[j][r] + bv;
+          if (relu) z = z > 0.f ? z : 0.f;
+          if (orow < M && col < N) out[static_cast<int64_t>(orow) * N + col] = z;
+        }
       }
     }
   }
 }
 
-template <int NCH>
+template <int NCH, int J, int SPLIT>
 void launch_slab(const int32_t* sizes, const float* hs, const float* ag, const float* ws, const float* wn,
                  const float* bias, int K, int N, int relu, float* out, int64_t cap_rows, hipStream_t s) {
   // LDS bounds the workgroups per CU; size the persistent grid to fill the
   // 256 CUs about twice over.
-  constexpr int per_cu = (160 * 1024) / (NCH * 16 * 64 * 4);
-  const int col_tiles = (N + 63) / 64;
-  int64_t rows = (cap_rows + 63) / 64;
+  constexpr int BN = 16 * J;
+  constexpr int ROWS = SPLIT > 1 ? 16 : 64;
+  constexpr int lds = NCH * 16 * BN * 4 + (SPLIT > 1 ? 4 * J * 64 * 16 : 0);
+  constexpr int per_cu = (160 * 1024) / lds;
+  const int col_tiles = (N + BN - 1) / BN;
+  int64_t rows = (cap_rows + ROWS - 1) / ROWS;
   int64_t want = (2 * 256 * (per_cu < 1 ? 1 : per_cu) + col_tiles - 1) / col_tiles;
   if (rows > want) rows = want;
   if (rows < 1) rows = 1;
   const uintptr_t walign = reinterpret_cast<uintptr_t>(ws) | reinterpret_cast<uintptr_t>(wn);
   const int vec4 = (N % 4 == 0 && walign % 16 == 0) ? 1 : 0;
-  hipLaunchKernelGGL(k_linear_f32_slab<NCH>, dim3(static_cast<unsigned>(rows), col_tiles), dim3(256), 0,
-                     s, sizes, hs, ag, ws, wn, bias, K, N, relu, vec4, out);
+  hipLaunchKernelGGL((k_linear_f32_slab<NCH, J, SPLIT>), dim3(static_cast<unsigned>(rows), col_tiles),
+                     dim3(256), 0, s, sizes, hs, ag, ws, wn, bias, K, N, relu, vec4, out);
+}
+
+// Picks the tiling: layers with enough 64-row tiles to fill the chip twice
+// keep one wave per 16 rows and 64 columns; smaller layers split K over
+// the waves and use 32-column tiles, which halves the slab.
+template <int NCH>
+void launch_slab_for(const int32_t* sizes, const float* hs, const float* ag, const float* ws,
+                     const float* wn, const float* bias, int K, int N, int relu, float* out,
+                     int64_t cap_rows, hipStream_t s) {
+  const int64_t big_tiles = ((cap_rows + 63) / 64) * ((N + 63) / 64);
+  if (big_tiles >= 2 * 256)
+    launch_slab<NCH, 4, 1>(sizes, hs, ag, ws, wn, bias, K, N, relu, out, cap_rows, s);
+  else
+    launch_slab<NCH, 2, 4>(sizes, hs, ag, ws, wn, bias, K, N, relu, out, cap_rows, s);
 }
 
 }  // namespace
@@ -524,7 +580,7 @@ hipError_t launch_sage_linear(const int32_t* sizes, const void* h_self, const vo
     const int nch = (2 * d_in + 15) / 16;
     if (d_in % 4 == 0 && align % 16 == 0 && nch <= 40) {
       float* o = static_cast<float*>(out);
-#define GMB_SLAB(C) launch_slab<C>(sizes, hs, ag, ws, wn, bias, d_in, d_out, relu, o, cap_rows, s)
+#define GMB_SLAB(C) launch_slab_for<C>(sizes, hs, ag, ws, wn, bias, d_in, d_out, relu, o, cap_rows, s)
       if (nch <= 2) GMB_SLAB(2);
       else if (nch <= 4) GMB_SLAB(4);
       else if (nch <= 8) GMB_SLAB(8);

@@ -34,6 +34,24 @@ __device__ __forceinline__ CsrView view(const CsrArgs& a) {
   return CsrView{a.indptr, a.indices, a.num_nodes, a.wide};
 }
 
+// Items [base, base + 8) of a scan tile.  Full groups are two 16-byte loads
+// (base is a multiple of 8 and the arrays are 256-byte aligned); the group
+// holding the end of the data reads element-wise, and entries at or past n
+// are left as they came (the caller ignores them).
+__device__ __forceinline__ void load_items(const int32_t* a, int64_t base, int64_t n,
+                                           int32_t (&v)[kScanItems]) {
+  static_assert(kScanItems == 8, "two int4 loads per thread");
+  if (base + kScanItems <= n) {
+    const int4 x = *reinterpret_cast<const int4*>(a + base);
+    const int4 y = *reinterpret_cast<const int4*>(a + base + 4);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) v[q] = base + q < n ? a[base + q] : 0;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_state_init(uint32_t* table, uint32_t* status, int64_t n) {
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
@@ -75,28 +93,35 @@ __global__ __launch_bounds__(kScanBlock) void k_count_scan(CsrArgs ga, const int
   if (tile >= num_tiles) return;
 
   const int64_t base = static_cast<int64_t>(tile) * kScanTile + threadIdx.x * kScanItems;
+  // Eight consecutive ids per thread, then all sixteen row-offset reads at
+  // once from clamped vertices.
+  int32_t v[kScanItems];
+  load_items(ids, base, n, v);
+  int64_t rb[kScanItems], re[kScanItems];
+  bool bad = false;
+#pragma unroll
+  for (int q = 0; q < kScanItems; ++q) {
+    const bool live = base + q < n;
+    const bool ok = valid_vertex(v[q], g.num_nodes);
+    bad |= live & !ok;
+    v[q] = (live & ok) ? v[q] : -1;
+    row_range(g, v[q] < 0 ? 0 : v[q], rb[q], re[q]);
+  }
+  if (bad) raise_status(status, GMB_STATUS_ERANGE);
   int32_t k[kScanItems];
   int32_t sum = 0;
 #pragma unroll
   for (int q = 0; q < kScanItems; ++q) {
-    const int64_t p = base + q;
-    k[q] = 0;
-    if (p < n) {
-      const int32_t v = ids[p];
-      if (valid_vertex(v, g.num_nodes)) {
-        int64_t b, e;
-        row_range(g, v, b, e);
-        const int64_t d = e - b;
-        k[q] = static_cast<int32_t>(d < 0 ? 0 : (d < fanout ? d : fanout));
-      } else {
-        raise_status(status, GMB_STATUS_ERANGE);
-      }
-    }
+    const int64_t d = v[q] < 0 ? 0 : re[q] - rb[q];
+    k[q] = static_cast<int32_t>(d < 0 ? 0 : (d < fanout ? d : fanout));
     sum += k[q];
   }
   int32_t total;
   const int32_t thread_excl = block_exclusive_scan<kScanBlock>(sum, total, s_wave);
-  if (threadIdx.x == 0) s_excl = tile_lookback(tiles, tile, total);
+  if (threadIdx.x < 64) {
+    const int32_t ex = tile_lookback_wave(tiles, tile, total);
+    if (threadIdx.x == 0) s_excl = ex;
+  }
   __syncthreads();
   int32_t run = s_excl + thread_excl;
 #pragma unroll
@@ -245,23 +270,29 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(const int32_t* nbr, int32
 
   const int64_t base = static_cast<int64_t>(tile) * kScanTile + threadIdx.x * kScanItems;
   int32_t u[kScanItems];
+  load_items(nbr, base, n, u);
+  uint32_t t[kScanItems];
+#pragma unroll
+  for (int q = 0; q < kScanItems; ++q) {
+    const bool ok = (base + q < n) & valid_vertex(u[q], num_nodes);
+    u[q] = ok ? u[q] : -1;
+    t[q] = table[u[q] < 0 ? 0 : u[q]];
+  }
   uint32_t flags = 0;
   int32_t sum = 0;
 #pragma unroll
   for (int q = 0; q < kScanItems; ++q) {
-    const int64_t e = base + q;
-    u[q] = -1;
-    if (e < n) {
-      u[q] = nbr[e];
-      if (valid_vertex(u[q], num_nodes) && table[u[q]] == (kEdgeTag | static_cast<uint32_t>(e))) {
-        flags |= 1u << q;
-        ++sum;
-      }
+    if (u[q] >= 0 && t[q] == (kEdgeTag | static_cast<uint32_t>(base + q))) {
+      flags |= 1u << q;
+      ++sum;
     }
   }
   int32_t total;
   const int32_t thread_excl = block_exclusive_scan<kScanBlock>(sum, total, s_wave);
-  if (threadIdx.x == 0) s_excl = tile_lookback(tiles, tile, total);
+  if (threadIdx.x < 64) {
+    const int32_t ex = tile_lookback_wave(tiles, tile, total);
+    if (threadIdx.x == 0) s_excl = ex;
+  }
   __syncthreads();
   int32_t r = n_dst + s_excl + thread_excl;
 #pragma unroll

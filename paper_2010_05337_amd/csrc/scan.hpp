@@ -52,27 +52,38 @@ __device__ __forceinline__ void publish_tile(uint64_t* tiles, int tile, uint64_t
   __hip_atomic_store(&tiles[tile], word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Called by one thread per tile.  Publishes the tile's aggregate, resolves
-// the exclusive prefix of the tile from its predecessors, publishes the
-// inclusive prefix and returns the exclusive one.  Values are non-negative
-// and below 2^31.
-__device__ int32_t tile_lookback(uint64_t* tiles, int tile, int32_t aggregate) {
+// Called by the whole first wave of a tile (threadIdx.x < 64).  Publishes
+// the tile's aggregate, resolves the tile's exclusive prefix from its
+// predecessors 64 at a time (lane i reads tile - 1 - i; a predecessor that
+// has published nothing yet is re-read until it has), publishes the
+// inclusive prefix and returns the exclusive one to every lane.  Values
+// are non-negative and below 2^31.
+__device__ int32_t tile_lookback_wave(uint64_t* tiles, int tile, int32_t aggregate) {
+  const int lane = threadIdx.x & 63;
   if (tile == 0) {
-    publish_tile(tiles, 0, kTilePrefix | static_cast<uint32_t>(aggregate));
+    if (lane == 0) publish_tile(tiles, 0, kTilePrefix | static_cast<uint32_t>(aggregate));
     return 0;
   }
-  publish_tile(tiles, tile, kTileAggregate | static_cast<uint32_t>(aggregate));
+  if (lane == 0) publish_tile(tiles, tile, kTileAggregate | static_cast<uint32_t>(aggregate));
   int32_t exclusive = 0;
-  for (int t = tile - 1;; --t) {
-    uint64_t w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    while ((w >> 62) == 0) {
+  for (int base = tile - 1;; base -= 64) {
+    const int t = base - lane;
+    uint64_t w = kTilePrefix;   // before tile 0: a prefix of 0
+    if (t >= 0) w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while (__any((w >> 62) == 0)) {
       __builtin_amdgcn_s_sleep(1);
-      w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if ((w >> 62) == 0) w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    exclusive += static_cast<int32_t>(static_cast<uint32_t>(w));
-    if ((w >> 62) == 2) break;
+    const uint64_t prefixes = __ballot((w >> 62) == 2);
+    // lanes up to and including the nearest published prefix contribute
+    const int stop = prefixes ? __ffsll(static_cast<long long>(prefixes)) - 1 : 63;
+    int32_t v = lane <= stop ? static_cast<int32_t>(static_cast<uint32_t>(w)) : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    exclusive += v;
+    if (prefixes) break;
   }
-  publish_tile(tiles, tile, kTilePrefix | static_cast<uint32_t>(exclusive + aggregate));
+  if (lane == 0) publish_tile(tiles, tile, kTilePrefix | static_cast<uint32_t>(exclusive + aggregate));
   return exclusive;
 }
 
