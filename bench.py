@@ -202,6 +202,7 @@ def main():
     t0 = time.perf_counter()
     for i in range(K):
         step(i, S)
+    T_enq = time.perf_counter() - t0
     torch.cuda.synchronize()
     T = time.perf_counter() - t0
     for ln in lanes:
@@ -259,6 +260,7 @@ def main():
                    "num_edges": g.num_edges, "dims": list(cfg.dims), "batches_per_epoch": nb},
         "sampled_edges_per_s": edges_total / T,
         "streams": S,
+        "host_enqueue_ms_per_step": 1e3 * T_enq / K,
         "seeds": seeds_total,
         "sampled_edges": edges_total,
         "datagen_s": t_gen,

@@ -511,18 +511,31 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
   }
 }
 
+#ifndef GMB_SLAB_BLOCKS_WIDE
+#define GMB_SLAB_BLOCKS_WIDE 2
+#endif
+#ifndef GMB_SLAB_BLOCKS_SPLIT
+#define GMB_SLAB_BLOCKS_SPLIT 1
+#endif
+constexpr int kSlabBlocksWide = GMB_SLAB_BLOCKS_WIDE;    // workgroups per CU, one wave per 16 rows
+constexpr int kSlabBlocksSplit = GMB_SLAB_BLOCKS_SPLIT;  // workgroups per CU, split-K tiles
+
 template <int NCH, int J, int SPLIT>
 void launch_slab(const int32_t* sizes, const float* hs, const float* ag, const float* ws, const float* wn,
                  const float* bias, int K, int N, int relu, float* out, int64_t cap_rows, hipStream_t s) {
-  // LDS bounds the workgroups per CU; size the persistent grid to fill the
-  // 256 CUs about twice over.
+  // LDS bounds the workgroups per CU.  The persistent grid holds
+  // kSlabBlocks{Wide,Split} workgroups per CU (capped by LDS): every workgroup
+  // reloads the slab, so a smaller grid reads the weights fewer times and
+  // leaves room for kernels of other streams.
   constexpr int BN = 16 * J;
   constexpr int ROWS = SPLIT > 1 ? 16 : 64;
   constexpr int lds = NCH * 16 * BN * 4 + (SPLIT > 1 ? 4 * J * 64 * 16 : 0);
   constexpr int per_cu = (160 * 1024) / lds;
   const int col_tiles = (N + BN - 1) / BN;
   int64_t rows = (cap_rows + ROWS - 1) / ROWS;
-  int64_t want = (2 * 256 * (per_cu < 1 ? 1 : per_cu) + col_tiles - 1) / col_tiles;
+  const int occ = SPLIT > 1 ? kSlabBlocksSplit : kSlabBlocksWide;
+  const int blocks_per_cu = occ < per_cu ? occ : (per_cu < 1 ? 1 : per_cu);
+  int64_t want = (256 * blocks_per_cu + col_tiles - 1) / col_tiles;
   if (rows > want) rows = want;
   if (rows < 1) rows = 1;
   const uintptr_t walign = reinterpret_cast<uintptr_t>(ws) | reinterpret_cast<uintptr_t>(wn);
