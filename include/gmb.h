@@ -56,6 +56,7 @@ typedef enum { GMB_F32 = 0, GMB_BF16 = 1 } gmb_dtype;
 /* Bits of the device status word. */
 #define GMB_STATUS_ERANGE 1u
 #define GMB_STATUS_EDUP 2u
+#define GMB_STATUS_INTERNAL 4u   /* a bounded wait inside the relabel step ran out */
 
 /* In-neighbour CSR of the input graph G(V, E) (Section II-A): row v lists
  * the sources u of the edges u -> v, so sampling row v samples the vertices
@@ -147,7 +148,8 @@ int gmb_sampler_state_init(void* state, size_t state_bytes, int64_t num_nodes, v
 uint32_t* gmb_state_status_word(void* state);
 
 /* Synchronises `stream`, reads and clears the status word and returns the
- * matching status (GMB_ERANGE before GMB_EDUP), or GMB_OK. */
+ * matching status (GMB_ERANGE before GMB_EDUP before GMB_EDEVICE for
+ * GMB_STATUS_INTERNAL), or GMB_OK. */
 int gmb_read_status(void* state, void* stream);
 
 /* ---- sampling (Section II-B, steps (i)-(ii), recursive per layer) ------- */

@@ -50,7 +50,7 @@ struct HopPlan {
   int fanout;
   int64_t cap_dst, cap_nnz, cap_src;
   size_t off_indptr, off_nbr, off_local;
-  int64_t count_tiles_word, count_ticket_word, flag_tiles_word, flag_ticket_word;
+  int64_t tiles_word, ticket_word, tile_stride;
 };
 
 struct SamplePlan {
@@ -58,9 +58,12 @@ struct SamplePlan {
   HopPlan hop[GMB_MAX_LAYERS];
   size_t off_ids, off_sizes, off_zero;
   int64_t num_zero_words;
+  int32_t num_size_words;   // 4 per layer, then the segment-totals matrix
   int64_t cap_ids;
   size_t total;
 };
+
+constexpr int kTotalsWords = GMB_MAX_LAYERS * GMB_MAX_LAYERS;
 
 // Fills the plan; returns GMB_OK or an argument error (message set).
 int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers, int64_t num_nodes,
@@ -92,19 +95,19 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
     if (hp.cap_nnz >= kMaxInt32 || hp.cap_src >= kMaxInt32)
       return fail(GMB_EINVAL, "hop %d: capacity %lld edges / %lld sources exceeds 2^31-1", h,
                   static_cast<long long>(hp.cap_nnz), static_cast<long long>(hp.cap_src));
-    hp.count_tiles_word = zero_words;
-    zero_words += gmb::scan_tiles(hp.cap_dst);
-    hp.count_ticket_word = zero_words++;
-    hp.flag_tiles_word = zero_words;
-    zero_words += gmb::scan_tiles(hp.cap_nnz);
-    hp.flag_ticket_word = zero_words++;
+    // the relabel scan of hop h carries 1 + (later hops) values
+    hp.tile_stride = gmb::scan_tiles(hp.cap_nnz);
+    hp.tiles_word = zero_words;
+    zero_words += hp.tile_stride * (num_layers - h);
+    hp.ticket_word = zero_words++;
     cap_dst = hp.cap_src;
   }
   p.cap_ids = p.hop[num_layers - 1].cap_src;
   p.off_ids = off;
   off = align_up(off + sizeof(int32_t) * std::max<int64_t>(p.cap_ids, 1));
+  p.num_size_words = 4 * num_layers + kTotalsWords;
   p.off_sizes = off;
-  off = align_up(off + sizeof(int32_t) * 4 * num_layers);
+  off = align_up(off + sizeof(int32_t) * p.num_size_words);
   p.off_zero = off;
   p.num_zero_words = zero_words;
   off = align_up(off + sizeof(uint64_t) * zero_words);
@@ -218,6 +221,8 @@ int gmb_read_status(void* state, void* stream) {
   }
   if (word & GMB_STATUS_ERANGE) return fail(GMB_ERANGE, "a vertex id outside [0, num_nodes) was found on the device");
   if (word & GMB_STATUS_EDUP) return fail(GMB_EDUP, "the seed list holds a vertex more than once");
+  if (word & GMB_STATUS_INTERNAL)
+    return fail(GMB_EDEVICE, "a bounded wait in the relabel step ran out (local ids set to -1)");
   return ok();
 }
 
@@ -260,6 +265,7 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
   const hipStream_t s = as_stream(stream);
 
   gmb::CsrArgs g{csr->indptr, csr->indices, csr->num_nodes, csr->indptr_bits == 64 ? 1 : 0};
+  int32_t* totals = sizes + 4 * num_layers;
   gmb::HopArgs hops[GMB_MAX_LAYERS];
   gmb_blocks res{};
   res.num_layers = num_layers;
@@ -268,14 +274,12 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
     const HopPlan& hp = p.hop[h];
     gmb::HopArgs& a = hops[h];
     a.sizes = sizes + 4 * hp.layer;
-    a.next_sizes = (h + 1 < num_layers) ? sizes + 4 * p.hop[h + 1].layer : nullptr;
     a.indptr = reinterpret_cast<int32_t*>(base + hp.off_indptr);
     a.nbr = reinterpret_cast<int32_t*>(base + hp.off_nbr);
     a.local = reinterpret_cast<int32_t*>(base + hp.off_local);
-    a.count_tiles = zero + hp.count_tiles_word;
-    a.count_ticket = reinterpret_cast<uint32_t*>(zero + hp.count_ticket_word);
-    a.flag_tiles = zero + hp.flag_tiles_word;
-    a.flag_ticket = reinterpret_cast<uint32_t*>(zero + hp.flag_ticket_word);
+    a.tiles = zero + hp.tiles_word;
+    a.ticket = reinterpret_cast<uint32_t*>(zero + hp.ticket_word);
+    a.tile_stride = hp.tile_stride;
     a.cap_dst = hp.cap_dst;
     a.cap_nnz = hp.cap_nnz;
     a.cap_src = hp.cap_src;
@@ -294,20 +298,43 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
     bk.layer = hp.layer;
   }
 
-  const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
-  hipError_t e = gmb::launch_prep(seeds, num_seeds, ids, table, csr->num_nodes, status, zero,
-                                  p.num_zero_words, sizes, 4 * num_layers, 4 * (num_layers - 1) + 0, s);
-  if (e != hipSuccess) return hip_fail(e, "prep launch");
+  gmb::SeedArgs sa{};
+  sa.seeds = seeds;
+  sa.num_seeds = num_seeds;
+  sa.first_sizes = 4 * p.hop[0].layer;
+  sa.ids = ids;
+  sa.zero = zero;
+  sa.num_zero = p.num_zero_words;
+  sa.sizes = sizes;
+  sa.num_size_words = p.num_size_words;
+  sa.totals = totals;
   for (int h = 0; h < num_layers; ++h) {
-    e = gmb::launch_count_scan(g, ids, hops[h], status, s);
-    if (e != hipSuccess) return hip_fail(e, "degree scan launch");
-    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, s);
+    sa.indptr[h] = hops[h].indptr;
+    sa.fanout[h] = hops[h].fanout;
+  }
+  const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
+  hipError_t e = gmb::launch_seed_scan(sa, num_layers, g, table, status, s);
+  if (e != hipSuccess) return hip_fail(e, "seed launch");
+  for (int h = 0; h < num_layers; ++h) {
+    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, h == 0 ? 1 : 0, s);
     if (e != hipSuccess) return hip_fail(e, "sample launch");
-    e = gmb::launch_assign(hops[h], ids, table, csr->num_nodes, s);
+    gmb::AssignArgs aa{};
+    aa.nbr = hops[h].nbr;
+    aa.local = hops[h].local;
+    aa.sizes = hops[h].sizes;
+    aa.next_sizes = (h + 1 < num_layers) ? hops[h + 1].sizes : nullptr;
+    aa.tiles = hops[h].tiles;
+    aa.tile_stride = hops[h].tile_stride;
+    aa.ticket = hops[h].ticket;
+    aa.totals = totals;
+    aa.hop = h;
+    for (int v = 1; h + v < num_layers; ++v) {
+      aa.indptr[v] = hops[h + v].indptr;
+      aa.fanout[v] = hops[h + v].fanout;
+    }
+    e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, ids, table, status, s);
     if (e != hipSuccess) return hip_fail(e, "relabel launch");
   }
-  e = gmb::launch_local(hops, num_layers, ids, num_seeds, table, csr->num_nodes, status, s);
-  if (e != hipSuccess) return hip_fail(e, "local-id launch");
   e = gmb::launch_cleanup(ids, sizes + 4 * 0, p.cap_ids, table, csr->num_nodes, s);
   if (e != hipSuccess) return hip_fail(e, "cleanup launch");
   *out = res;

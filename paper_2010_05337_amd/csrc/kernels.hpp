@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gmb.h"
+
 namespace gmb {
 
 // Indices of the per-block device size words.
@@ -20,14 +22,12 @@ struct CsrArgs {
 // Device pointers and host-known bounds of one sampling hop.
 struct HopArgs {
   int32_t* sizes;        // this block's {n_dst, n_src, nnz, 0}
-  int32_t* next_sizes;   // the next hop's size words (nullptr after the last hop)
   int32_t* indptr;       // [cap_dst + 1]
   int32_t* nbr;          // [cap_nnz]
   int32_t* local;        // [cap_nnz]
-  uint64_t* count_tiles; // look-back words of the degree scan
-  uint32_t* count_ticket;
-  uint64_t* flag_tiles;  // look-back words of the new-vertex scan
-  uint32_t* flag_ticket;
+  uint64_t* tiles;       // look-back words of this hop's relabel scan
+  uint32_t* ticket;
+  int64_t tile_stride;   // words per scanned value
   int64_t cap_dst, cap_nnz, cap_src;
   int fanout;
   int layer;
@@ -39,20 +39,48 @@ constexpr int kScanTile = kScanBlock * kScanItems;
 
 inline int64_t scan_tiles(int64_t n) { return n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile; }
 
+// Arguments of the seed kernel (segment 0: the seeds).  Per hop v:
+// indptr[v] its block row offsets, fanout[v] its fan-out.  totals is the
+// [GMB_MAX_LAYERS][GMB_MAX_LAYERS] matrix of segment totals (row =
+// segment, column = hop), cleared with the size words.
+struct SeedArgs {
+  const int32_t* seeds;
+  int32_t num_seeds;
+  int32_t first_sizes;   // offset of hop 0's size words in `sizes`
+  int32_t* ids;
+  uint64_t* zero;
+  int64_t num_zero;
+  int32_t* sizes;        // every size word, then the totals matrix
+  int32_t num_size_words;
+  int32_t* totals;
+  int32_t* indptr[GMB_MAX_LAYERS];
+  int32_t fanout[GMB_MAX_LAYERS];
+};
+
+// Arguments of hop `hop`'s relabel.  Value v >= 1 of its scan belongs to
+// hop hop + v: indptr[v], fanout[v].
+struct AssignArgs {
+  const int32_t* nbr;
+  int32_t* local;
+  int32_t* sizes;
+  int32_t* next_sizes;   // nullptr after the last hop
+  uint64_t* tiles;
+  int64_t tile_stride;
+  uint32_t* ticket;
+  int32_t* totals;
+  int hop;
+  int32_t* indptr[GMB_MAX_LAYERS];
+  int32_t fanout[GMB_MAX_LAYERS];
+};
+
 // sample.hip
 hipError_t launch_state_init(uint32_t* table, uint32_t* status, int64_t num_nodes, hipStream_t s);
-hipError_t launch_prep(const int32_t* seeds, int32_t num_seeds, int32_t* ids, uint32_t* table,
-                       int64_t num_nodes, uint32_t* status, uint64_t* zero_words, int64_t num_zero,
-                       int32_t* all_sizes, int32_t num_size_words, int32_t first_ndst_word,
-                       hipStream_t s);
-hipError_t launch_count_scan(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* status,
-                             hipStream_t s);
+hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, uint32_t* table,
+                            uint32_t* status, hipStream_t s);
 hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* table,
-                         uint32_t* status, uint32_t k0, uint32_t k1, hipStream_t s);
-hipError_t launch_assign(const HopArgs& h, int32_t* ids, uint32_t* table, int64_t num_nodes,
-                         hipStream_t s);
-hipError_t launch_local(const HopArgs* hops, int num_hops, const int32_t* ids, int32_t num_seeds,
-                        const uint32_t* table, int64_t num_nodes, uint32_t* status, hipStream_t s);
+                         uint32_t* status, uint32_t k0, uint32_t k1, int first_hop, hipStream_t s);
+hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
+                         int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s);
 hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src,
                           uint32_t* table, int64_t num_nodes, hipStream_t s);
 

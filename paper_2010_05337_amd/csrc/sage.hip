@@ -435,19 +435,27 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, r16 = lane & 15;
-  for (int rt = blockIdx.x; rt < row_tiles; rt += gridDim.x) {
+  // A fragments of row tile rt (a tile past the end reads row M-1: every
+  // load is unconditional)
+  auto load_tile = [&](int rt, float4 (&dst)[MYCH]) {
     const int row = SPLIT > 1 ? rt * 16 + r16 : rt * 64 + wave * 16 + r16;
     const int64_t arow = row < M ? row : M - 1;
     const float* hrow = Hs + arow * K;
     const float* grow = Ag + arow * K;
-    float4 a[MYCH];
 #pragma unroll
     for (int i = 0; i < MYCH; ++i) {
       const int c = SPLIT > 1 ? wave + 4 * i : i;
       const int k = c * 16 + 4 * q;
       const int kk = k >= K2 ? 0 : (k < K ? k : k - K);
-      a[i] = *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
+      dst[i] = *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
     }
+  };
+  // software pipeline over the workgroup's row tiles: the next tile's A
+  // reads are in flight while the current tile's MFMAs run
+  float4 a[MYCH], a_next[MYCH];
+  load_tile(blockIdx.x, a);
+  for (int rt = blockIdx.x; rt < row_tiles; rt += gridDim.x) {
+    load_tile(rt + gridDim.x, a_next);
     // keep the scheduler from sinking each read next to its first use
     __builtin_amdgcn_sched_barrier(0);
     floatx4 acc[J];
@@ -508,6 +516,8 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
         }
       }
     }
+#pragma unroll
+    for (int i = 0; i < MYCH; ++i) a[i] = a_next[i];
   }
 }
 
@@ -515,7 +525,7 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
 #define GMB_SLAB_BLOCKS_WIDE 2
 #endif
 #ifndef GMB_SLAB_BLOCKS_SPLIT
-#define GMB_SLAB_BLOCKS_SPLIT 1
+#define GMB_SLAB_BLOCKS_SPLIT 2
 #endif
 constexpr int kSlabBlocksWide = GMB_SLAB_BLOCKS_WIDE;    // workgroups per CU, one wave per 16 rows
 constexpr int kSlabBlocksSplit = GMB_SLAB_BLOCKS_SPLIT;  // workgroups per CU, split-K tiles

@@ -3,24 +3,29 @@
 // II-B: pick at most K neighbours of every target, repeat once per layer;
 // the sampled graph is the mini-batch's computation graph, Fig. 1(b)).
 //
-// One hop, for destinations dst = ids[0 : n_dst] (device-resident count):
-//   k_count_scan  k_p = min(deg(dst[p]), fanout), exclusive scan -> block
-//                 row offsets and nnz (single-pass look-back scan)
-//   k_sample      Floyd's algorithm per destination, one lane per draw,
-//                 Philox-keyed draws; sampled slots sorted by rank; the
-//                 sampled global ids are written in slot order and each
-//                 vertex's first edge position is recorded by atomicMin in
-//                 the dedup table
-//   k_assign      scan of the "first occurrence" flags: new vertex number
-//                 n_dst + rank, appended to ids and stored in the table
-// After the last hop:
-//   k_local       every edge's local id = table[global id] (all hops)
-//   k_cleanup     table entries of every vertex of the batch back to empty
-//
 // ids[] is shared by all hops: the sources of a block are its destinations
 // followed by its new vertices, which are exactly the next hop's
-// destinations, so every hop only appends.  A vertex keeps the same local
-// id in every block, and the table maps it to that id for the whole call.
+// destinations, so every hop only appends, and a vertex keeps the same
+// local id (its position in ids) in every block.  The positions come in
+// segments: segment 0 = the seeds, segment j >= 1 = the vertices new in hop
+// j - 1; hop h's destinations are segments 0..h.
+//
+// A vertex's clamped degree k_h = min(deg, fanout of hop h) is computed for
+// every later hop h as soon as the vertex gets its position, and scanned
+// within its segment; hop h's block row offsets are then the segment's
+// offsets plus the totals of the earlier segments.  So no hop needs a
+// degree pass of its own:
+//   k_seed_scan   (one workgroup) seeds -> ids and table; degree scans of
+//                 segment 0 for all hops; clears the look-back words; the
+//                 first hop's sampling checks that every seed owns its slot
+//   k_sample(h)   Floyd's algorithm per destination, one lane per draw,
+//                 Philox-keyed draws; sampled slots ranked in the group and
+//                 written in slot order; each vertex's first edge position
+//                 recorded by atomicMin in the dedup table
+//   k_assign(h)   scan of the "first occurrence" flags (new vertex number
+//                 n_dst + rank) together with the degree scans of the new
+//                 vertices for the later hops; writes every edge's local id
+//   k_cleanup     table entries of every vertex of the batch back to empty
 #include "common.hpp"
 #include "kernels.hpp"
 #include "philox.hpp"
@@ -34,10 +39,14 @@ __device__ __forceinline__ CsrView view(const CsrArgs& a) {
   return CsrView{a.indptr, a.indices, a.num_nodes, a.wide};
 }
 
+__device__ __forceinline__ int32_t clamp_degree(int64_t d, int fanout) {
+  return static_cast<int32_t>(d < 0 ? 0 : (d < fanout ? d : fanout));
+}
+
 // Items [base, base + 8) of a scan tile.  Full groups are two 16-byte loads
 // (base is a multiple of 8 and the arrays are 256-byte aligned); the group
 // holding the end of the data reads element-wise, and entries at or past n
-// are left as they came (the caller ignores them).
+// are left as 0 (the caller ignores them).
 __device__ __forceinline__ void load_items(const int32_t* a, int64_t base, int64_t n,
                                            int32_t (&v)[kScanItems]) {
   static_assert(kScanItems == 8, "two int4 loads per thread");
@@ -59,81 +68,70 @@ __global__ __launch_bounds__(256) void k_state_init(uint32_t* table, uint32_t* s
   if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
 
-// Seeds -> ids[0:B] and their table slots; clears the look-back words and
-// the size words.  all_sizes holds 4 words per layer; the first hop is the
-// last layer.
-__global__ __launch_bounds__(256) void k_prep(const int32_t* seeds, int32_t num_seeds, int32_t* ids,
-                                              uint32_t* table, int64_t num_nodes, uint32_t* status,
-                                              uint64_t* zero, int64_t num_zero, int32_t* all_sizes,
-                                              int32_t num_size_words, int32_t first_ndst_word) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < num_zero) zero[i] = 0;
-  if (i < num_size_words) all_sizes[i] = (i == first_ndst_word) ? num_seeds : 0;
-  if (i < num_seeds) {
-    const int32_t s = seeds[i];
-    ids[i] = s;
-    if (valid_vertex(s, num_nodes))
-      atomicMin(&table[s], static_cast<uint32_t>(i));
+// One workgroup.  Seeds -> ids[0:B] and their table slots (atomicMin, so a
+// vertex listed twice keeps its first position); segment 0's degree scans
+// for every hop; clears the look-back words and the size words.
+constexpr int kSeedBlock = 512;
+constexpr int kSeedItems = 4;
+
+template <int NV>
+__global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga, uint32_t* table,
+                                                          uint32_t* status) {
+  __shared__ int32_t s_wave[NV * (kSeedBlock / 64)];
+  const CsrView g = view(ga);
+  const int tid = threadIdx.x;
+  for (int64_t i = tid; i < a.num_zero; i += kSeedBlock) a.zero[i] = 0;
+  for (int i = tid; i < a.num_size_words; i += kSeedBlock) a.sizes[i] = 0;
+  const int32_t B = a.num_seeds;
+  for (int32_t p = tid; p < B; p += kSeedBlock) {
+    const int32_t s = a.seeds[p];
+    a.ids[p] = s;
+    if (valid_vertex(s, g.num_nodes))
+      atomicMin(&table[s], static_cast<uint32_t>(p));
     else
       raise_status(status, GMB_STATUS_ERANGE);
   }
-}
 
-__global__ __launch_bounds__(kScanBlock) void k_count_scan(CsrArgs ga, const int32_t* ids,
-                                                           int32_t* sizes, int32_t* blk_indptr,
-                                                           uint64_t* tiles, uint32_t* ticket,
-                                                           int fanout, uint32_t* status) {
-  __shared__ int s_tile;
-  __shared__ int32_t s_excl;
-  __shared__ int32_t s_wave[kScanBlock / 64];
-  const CsrView g = view(ga);
-  const int32_t n = load_size(&sizes[kNDst]);
-  const int num_tiles = n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile;
-  const int tile = claim_tile(ticket, &s_tile);
-  if (tile >= num_tiles) return;
-
-  const int64_t base = static_cast<int64_t>(tile) * kScanTile + threadIdx.x * kScanItems;
-  // Eight consecutive ids per thread, then all sixteen row-offset reads at
-  // once from clamped vertices.
-  int32_t v[kScanItems];
-  load_items(ids, base, n, v);
-  int64_t rb[kScanItems], re[kScanItems];
-  bool bad = false;
+  int32_t running[NV];
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q) {
-    const bool live = base + q < n;
-    const bool ok = valid_vertex(v[q], g.num_nodes);
-    bad |= live & !ok;
-    v[q] = (live & ok) ? v[q] : -1;
-    row_range(g, v[q] < 0 ? 0 : v[q], rb[q], re[q]);
-  }
-  if (bad) raise_status(status, GMB_STATUS_ERANGE);
-  int32_t k[kScanItems];
-  int32_t sum = 0;
+  for (int v = 0; v < NV; ++v) running[v] = 0;
+  for (int32_t base = 0; base < B; base += kSeedBlock * kSeedItems) {
+    int32_t deg[kSeedItems];
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q) {
-    const int64_t d = v[q] < 0 ? 0 : re[q] - rb[q];
-    k[q] = static_cast<int32_t>(d < 0 ? 0 : (d < fanout ? d : fanout));
-    sum += k[q];
-  }
-  int32_t total;
-  const int32_t thread_excl = block_exclusive_scan<kScanBlock>(sum, total, s_wave);
-  if (threadIdx.x < 64) {
-    const int32_t ex = tile_lookback_wave(tiles, tile, total);
-    if (threadIdx.x == 0) s_excl = ex;
-  }
-  __syncthreads();
-  int32_t run = s_excl + thread_excl;
+    for (int q = 0; q < kSeedItems; ++q) {
+      const int32_t p = base + tid * kSeedItems + q;
+      const int32_t s = p < B ? a.seeds[p] : -1;
+      int64_t b = 0, e = 0;
+      if (valid_vertex(s, g.num_nodes)) row_range(g, s, b, e);
+      deg[q] = static_cast<int32_t>(e - b);
+    }
+    int32_t sum[NV], excl[NV], total[NV];
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q) {
-    const int64_t p = base + q;
-    if (p < n) blk_indptr[p] = run;
-    run += k[q];
+    for (int v = 0; v < NV; ++v) {
+      sum[v] = 0;
+#pragma unroll
+      for (int q = 0; q < kSeedItems; ++q) sum[v] += clamp_degree(deg[q], a.fanout[v]);
+    }
+    block_exclusive_scan_multi<kSeedBlock, NV>(sum, excl, total, s_wave);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      int32_t run = running[v] + excl[v];
+#pragma unroll
+      for (int q = 0; q < kSeedItems; ++q) {
+        const int32_t p = base + tid * kSeedItems + q;
+        if (p < B) a.indptr[v][p] = run;
+        run += clamp_degree(deg[q], a.fanout[v]);
+      }
+      running[v] += total[v];
+    }
   }
-  if (tile == num_tiles - 1 && threadIdx.x == 0) {
-    const int32_t nnz = s_excl + total;
-    blk_indptr[n < 0 ? 0 : n] = nnz;
-    sizes[kNnz] = nnz;
+  if (tid == 0) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) a.totals[v] = running[v];   // segment 0 (row 0), hop v
+    // hop 0 has one segment: its sizes are known now
+    a.sizes[a.first_sizes + kNDst] = B;
+    a.sizes[a.first_sizes + kNnz] = running[0];
+    a.indptr[0][B] = running[0];
   }
 }
 
@@ -159,18 +157,22 @@ template <int G>
 __global__ __launch_bounds__(256) void k_sample(CsrArgs ga, const int32_t* ids, const int32_t* sizes,
                                                 const int32_t* blk_indptr, int32_t* nbr,
                                                 uint32_t* table, uint32_t* status, int fanout,
-                                                int layer, uint32_t k0, uint32_t k1) {
+                                                int layer, uint32_t k0, uint32_t k1, int check_seeds) {
   const CsrView g = view(ga);
   const int64_t p = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
   const int lane = threadIdx.x & (G - 1);
   const int32_t n_dst = load_size(&sizes[kNDst]);
   if (p >= n_dst) return;
   const int32_t v = ids[p];
-  if (!valid_vertex(v, g.num_nodes)) return;   // the degree scan gave it k = 0
+  if (!valid_vertex(v, g.num_nodes)) return;   // its clamped degree was 0
   int64_t begin, end;
   row_range(g, v, begin, end);
   const int64_t d = end - begin;
   const int32_t off = blk_indptr[p];
+  // first hop: every seed owns its table slot unless the seed list holds
+  // the vertex twice (the slot then names the first copy)
+  if (check_seeds && lane == 0 && table[v] != static_cast<uint32_t>(p))
+    raise_status(status, GMB_STATUS_EDUP);
 
   int32_t pos = -1, u = 0;
   if (d <= fanout) {
@@ -210,13 +212,15 @@ __global__ __launch_bounds__(256) void k_sample(CsrArgs ga, const int32_t* ids, 
 __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* ids,
                                                      const int32_t* sizes, const int32_t* blk_indptr,
                                                      int32_t* nbr, uint32_t* table, uint32_t* status,
-                                                     int fanout, int layer, uint32_t k0, uint32_t k1) {
+                                                     int fanout, int layer, uint32_t k0, uint32_t k1,
+                                                     int check_seeds) {
   const CsrView g = view(ga);
   const int64_t p = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int32_t n_dst = load_size(&sizes[kNDst]);
   if (p >= n_dst) return;
   const int32_t v = ids[p];
   if (!valid_vertex(v, g.num_nodes)) return;
+  if (check_seeds && table[v] != static_cast<uint32_t>(p)) raise_status(status, GMB_STATUS_EDUP);
   int64_t begin, end;
   row_range(g, v, begin, end);
   const int64_t d = end - begin;
@@ -249,104 +253,154 @@ __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* 
   }
 }
 
-// Edge e is the first occurrence of its vertex u when the table holds
-// (tag | e).  Those edges are numbered by a scan; the vertex becomes source
-// n_dst + rank of the block, is appended to ids and gets its local id in
-// the table.  Other tiles may read table[u] while it is rewritten: they see
-// either the tag of another edge or the local id, never their own tag, so
-// their flag is 0 either way.
-__global__ __launch_bounds__(kScanBlock) void k_assign(const int32_t* nbr, int32_t* sizes,
-                                                       int32_t* next_sizes, int32_t* ids,
-                                                       uint32_t* table, int64_t num_nodes,
-                                                       uint64_t* tiles, uint32_t* ticket) {
+// Hop h's relabel.  Edge e is the first occurrence of its vertex u when the
+// table holds (tag | e); those edges are numbered by a scan, the vertex
+// becomes source n_dst + rank, is appended to ids and gets its local id in
+// the table.  Value 0 of the scan counts them; value v >= 1 carries the
+// new vertices' clamped degrees for hop h + v, which become those hops'
+// block row offsets.  Every edge's local id is written here: a vertex seen
+// before this hop has it in the table; a repeat of a vertex that is new in
+// this hop takes it from LDS when the first occurrence is in the same tile,
+// else from the table once the earlier tile has stored it (that tile holds
+// an earlier ticket, so it is running and never waits on this one).  Other
+// tiles may read table[u] while it is rewritten: they see either a tag or
+// the local id, never their own tag, so their flag is 0 either way.
+constexpr int kSpinLimit = 1 << 22;
+
+template <int NV>
+__global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga, int32_t* ids,
+                                                       uint32_t* table, uint32_t* status) {
   __shared__ int s_tile;
-  __shared__ int32_t s_excl;
-  __shared__ int32_t s_wave[kScanBlock / 64];
-  const int32_t n = load_size(&sizes[kNnz]);
-  const int32_t n_dst = load_size(&sizes[kNDst]);
+  __shared__ int32_t s_excl[NV];
+  __shared__ int32_t s_wave[NV * (kScanBlock / 64)];
+  __shared__ int32_t s_pos[kScanTile];
+  const CsrView g = view(ga);
+  const int32_t n = load_size(&a.sizes[kNnz]);
+  const int32_t n_dst = load_size(&a.sizes[kNDst]);
   const int num_tiles = n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile;
-  const int tile = claim_tile(ticket, &s_tile);
+  const int tile = claim_tile(a.ticket, &s_tile);
   if (tile >= num_tiles) return;
 
-  const int64_t base = static_cast<int64_t>(tile) * kScanTile + threadIdx.x * kScanItems;
+  const int64_t tile_base = static_cast<int64_t>(tile) * kScanTile;
+  const int64_t base = tile_base + threadIdx.x * kScanItems;
   int32_t u[kScanItems];
-  load_items(nbr, base, n, u);
+  load_items(a.nbr, base, n, u);
   uint32_t t[kScanItems];
 #pragma unroll
   for (int q = 0; q < kScanItems; ++q) {
-    const bool ok = (base + q < n) & valid_vertex(u[q], num_nodes);
+    const bool ok = (base + q < n) & valid_vertex(u[q], g.num_nodes);
     u[q] = ok ? u[q] : -1;
     t[q] = table[u[q] < 0 ? 0 : u[q]];
   }
   uint32_t flags = 0;
-  int32_t sum = 0;
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q) {
-    if (u[q] >= 0 && t[q] == (kEdgeTag | static_cast<uint32_t>(base + q))) {
-      flags |= 1u << q;
-      ++sum;
+  for (int q = 0; q < kScanItems; ++q)
+    if (u[q] >= 0 && t[q] == (kEdgeTag | static_cast<uint32_t>(base + q))) flags |= 1u << q;
+  // degrees of the new vertices (a non-flagged item reads vertex 0's row
+  // and contributes nothing)
+  int32_t deg[kScanItems];
+#pragma unroll
+  for (int q = 0; q < kScanItems; ++q) deg[q] = 0;
+  if constexpr (NV > 1) {
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) {
+      const bool f = (flags >> q) & 1u;
+      int64_t b, e;
+      row_range(g, f ? u[q] : 0, b, e);
+      deg[q] = f ? static_cast<int32_t>(e - b) : 0;
     }
   }
-  int32_t total;
-  const int32_t thread_excl = block_exclusive_scan<kScanBlock>(sum, total, s_wave);
+  int32_t sum[NV], thr[NV], total[NV], excl[NV];
+  sum[0] = __popc(flags);
+#pragma unroll
+  for (int v = 1; v < NV; ++v) {
+    sum[v] = 0;
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) sum[v] += clamp_degree(deg[q], a.fanout[v]);
+  }
+  block_exclusive_scan_multi<kScanBlock, NV>(sum, thr, total, s_wave);
   if (threadIdx.x < 64) {
-    const int32_t ex = tile_lookback_wave(tiles, tile, total);
-    if (threadIdx.x == 0) s_excl = ex;
+    int32_t ex[NV];
+    tile_lookback_multi<NV>(a.tiles, a.tile_stride, tile, total, ex);
+    if (threadIdx.x == 0) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) s_excl[v] = ex[v];
+    }
   }
   __syncthreads();
-  int32_t r = n_dst + s_excl + thread_excl;
+#pragma unroll
+  for (int v = 0; v < NV; ++v) excl[v] = s_excl[v];
+
+  // row offsets of hop h + v start after the earlier segments' totals
+  int32_t basev[NV];
+#pragma unroll
+  for (int v = 1; v < NV; ++v) {
+    basev[v] = 0;
+    for (int i = 0; i <= a.hop; ++i) basev[v] += a.totals[i * GMB_MAX_LAYERS + a.hop + v];
+  }
+  // new vertices: position, ids, table, local id, later hops' row offsets
+  int32_t r = n_dst + excl[0] + thr[0];
+  int32_t run[NV];
+#pragma unroll
+  for (int v = 1; v < NV; ++v) run[v] = basev[v] + excl[v] + thr[v];
 #pragma unroll
   for (int q = 0; q < kScanItems; ++q) {
-    if (flags & (1u << q)) {
+    if ((flags >> q) & 1u) {
       ids[r] = u[q];
-      table[u[q]] = static_cast<uint32_t>(r);
+      a.local[base + q] = r;
+      __hip_atomic_store(&table[u[q]], static_cast<uint32_t>(r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_pos[threadIdx.x * kScanItems + q] = r;
+#pragma unroll
+      for (int v = 1; v < NV; ++v) {
+        a.indptr[v][r] = run[v];
+        run[v] += clamp_degree(deg[q], a.fanout[v]);
+      }
       ++r;
     }
   }
-  if (tile == num_tiles - 1 && threadIdx.x == 0) {
-    const int32_t n_src = n_dst + s_excl + total;
-    sizes[kNSrc] = n_src;
-    if (next_sizes) next_sizes[kNDst] = n_src;
-  }
-}
-
-struct LocalSeg {
-  const int32_t* nbr;
-  int32_t* local;
-  const int32_t* sizes;
-  int64_t first_block;
-};
-
-struct LocalArgs {
-  LocalSeg seg[GMB_MAX_LAYERS];
-  int num_seg;
-  int64_t seed_first_block;
-};
-
-// local[e] = table[nbr[e]] for the edges of every hop; the blocks past the
-// edge segments check that each seed owns its table slot (a duplicated
-// seed does not).
-__global__ __launch_bounds__(256) void k_local(LocalArgs a, const int32_t* ids, int32_t num_seeds,
-                                               const uint32_t* table, int64_t num_nodes,
-                                               uint32_t* status) {
-  const int64_t b = blockIdx.x;
-  if (b >= a.seed_first_block) {
-    const int64_t p = (b - a.seed_first_block) * blockDim.x + threadIdx.x;
-    if (p < num_seeds) {
-      const int32_t s = ids[p];
-      if (valid_vertex(s, num_nodes) && table[s] != static_cast<uint32_t>(p))
-        raise_status(status, GMB_STATUS_EDUP);
+  __syncthreads();
+  bool lost = false;
+  for (int q = 0; q < kScanItems; ++q) {
+    if (base + q >= n || ((flags >> q) & 1u)) continue;
+    int32_t loc = -1;
+    if (u[q] >= 0) {
+      if (t[q] < kEdgeTag) {
+        loc = static_cast<int32_t>(t[q]);
+      } else {
+        const int64_t e0 = t[q] & ~kEdgeTag;
+        if (e0 >= tile_base) {
+          loc = s_pos[e0 - tile_base];
+        } else {
+          uint32_t x = __hip_atomic_load(&table[u[q]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          for (int spin = 0; x >= kEdgeTag && spin < kSpinLimit; ++spin) {
+            __builtin_amdgcn_s_sleep(2);
+            x = __hip_atomic_load(&table[u[q]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+          lost |= x >= kEdgeTag;
+          loc = x < kEdgeTag ? static_cast<int32_t>(x) : -1;
+        }
+      }
     }
-    return;
+    a.local[base + q] = loc;
   }
-  int k = 0;
-  while (k + 1 < a.num_seg && b >= a.seg[k + 1].first_block) ++k;
-  const LocalSeg& s = a.seg[k];
-  const int64_t e = (b - s.first_block) * blockDim.x + threadIdx.x;
-  const int32_t n = load_size(&s.sizes[kNnz]);
-  if (e >= n) return;
-  const int32_t u = s.nbr[e];
-  s.local[e] = valid_vertex(u, num_nodes) ? static_cast<int32_t>(table[u]) : -1;
+  if (lost) raise_status(status, GMB_STATUS_INTERNAL);
+  if (tile == num_tiles - 1 && threadIdx.x == 0) {
+    const int32_t n_src = n_dst + excl[0] + total[0];
+    a.sizes[kNSrc] = n_src;
+    if (a.next_sizes) {
+      a.next_sizes[kNDst] = n_src;
+      if constexpr (NV > 1) {
+        // this hop's new vertices are segment h + 1
+#pragma unroll
+        for (int v = 1; v < NV; ++v)
+          a.totals[(a.hop + 1) * GMB_MAX_LAYERS + a.hop + v] = excl[v] + total[v];
+        // the next hop's destinations are complete: its edge count is known
+        const int32_t nnz = basev[1] + excl[1] + total[1];
+        a.next_sizes[kNnz] = nnz;
+        a.indptr[1][n_src] = nnz;
+      }
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void k_cleanup(const int32_t* ids, const int32_t* final_sizes,
@@ -374,69 +428,59 @@ hipError_t launch_state_init(uint32_t* table, uint32_t* status, int64_t num_node
   return hipGetLastError();
 }
 
-hipError_t launch_prep(const int32_t* seeds, int32_t num_seeds, int32_t* ids, uint32_t* table,
-                       int64_t num_nodes, uint32_t* status, uint64_t* zero_words, int64_t num_zero,
-                       int32_t* all_sizes, int32_t num_size_words, int32_t first_ndst_word,
-                       hipStream_t s) {
-  int64_t n = num_zero;
-  if (num_seeds > n) n = num_seeds;
-  if (num_size_words > n) n = num_size_words;
-  hipLaunchKernelGGL(k_prep, dim3(grid_for(n)), dim3(256), 0, s, seeds, num_seeds, ids, table,
-                     num_nodes, status, zero_words, num_zero, all_sizes, num_size_words,
-                     first_ndst_word);
-  return hipGetLastError();
-}
-
-hipError_t launch_count_scan(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* status,
-                             hipStream_t s) {
-  const unsigned grid = static_cast<unsigned>(scan_tiles(h.cap_dst));
-  hipLaunchKernelGGL(k_count_scan, dim3(grid), dim3(kScanBlock), 0, s, g, ids, h.sizes, h.indptr,
-                     h.count_tiles, h.count_ticket, h.fanout, status);
+hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, uint32_t* table,
+                            uint32_t* status, hipStream_t s) {
+#define GMB_SEED(V) \
+  hipLaunchKernelGGL(k_seed_scan<V>, dim3(1), dim3(kSeedBlock), 0, s, a, g, table, status)
+  switch (num_values) {
+    case 1: GMB_SEED(1); break;
+    case 2: GMB_SEED(2); break;
+    case 3: GMB_SEED(3); break;
+    case 4: GMB_SEED(4); break;
+    case 5: GMB_SEED(5); break;
+    case 6: GMB_SEED(6); break;
+    case 7: GMB_SEED(7); break;
+    case 8: GMB_SEED(8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef GMB_SEED
   return hipGetLastError();
 }
 
 hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* table,
-                         uint32_t* status, uint32_t k0, uint32_t k1, hipStream_t s) {
+                         uint32_t* status, uint32_t k0, uint32_t k1, int first_hop, hipStream_t s) {
   const int f = h.fanout;
 #define GMB_LAUNCH_SAMPLE(G)                                                                       \
   hipLaunchKernelGGL(k_sample<G>, dim3(grid_for(h.cap_dst * (G))), dim3(256), 0, s, g, ids, h.sizes, \
-                     h.indptr, h.nbr, table, status, f, h.layer, k0, k1)
+                     h.indptr, h.nbr, table, status, f, h.layer, k0, k1, first_hop)
   if (f <= 8) GMB_LAUNCH_SAMPLE(8);
   else if (f <= 16) GMB_LAUNCH_SAMPLE(16);
   else if (f <= 32) GMB_LAUNCH_SAMPLE(32);
   else if (f <= 64) GMB_LAUNCH_SAMPLE(64);
   else
     hipLaunchKernelGGL(k_sample_wide, dim3(grid_for(h.cap_dst)), dim3(256), 0, s, g, ids, h.sizes,
-                       h.indptr, h.nbr, table, status, f, h.layer, k0, k1);
+                       h.indptr, h.nbr, table, status, f, h.layer, k0, k1, first_hop);
 #undef GMB_LAUNCH_SAMPLE
   return hipGetLastError();
 }
 
-hipError_t launch_assign(const HopArgs& h, int32_t* ids, uint32_t* table, int64_t num_nodes,
-                         hipStream_t s) {
-  const unsigned grid = static_cast<unsigned>(scan_tiles(h.cap_nnz));
-  hipLaunchKernelGGL(k_assign, dim3(grid), dim3(kScanBlock), 0, s, h.nbr, h.sizes, h.next_sizes, ids,
-                     table, num_nodes, h.flag_tiles, h.flag_ticket);
-  return hipGetLastError();
-}
-
-hipError_t launch_local(const HopArgs* hops, int num_hops, const int32_t* ids, int32_t num_seeds,
-                        const uint32_t* table, int64_t num_nodes, uint32_t* status, hipStream_t s) {
-  LocalArgs a{};
-  int64_t blocks = 0;
-  for (int i = 0; i < num_hops; ++i) {
-    a.seg[i].nbr = hops[i].nbr;
-    a.seg[i].local = hops[i].local;
-    a.seg[i].sizes = hops[i].sizes;
-    a.seg[i].first_block = blocks;
-    blocks += (hops[i].cap_nnz + 255) / 256;
+hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
+                         int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s) {
+  const unsigned grid = static_cast<unsigned>(scan_tiles(cap_nnz));
+#define GMB_ASSIGN(V) \
+  hipLaunchKernelGGL(k_assign<V>, dim3(grid), dim3(kScanBlock), 0, s, a, g, ids, table, status)
+  switch (num_values) {
+    case 1: GMB_ASSIGN(1); break;
+    case 2: GMB_ASSIGN(2); break;
+    case 3: GMB_ASSIGN(3); break;
+    case 4: GMB_ASSIGN(4); break;
+    case 5: GMB_ASSIGN(5); break;
+    case 6: GMB_ASSIGN(6); break;
+    case 7: GMB_ASSIGN(7); break;
+    case 8: GMB_ASSIGN(8); break;
+    default: return hipErrorInvalidValue;
   }
-  a.num_seg = num_hops;
-  a.seed_first_block = blocks;
-  blocks += (num_seeds + 255) / 256;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_local, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a, ids, num_seeds,
-                     table, num_nodes, status);
+#undef GMB_ASSIGN
   return hipGetLastError();
 }
 

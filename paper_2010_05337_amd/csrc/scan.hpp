@@ -87,6 +87,103 @@ __device__ int32_t tile_lookback_wave(uint64_t* tiles, int tile, int32_t aggrega
   return exclusive;
 }
 
+// Exclusive scans of NV values per thread over a block of BLOCK threads;
+// `smem` holds NV * BLOCK/64 ints.  Every thread of the block must call it.
+template <int BLOCK, int NV>
+__device__ __forceinline__ void block_exclusive_scan_multi(const int32_t (&x)[NV], int32_t (&excl)[NV],
+                                                           int32_t (&total)[NV], int32_t* smem) {
+  constexpr int W = BLOCK / 64;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int32_t inc[NV];
+#pragma unroll
+  for (int a = 0; a < NV; ++a) inc[a] = wave_inclusive_scan(x[a]);
+  if (lane == 63) {
+#pragma unroll
+    for (int a = 0; a < NV; ++a) smem[a * W + wave] = inc[a];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < NV; ++a) {
+    int32_t before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      const int32_t s = smem[a * W + w];
+      before += (w < wave) ? s : 0;
+      all += s;
+    }
+    excl[a] = before + inc[a] - x[a];
+    total[a] = all;
+  }
+  __syncthreads();
+}
+
+// Decoupled look-back over NV independent scans at once (array a of the
+// look-back words starts at tiles + a * stride).  Called by the whole first
+// wave of a tile; the rules are those of tile_lookback_wave, per array.
+template <int NV>
+__device__ void tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
+                                    const int32_t (&aggregate)[NV], int32_t (&exclusive)[NV]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int a = 0; a < NV; ++a) exclusive[a] = 0;
+  if (tile == 0) {
+    if (lane == 0) {
+#pragma unroll
+      for (int a = 0; a < NV; ++a)
+        publish_tile(tiles + a * stride, 0, kTilePrefix | static_cast<uint32_t>(aggregate[a]));
+    }
+    return;
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int a = 0; a < NV; ++a)
+      publish_tile(tiles + a * stride, tile, kTileAggregate | static_cast<uint32_t>(aggregate[a]));
+  }
+  bool done[NV];
+#pragma unroll
+  for (int a = 0; a < NV; ++a) done[a] = false;
+  for (int base = tile - 1;; base -= 64) {
+    const int t = base - lane;
+    uint64_t w[NV];
+#pragma unroll
+    for (int a = 0; a < NV; ++a)
+      w[a] = t >= 0 ? __hip_atomic_load(&tiles[a * stride + t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                    : kTilePrefix;
+    for (;;) {
+      bool pending = false;
+#pragma unroll
+      for (int a = 0; a < NV; ++a) pending |= !done[a] && (w[a] >> 62) == 0;
+      if (!__any(pending)) break;
+      __builtin_amdgcn_s_sleep(1);
+      // re-read the whole window of every open scan (a word only ever moves
+      // from nothing to aggregate to prefix, so re-reading is harmless)
+#pragma unroll
+      for (int a = 0; a < NV; ++a)
+        if (!done[a] && t >= 0)
+          w[a] = __hip_atomic_load(&tiles[a * stride + t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    bool all_done = true;
+#pragma unroll
+    for (int a = 0; a < NV; ++a) {
+      if (done[a]) continue;
+      const uint64_t prefixes = __ballot((w[a] >> 62) == 2);
+      const int stop = prefixes ? __ffsll(static_cast<long long>(prefixes)) - 1 : 63;
+      int32_t v = lane <= stop ? static_cast<int32_t>(static_cast<uint32_t>(w[a])) : 0;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+      exclusive[a] += v;
+      if (prefixes) done[a] = true;
+      else all_done = false;
+    }
+    if (all_done) break;
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int a = 0; a < NV; ++a)
+      publish_tile(tiles + a * stride, tile, kTilePrefix | static_cast<uint32_t>(exclusive[a] + aggregate[a]));
+  }
+}
+
 // Claims the next tile number for this workgroup (thread 0 takes a ticket,
 // the block reads it from LDS).
 __device__ __forceinline__ int claim_tile(uint32_t* counter, int* s_tile) {

@@ -210,3 +210,14 @@ def test_forward_wide_model_f32(orc, dg):
     w = dg.sage_weights([100, 256, 256, 47], 23)
     seeds = dg.permutation(30000, 24)[:256]
     _forward_case(orc, dg, g, feats, w, seeds, [15, 10, 5], 25, TOL_F32)
+
+
+@pytest.mark.parametrize("dims,fanouts", [([8, 300, 20], [6, 3]), ([64, 130, 12], [4, 7]),
+                                          ([128, 64, 40, 3], [3, 2, 5])])
+def test_forward_more_shapes_f32(orc, dg, tiny, dims, fanouts):
+    """Output widths above 256 (several column tiles), a narrow input, and
+    deep small layers."""
+    feats = dg.features(10000, dims[0], 31, "f32")
+    w = dg.sage_weights(dims, 32)
+    seeds = dg.permutation(10000, 33)[:150]
+    _forward_case(orc, dg, tiny, feats, w, seeds, fanouts, 34, TOL_F32)
