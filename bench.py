@@ -45,6 +45,10 @@ def parse():
                     help="print a markdown summary of a rocprofv3 CSV run of this script "
                          "(PREFIX_kernel_stats.csv, PREFIX_kernel_trace.csv) and exit; --steps "
                          "and --warmup must match that run")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the HBM traffic of the gather and copy kernels from two rocprofv3 "
+                         "--pmc runs of this script (FETCH_SIZE, then WRITE_SIZE; CSV output "
+                         "under each directory) as JSON and exit")
     ap.add_argument("--streams", type=int, default=4,
                     help="mini-batches in flight: batch i runs on stream i %% streams, each stream "
                          "with its own sampler state and workspaces")
@@ -108,10 +112,100 @@ def summarize_profile(args):
     print("\n".join(out))
 
 
+COPY_BYTES = 1 << 30   # the plain copy that calibrates bandwidth and HBM counters
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gather_products2m_traffic.json")
+GATHER_SOURCE = os.path.join(ROOT, "paper_2010_05337_amd", "csrc", "gather.hip")
+
+
+def _source_digest(path: str) -> str:
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _pmc_per_dispatch(d: str, counter: str):
+    """{kernel name: [value of `counter` per dispatch]} from the
+    counter_collection CSV files rocprofv3 wrote under `d`."""
+    import csv
+    import glob
+    acc = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r.get("Counter_Name") != counter:
+                continue
+            name = r["Kernel_Name"].replace("gmb::(anonymous namespace)::", "").replace("void ", "")
+            per = acc.setdefault(name, {})
+            key = r.get("Dispatch_Id", str(len(per)))
+            per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    return {k: list(v.values()) for k, v in acc.items()}
+
+
+def summarize_pmc(args):
+    """HBM bytes per launch of the gather kernel from FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch), each scaled by the factor that makes the
+    same counter read the known size of the plain copy (COPY_BYTES read,
+    COPY_BYTES written) in the same run.  The copy's dispatches are the
+    copy-kernel dispatches within 20% of the largest."""
+    fetch = _pmc_per_dispatch(args.summarize_pmc[0], "FETCH_SIZE")
+    write = _pmc_per_dispatch(args.summarize_pmc[1], "WRITE_SIZE")
+
+    def gather(tab):
+        ks = [k for k in tab if "k_gather" in k]
+        if not ks:
+            raise SystemExit("no gather dispatches in the counter files")
+        v = [x for k in ks for x in tab[k]]
+        return ks[0].split("(")[0], sum(v) / len(v), len(v)
+
+    def copy(tab):
+        v = [x for k in tab if "copyBuffer" in k for x in tab[k]]
+        if not v:
+            raise SystemExit("no copy-kernel dispatches in the counter files")
+        big = [x for x in v if x >= 0.8 * max(v)]
+        return sum(big) / len(big), len(big)
+    gk, g_fetch, n_gf = gather(fetch)
+    _, g_write, n_gw = gather(write)
+    c_fetch, n_cf = copy(fetch)
+    c_write, n_cw = copy(write)
+    f_fetch = COPY_BYTES / (1024.0 * c_fetch)
+    f_write = COPY_BYTES / (1024.0 * c_write)
+    out = {"kernel": gk, "copy_bytes": COPY_BYTES,
+           "fetch_kib_per_launch": g_fetch, "write_kib_per_launch": g_write,
+           "gather_dispatches": [n_gf, n_gw], "copy_dispatches": [n_cf, n_cw],
+           "copy_fetch_kib": c_fetch, "copy_write_kib": c_write,
+           "fetch_scale": f_fetch, "write_scale": f_write,
+           "traffic_bytes_per_launch": 1024.0 * (g_fetch * f_fetch + g_write * f_write),
+           "gather_source_sha256_16": _source_digest(GATHER_SOURCE)}
+    # the benchmark line of the FETCH_SIZE run, if saved next to its CSV
+    try:
+        with open(os.path.join(args.summarize_pmc[0], "bench.json")) as f:
+            alg = json.loads(f.read().strip().splitlines()[-1])["roofline"]["alg_bytes_per_launch"]
+        out["alg_bytes_per_launch"] = alg
+        out["traffic_over_alg"] = out["traffic_bytes_per_launch"] / alg
+    except (OSError, ValueError, KeyError, IndexError):
+        pass
+    print(json.dumps(out, indent=1))
+
+
+def gather_traffic():
+    """Measured HBM bytes per gather launch, if the stored counter summary
+    was taken on the current gather kernel; otherwise None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("gather_source_sha256_16") != _source_digest(GATHER_SOURCE):
+        return None
+    return t["traffic_bytes_per_launch"]
+
+
 def main():
     args = parse()
     if args.summarize_profile:
         summarize_profile(args)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
@@ -224,6 +318,39 @@ def main():
         stage["gather"] += e[1].elapsed_time(e[2])
         stage["forward"] += e[2].elapsed_time(e[3])
 
+    # pass C: sampling + gather only, S streams in flight (a mini-batch
+    # loader that runs ahead of the model)
+    def step_sg(i, nstreams):
+        b = i % nb
+        ln = lanes[i % nstreams]
+        with torch.cuda.stream(streams[i % nstreams]):
+            blocks = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b),
+                                       workspace=ln["ws_sample"])
+            gmb.gather_features(blocks, feats, out=ln["x"])
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for i in range(K):
+        step_sg(i, S)
+    torch.cuda.synchronize()
+    T2 = time.perf_counter() - t2
+    for ln in lanes:
+        ln["csr"].check_status()
+
+    # a plain device copy of known size: the bandwidth a streaming kernel
+    # reaches on this GPU, and the calibration of the HBM byte counters
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ce[0].record()
+    for _ in range(5):
+        dst.copy_(src)
+    ce[1].record()
+    torch.cuda.synchronize()
+    copy_GBps = 5 * 2 * COPY_BYTES / (ce[0].elapsed_time(ce[1]) / 1e3) / 1e9
+    del src, dst
+
     # sizes per batch (sampling is a pure function of the batch and its key)
     seeds_total = edges_total = 0
     b_sample = b_gather = b_fwd = flops = 0
@@ -270,9 +397,14 @@ def main():
                             "stage_ms_per_step": {k: v / K for k, v in stage.items()}}
     res["gather_GBps"] = b_gather / tg / 1e9
     res["sampling_edges_per_s"] = edges_total / ts
+    # isolated: stage times of pass B; pipelined: pass C wall time
     res["sample_gather_hbm"] = {"alg_bytes": b_sample + b_gather,
                                 "GBps": (b_sample + b_gather) / (ts + tg) / 1e9,
-                                "frac_of_peak": (b_sample + b_gather) / (ts + tg) / 1e9 / HBM_PEAK_GBPS}
+                                "frac_of_peak": (b_sample + b_gather) / (ts + tg) / 1e9 / HBM_PEAK_GBPS,
+                                "pipelined_GBps": (b_sample + b_gather) / T2 / 1e9,
+                                "pipelined_frac_of_peak": (b_sample + b_gather) / T2 / 1e9 / HBM_PEAK_GBPS,
+                                "pipelined_streams": S}
+    res["stream_copy_GBps"] = copy_GBps
     peak = BF16_MFMA_PEAK_TFLOPS if bf16 else FP32_MFMA_PEAK_TFLOPS
     res["forward"] = {"alg_bytes": b_fwd, "linear_flops": flops,
                       "linear_TFLOPs_lower_bound": flops / tf / 1e12, "mfma_peak_TFLOPs": peak}
@@ -280,7 +412,7 @@ def main():
     # timed in the isolated pass (launches W+K .. W+2K-1 of the run)
     res["roofline"] = {"kernel": "k_gather", "bound": "hbm",
                        "achieved": b_gather / tg / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                       "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": None,
+                       "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": gather_traffic(),
                        "alg_bytes_per_launch": b_gather / K, "avg_launch_ms": 1e3 * tg / K,
                        "launches": f"{args.warmup + K}..{args.warmup + 2 * K - 1} (pass B)"}
 
