@@ -56,7 +56,7 @@ typedef enum { GMB_F32 = 0, GMB_BF16 = 1 } gmb_dtype;
 /* Bits of the device status word. */
 #define GMB_STATUS_ERANGE 1u
 #define GMB_STATUS_EDUP 2u
-#define GMB_STATUS_INTERNAL 4u   /* a bounded wait inside the relabel step ran out */
+#define GMB_STATUS_INTERNAL 4u   /* a bounded wait inside the relabel scan ran out */
 
 /* In-neighbour CSR of the input graph G(V, E) (Section II-A): row v lists
  * the sources u of the edges u -> v, so sampling row v samples the vertices

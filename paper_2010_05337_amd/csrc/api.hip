@@ -58,12 +58,12 @@ struct SamplePlan {
   HopPlan hop[GMB_MAX_LAYERS];
   size_t off_ids, off_sizes, off_zero;
   int64_t num_zero_words;
-  int32_t num_size_words;   // 4 per layer, then the segment-totals matrix
+  int32_t num_size_words;   // 4 per layer, then the running edge count of every hop
   int64_t cap_ids;
   size_t total;
 };
 
-constexpr int kTotalsWords = GMB_MAX_LAYERS * GMB_MAX_LAYERS;
+constexpr int kTotalsWords = GMB_MAX_LAYERS;
 
 // Fills the plan; returns GMB_OK or an argument error (message set).
 int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers, int64_t num_nodes,
@@ -222,7 +222,7 @@ int gmb_read_status(void* state, void* stream) {
   if (word & GMB_STATUS_ERANGE) return fail(GMB_ERANGE, "a vertex id outside [0, num_nodes) was found on the device");
   if (word & GMB_STATUS_EDUP) return fail(GMB_EDUP, "the seed list holds a vertex more than once");
   if (word & GMB_STATUS_INTERNAL)
-    return fail(GMB_EDEVICE, "a bounded wait in the relabel step ran out (local ids set to -1)");
+    return fail(GMB_EDEVICE, "a bounded wait in the relabel scan ran out (the blocks of that call are wrong)");
   return ok();
 }
 
@@ -316,7 +316,10 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
   hipError_t e = gmb::launch_seed_scan(sa, num_layers, g, table, status, s);
   if (e != hipSuccess) return hip_fail(e, "seed launch");
   for (int h = 0; h < num_layers; ++h) {
-    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, h == 0 ? 1 : 0, s);
+    // the first hop has nothing deferred: word 3 of a block's sizes is 0
+    gmb::DeferredArgs fix{hops[0].local, hops[0].sizes + 3 - gmb::kNnz, 1};
+    if (h > 0) fix = gmb::DeferredArgs{hops[h - 1].local, hops[h - 1].sizes, std::max<int64_t>(hops[h - 1].cap_nnz, 1)};
+    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, h == 0 ? 1 : 0, fix, s);
     if (e != hipSuccess) return hip_fail(e, "sample launch");
     gmb::AssignArgs aa{};
     aa.nbr = hops[h].nbr;
@@ -335,7 +338,9 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
     e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, ids, table, status, s);
     if (e != hipSuccess) return hip_fail(e, "relabel launch");
   }
-  e = gmb::launch_cleanup(ids, sizes + 4 * 0, p.cap_ids, table, csr->num_nodes, s);
+  const gmb::HopArgs& last = hops[num_layers - 1];
+  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, table, csr->num_nodes,
+                          gmb::DeferredArgs{last.local, last.sizes, std::max<int64_t>(last.cap_nnz, 1)}, s);
   if (e != hipSuccess) return hip_fail(e, "cleanup launch");
   *out = res;
   return ok();

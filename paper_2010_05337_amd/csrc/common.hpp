@@ -38,6 +38,21 @@ __device__ __forceinline__ void row_range(const CsrView& g, int32_t v, int64_t& 
   }
 }
 
+// The same with the row-offset width known at compile time (no branch
+// between the reads of a batch).
+template <bool WIDE>
+__device__ __forceinline__ void row_range_t(const CsrView& g, int32_t v, int64_t& begin, int64_t& end) {
+  if constexpr (WIDE) {
+    const int64_t* p = static_cast<const int64_t*>(g.indptr);
+    begin = p[v];
+    end = p[v + 1];
+  } else {
+    const int32_t* p = static_cast<const int32_t*>(g.indptr);
+    begin = p[v];
+    end = p[v + 1];
+  }
+}
+
 __device__ __forceinline__ bool valid_vertex(int32_t v, int64_t n) {
   return v >= 0 && static_cast<int64_t>(v) < n;
 }

@@ -40,9 +40,9 @@ constexpr int kScanTile = kScanBlock * kScanItems;
 inline int64_t scan_tiles(int64_t n) { return n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile; }
 
 // Arguments of the seed kernel (segment 0: the seeds).  Per hop v:
-// indptr[v] its block row offsets, fanout[v] its fan-out.  totals is the
-// [GMB_MAX_LAYERS][GMB_MAX_LAYERS] matrix of segment totals (row =
-// segment, column = hop), cleared with the size words.
+// indptr[v] its block row offsets, fanout[v] its fan-out.  totals[v] is
+// hop v's edge count over the segments placed so far (GMB_MAX_LAYERS
+// words after the size words, cleared with them).
 struct SeedArgs {
   const int32_t* seeds;
   int32_t num_seeds;
@@ -50,7 +50,7 @@ struct SeedArgs {
   int32_t* ids;
   uint64_t* zero;
   int64_t num_zero;
-  int32_t* sizes;        // every size word, then the totals matrix
+  int32_t* sizes;        // every size word, then the totals
   int32_t num_size_words;
   int32_t* totals;
   int32_t* indptr[GMB_MAX_LAYERS];
@@ -73,16 +73,27 @@ struct AssignArgs {
   int32_t fanout[GMB_MAX_LAYERS];
 };
 
+// Local ids that a hop's relabel left deferred (entries -(e0 + 1): copy the
+// local id of edge e0); the next kernel on the stream resolves them.  The
+// edge count is sizes[kNnz]; cap (>= 1) bounds it and every read of local.
+// Nothing to resolve: any local array of cap entries and an edge count of 0.
+struct DeferredArgs {
+  int32_t* local;
+  const int32_t* sizes;
+  int64_t cap;
+};
+
 // sample.hip
 hipError_t launch_state_init(uint32_t* table, uint32_t* status, int64_t num_nodes, hipStream_t s);
 hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, uint32_t* table,
                             uint32_t* status, hipStream_t s);
 hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* table,
-                         uint32_t* status, uint32_t k0, uint32_t k1, int first_hop, hipStream_t s);
+                         uint32_t* status, uint32_t k0, uint32_t k1, int first_hop,
+                         const DeferredArgs& fix, hipStream_t s);
 hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
                          int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s);
 hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src,
-                          uint32_t* table, int64_t num_nodes, hipStream_t s);
+                          uint32_t* table, int64_t num_nodes, const DeferredArgs& fix, hipStream_t s);
 
 // gather.hip
 hipError_t launch_gather(const int32_t* ids, const int32_t* n_dev, int64_t n_cap, const void* feats,

@@ -26,6 +26,8 @@
 //                 n_dst + rank) together with the degree scans of the new
 //                 vertices for the later hops; writes every edge's local id
 //   k_cleanup     table entries of every vertex of the batch back to empty
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "philox.hpp"
@@ -74,7 +76,7 @@ __global__ __launch_bounds__(256) void k_state_init(uint32_t* table, uint32_t* s
 constexpr int kSeedBlock = 512;
 constexpr int kSeedItems = 4;
 
-template <int NV>
+template <int NV, bool WIDE>
 __global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga, uint32_t* table,
                                                           uint32_t* status) {
   __shared__ int32_t s_wave[NV * (kSeedBlock / 64)];
@@ -100,10 +102,11 @@ __global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga
 #pragma unroll
     for (int q = 0; q < kSeedItems; ++q) {
       const int32_t p = base + tid * kSeedItems + q;
-      const int32_t s = p < B ? a.seeds[p] : -1;
-      int64_t b = 0, e = 0;
-      if (valid_vertex(s, g.num_nodes)) row_range(g, s, b, e);
-      deg[q] = static_cast<int32_t>(e - b);
+      const int32_t s = a.seeds[p < B ? p : (B > 0 ? B - 1 : 0)];
+      const bool ok = p < B && valid_vertex(s, g.num_nodes);
+      int64_t b, e;
+      row_range_t<WIDE>(g, ok ? s : 0, b, e);
+      deg[q] = ok ? static_cast<int32_t>(e - b) : 0;
     }
     int32_t sum[NV], excl[NV], total[NV];
 #pragma unroll
@@ -127,7 +130,7 @@ __global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga
   }
   if (tid == 0) {
 #pragma unroll
-    for (int v = 0; v < NV; ++v) a.totals[v] = running[v];   // segment 0 (row 0), hop v
+    for (int v = 0; v < NV; ++v) a.totals[v] = running[v];   // segment 0's edges of hop v
     // hop 0 has one segment: its sizes are known now
     a.sizes[a.first_sizes + kNDst] = B;
     a.sizes[a.first_sizes + kNnz] = running[0];
@@ -135,44 +138,90 @@ __global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga
   }
 }
 
+// Emits edge `pos` (sampled vertex u) and records it in the dedup table.
+// With GMB_EMIT_PREREAD the table is read first: entries only decrease
+// during the kernel, so a read that is already <= the edge's tag proves the
+// atomic would change nothing and it is skipped.
+#ifndef GMB_EMIT_PREREAD
+#define GMB_EMIT_PREREAD 1
+#endif
 __device__ __forceinline__ void emit_edge(int32_t pos, int32_t u, int32_t* nbr, uint32_t* table,
                                           int64_t num_nodes, uint32_t* status) {
   nbr[pos] = u;
   if (valid_vertex(u, num_nodes)) {
     const uint32_t tag = kEdgeTag | static_cast<uint32_t>(pos);
-    // Entries only decrease during the kernel, so a stale read that is
-    // already <= tag proves the atomic would not change anything.
-    if (table[u] > tag) atomicMin(&table[u], tag);
+    if (!GMB_EMIT_PREREAD || table[u] > tag) atomicMin(&table[u], tag);
   } else {
     raise_status(status, GMB_STATUS_ERANGE);
   }
+}
+
+// Deferred local ids of the previous hop (written by its relabel as
+// -(e0 + 1), e0 = the vertex's first edge, in an earlier tile): edge e
+// takes the local id of edge e0, final since that relabel ended.  One edge
+// per thread.  The reads are unconditional (clamped indices; the first hop
+// passes an edge count of 0) so that they overlap with the caller's.
+struct DeferredItem {
+  int32_t n, x, y;
+};
+
+// First read: the edge count and the edge's entry.
+__device__ __forceinline__ DeferredItem deferred_read(const DeferredArgs& fix, int64_t e) {
+  DeferredItem it;
+  it.n = load_size(&fix.sizes[kNnz]);
+  it.x = fix.local[e < fix.cap ? e : fix.cap - 1];
+  it.y = 0;
+  return it;
+}
+
+// Second read: the entry of the first occurrence (entry 0 when nothing is
+// deferred).
+__device__ __forceinline__ void deferred_fetch(const DeferredArgs& fix, DeferredItem& it) {
+  const int32_t e0 = it.x < 0 ? -(it.x + 1) : 0;
+  it.y = fix.local[e0 < it.n ? e0 : 0];
+}
+
+__device__ __forceinline__ void deferred_store(const DeferredArgs& fix, int64_t e, const DeferredItem& it) {
+  if (e < it.n && it.x < 0) fix.local[e] = it.y;
 }
 
 // G lanes per destination (G >= fanout, G a power of two <= 64): lane i
 // draws t_i uniform in [0, j_i], j_i = d - f + i; Floyd's rule is then
 // resolved in draw order with one group-wide vote per step (x_s = t_s
 // unless an earlier lane already holds t_s, then x_s = j_s), and every lane
-// finds the rank of its slot among the group's.
-template <int G>
+// finds the rank of its slot among the group's.  The grid also covers the
+// previous hop's edges for the deferred local ids.
+template <int G, bool WIDE>
 __global__ __launch_bounds__(256) void k_sample(CsrArgs ga, const int32_t* ids, const int32_t* sizes,
-                                                const int32_t* blk_indptr, int32_t* nbr,
-                                                uint32_t* table, uint32_t* status, int fanout,
-                                                int layer, uint32_t k0, uint32_t k1, int check_seeds) {
+                                                const int32_t* blk_indptr, int64_t cap_dst,
+                                                int32_t* nbr, uint32_t* table, uint32_t* status,
+                                                int fanout, int layer, uint32_t k0, uint32_t k1,
+                                                int check_seeds, DeferredArgs fix) {
   const CsrView g = view(ga);
-  const int64_t p = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
+  const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t p = tid / G;
   const int lane = threadIdx.x & (G - 1);
+  // the first reads do not depend on each other: a position past the
+  // capacity reads the last one and is dropped below
+  const int64_t pc = p < cap_dst ? p : cap_dst - 1;
   const int32_t n_dst = load_size(&sizes[kNDst]);
-  if (p >= n_dst) return;
-  const int32_t v = ids[p];
-  if (!valid_vertex(v, g.num_nodes)) return;   // its clamped degree was 0
+  const int32_t v = ids[pc];
+  const int32_t off = blk_indptr[pc];
+  DeferredItem it = deferred_read(fix, tid);
+  // second round, again independent reads: the deferred edge's source
+  // entry, the seed's table slot (first hop) and the row of v
+  const bool valid = valid_vertex(v, g.num_nodes);
+  const int32_t vc = valid ? v : 0;
+  deferred_fetch(fix, it);
+  const uint32_t slot = check_seeds ? table[vc] : 0u;
   int64_t begin, end;
-  row_range(g, v, begin, end);
-  const int64_t d = end - begin;
-  const int32_t off = blk_indptr[p];
+  row_range_t<WIDE>(g, vc, begin, end);
+  deferred_store(fix, tid, it);
+  if (p >= n_dst || !valid) return;   // an invalid vertex's clamped degree was 0
   // first hop: every seed owns its table slot unless the seed list holds
   // the vertex twice (the slot then names the first copy)
-  if (check_seeds && lane == 0 && table[v] != static_cast<uint32_t>(p))
-    raise_status(status, GMB_STATUS_EDUP);
+  if (check_seeds && lane == 0 && slot != static_cast<uint32_t>(p)) raise_status(status, GMB_STATUS_EDUP);
+  const int64_t d = end - begin;
 
   int32_t pos = -1, u = 0;
   if (d <= fanout) {
@@ -213,9 +262,14 @@ __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* 
                                                      const int32_t* sizes, const int32_t* blk_indptr,
                                                      int32_t* nbr, uint32_t* table, uint32_t* status,
                                                      int fanout, int layer, uint32_t k0, uint32_t k1,
-                                                     int check_seeds) {
+                                                     int check_seeds, DeferredArgs fix) {
   const CsrView g = view(ga);
   const int64_t p = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  {
+    DeferredItem it = deferred_read(fix, p);
+    deferred_fetch(fix, it);
+    deferred_store(fix, p, it);
+  }
   const int32_t n_dst = load_size(&sizes[kNDst]);
   if (p >= n_dst) return;
   const int32_t v = ids[p];
@@ -258,16 +312,16 @@ __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* 
 // becomes source n_dst + rank, is appended to ids and gets its local id in
 // the table.  Value 0 of the scan counts them; value v >= 1 carries the
 // new vertices' clamped degrees for hop h + v, which become those hops'
-// block row offsets.  Every edge's local id is written here: a vertex seen
-// before this hop has it in the table; a repeat of a vertex that is new in
-// this hop takes it from LDS when the first occurrence is in the same tile,
-// else from the table once the earlier tile has stored it (that tile holds
-// an earlier ticket, so it is running and never waits on this one).  Other
-// tiles may read table[u] while it is rewritten: they see either a tag or
-// the local id, never their own tag, so their flag is 0 either way.
-constexpr int kSpinLimit = 1 << 22;
-
-template <int NV>
+// block row offsets.  Every edge's local id is written here, or deferred:
+// a vertex seen before this hop has it in the table; a repeat of a vertex
+// that is new in this hop takes it from LDS when the first occurrence is in
+// the same tile, else it stores -(e0 + 1) (e0 = the first occurrence) and
+// the next kernel on the stream copies local[e0].  Other tiles may read
+// table[u] while it is rewritten: they see either a tag or the local id,
+// never their own tag, so their flag is 0 either way, and either one gives
+// them the right local id; so the table store needs no ordering within
+// this kernel.
+template <int NV, bool WIDE>
 __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga, int32_t* ids,
                                                        uint32_t* table, uint32_t* status) {
   __shared__ int s_tile;
@@ -275,54 +329,56 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
   __shared__ int32_t s_wave[NV * (kScanBlock / 64)];
   __shared__ int32_t s_pos[kScanTile];
   const CsrView g = view(ga);
+  // row offsets of hop h + v start after the edges of segments 0..h
+  // (final before this kernel; read early, used after the look-back)
+  int32_t basev[NV];
+#pragma unroll
+  for (int v = 1; v < NV; ++v) basev[v] = a.totals[a.hop + v];
   const int32_t n = load_size(&a.sizes[kNnz]);
   const int32_t n_dst = load_size(&a.sizes[kNDst]);
-  const int num_tiles = n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile;
   const int tile = claim_tile(a.ticket, &s_tile);
+  const int num_tiles = n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile;
   if (tile >= num_tiles) return;
 
   const int64_t tile_base = static_cast<int64_t>(tile) * kScanTile;
   const int64_t base = tile_base + threadIdx.x * kScanItems;
   int32_t u[kScanItems];
   load_items(a.nbr, base, n, u);
+  // table entries and (for the later hops) the degrees of every item, in
+  // one round of reads; an invalid item reads vertex 0 and is dropped
   uint32_t t[kScanItems];
+  int32_t deg[kScanItems];
 #pragma unroll
   for (int q = 0; q < kScanItems; ++q) {
     const bool ok = (base + q < n) & valid_vertex(u[q], g.num_nodes);
     u[q] = ok ? u[q] : -1;
-    t[q] = table[u[q] < 0 ? 0 : u[q]];
+    const int32_t uc = u[q] < 0 ? 0 : u[q];
+    t[q] = table[uc];
+    deg[q] = 0;
+    if constexpr (NV > 1) {
+      int64_t b, e;
+      row_range_t<WIDE>(g, uc, b, e);
+      deg[q] = static_cast<int32_t>(e - b);
+    }
   }
   uint32_t flags = 0;
 #pragma unroll
   for (int q = 0; q < kScanItems; ++q)
     if (u[q] >= 0 && t[q] == (kEdgeTag | static_cast<uint32_t>(base + q))) flags |= 1u << q;
-  // degrees of the new vertices (a non-flagged item reads vertex 0's row
-  // and contributes nothing)
-  int32_t deg[kScanItems];
-#pragma unroll
-  for (int q = 0; q < kScanItems; ++q) deg[q] = 0;
-  if constexpr (NV > 1) {
-#pragma unroll
-    for (int q = 0; q < kScanItems; ++q) {
-      const bool f = (flags >> q) & 1u;
-      int64_t b, e;
-      row_range(g, f ? u[q] : 0, b, e);
-      deg[q] = f ? static_cast<int32_t>(e - b) : 0;
-    }
-  }
   int32_t sum[NV], thr[NV], total[NV], excl[NV];
   sum[0] = __popc(flags);
 #pragma unroll
   for (int v = 1; v < NV; ++v) {
     sum[v] = 0;
 #pragma unroll
-    for (int q = 0; q < kScanItems; ++q) sum[v] += clamp_degree(deg[q], a.fanout[v]);
+    for (int q = 0; q < kScanItems; ++q) sum[v] += ((flags >> q) & 1u) ? clamp_degree(deg[q], a.fanout[v]) : 0;
   }
   block_exclusive_scan_multi<kScanBlock, NV>(sum, thr, total, s_wave);
   if (threadIdx.x < 64) {
     int32_t ex[NV];
-    tile_lookback_multi<NV>(a.tiles, a.tile_stride, tile, total, ex);
+    const bool ok = tile_lookback_multi<NV>(a.tiles, a.tile_stride, tile, total, ex);
     if (threadIdx.x == 0) {
+      if (!ok) raise_status(status, GMB_STATUS_INTERNAL);
 #pragma unroll
       for (int v = 0; v < NV; ++v) s_excl[v] = ex[v];
     }
@@ -331,13 +387,6 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
 #pragma unroll
   for (int v = 0; v < NV; ++v) excl[v] = s_excl[v];
 
-  // row offsets of hop h + v start after the earlier segments' totals
-  int32_t basev[NV];
-#pragma unroll
-  for (int v = 1; v < NV; ++v) {
-    basev[v] = 0;
-    for (int i = 0; i <= a.hop; ++i) basev[v] += a.totals[i * GMB_MAX_LAYERS + a.hop + v];
-  }
   // new vertices: position, ids, table, local id, later hops' row offsets
   int32_t r = n_dst + excl[0] + thr[0];
   int32_t run[NV];
@@ -348,7 +397,7 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
     if ((flags >> q) & 1u) {
       ids[r] = u[q];
       a.local[base + q] = r;
-      __hip_atomic_store(&table[u[q]], static_cast<uint32_t>(r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      table[u[q]] = static_cast<uint32_t>(r);   // read by later kernels only
       s_pos[threadIdx.x * kScanItems + q] = r;
 #pragma unroll
       for (int v = 1; v < NV; ++v) {
@@ -359,31 +408,20 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
     }
   }
   __syncthreads();
-  bool lost = false;
+#pragma unroll
   for (int q = 0; q < kScanItems; ++q) {
     if (base + q >= n || ((flags >> q) & 1u)) continue;
-    int32_t loc = -1;
+    int32_t loc = 0;   // an invalid vertex (reported by the sampling) gets 0
     if (u[q] >= 0) {
       if (t[q] < kEdgeTag) {
         loc = static_cast<int32_t>(t[q]);
       } else {
         const int64_t e0 = t[q] & ~kEdgeTag;
-        if (e0 >= tile_base) {
-          loc = s_pos[e0 - tile_base];
-        } else {
-          uint32_t x = __hip_atomic_load(&table[u[q]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          for (int spin = 0; x >= kEdgeTag && spin < kSpinLimit; ++spin) {
-            __builtin_amdgcn_s_sleep(2);
-            x = __hip_atomic_load(&table[u[q]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
-          lost |= x >= kEdgeTag;
-          loc = x < kEdgeTag ? static_cast<int32_t>(x) : -1;
-        }
+        loc = e0 >= tile_base ? s_pos[e0 - tile_base] : -static_cast<int32_t>(e0) - 1;
       }
     }
     a.local[base + q] = loc;
   }
-  if (lost) raise_status(status, GMB_STATUS_INTERNAL);
   if (tile == num_tiles - 1 && threadIdx.x == 0) {
     const int32_t n_src = n_dst + excl[0] + total[0];
     a.sizes[kNSrc] = n_src;
@@ -392,8 +430,7 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
       if constexpr (NV > 1) {
         // this hop's new vertices are segment h + 1
 #pragma unroll
-        for (int v = 1; v < NV; ++v)
-          a.totals[(a.hop + 1) * GMB_MAX_LAYERS + a.hop + v] = excl[v] + total[v];
+        for (int v = 1; v < NV; ++v) a.totals[a.hop + v] = basev[v] + excl[v] + total[v];
         // the next hop's destinations are complete: its edge count is known
         const int32_t nnz = basev[1] + excl[1] + total[1];
         a.next_sizes[kNnz] = nnz;
@@ -403,13 +440,18 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
   }
 }
 
-__global__ __launch_bounds__(256) void k_cleanup(const int32_t* ids, const int32_t* final_sizes,
-                                                 uint32_t* table, int64_t num_nodes) {
+// Resets the table entries of every vertex of the batch and resolves the
+// last hop's deferred local ids (the table is not read for those).
+__global__ __launch_bounds__(256) void k_cleanup(const int32_t* ids, int64_t cap_src,
+                                                 const int32_t* final_sizes, uint32_t* table,
+                                                 int64_t num_nodes, DeferredArgs fix) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  DeferredItem it = deferred_read(fix, i);
   const int32_t n = load_size(&final_sizes[kNSrc]);
-  if (i >= n) return;
-  const int32_t u = ids[i];
-  if (valid_vertex(u, num_nodes)) table[u] = kEmpty;
+  const int32_t u = ids[i < cap_src ? i : cap_src - 1];
+  deferred_fetch(fix, it);
+  deferred_store(fix, i, it);
+  if (i < n && valid_vertex(u, num_nodes)) table[u] = kEmpty;
 }
 
 inline unsigned grid_for(int64_t threads, int block = 256) {
@@ -430,17 +472,20 @@ hipError_t launch_state_init(uint32_t* table, uint32_t* status, int64_t num_node
 
 hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, uint32_t* table,
                             uint32_t* status, hipStream_t s) {
-#define GMB_SEED(V) \
-  hipLaunchKernelGGL(k_seed_scan<V>, dim3(1), dim3(kSeedBlock), 0, s, a, g, table, status)
+#define GMB_SEED(V)                                                                                \
+  if (g.wide)                                                                                      \
+    hipLaunchKernelGGL((k_seed_scan<V, true>), dim3(1), dim3(kSeedBlock), 0, s, a, g, table, status); \
+  else                                                                                             \
+    hipLaunchKernelGGL((k_seed_scan<V, false>), dim3(1), dim3(kSeedBlock), 0, s, a, g, table, status)
   switch (num_values) {
-    case 1: GMB_SEED(1); break;
-    case 2: GMB_SEED(2); break;
-    case 3: GMB_SEED(3); break;
-    case 4: GMB_SEED(4); break;
-    case 5: GMB_SEED(5); break;
-    case 6: GMB_SEED(6); break;
-    case 7: GMB_SEED(7); break;
-    case 8: GMB_SEED(8); break;
+    case 1: { GMB_SEED(1); } break;
+    case 2: { GMB_SEED(2); } break;
+    case 3: { GMB_SEED(3); } break;
+    case 4: { GMB_SEED(4); } break;
+    case 5: { GMB_SEED(5); } break;
+    case 6: { GMB_SEED(6); } break;
+    case 7: { GMB_SEED(7); } break;
+    case 8: { GMB_SEED(8); } break;
     default: return hipErrorInvalidValue;
   }
 #undef GMB_SEED
@@ -448,18 +493,31 @@ hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g,
 }
 
 hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* table,
-                         uint32_t* status, uint32_t k0, uint32_t k1, int first_hop, hipStream_t s) {
+                         uint32_t* status, uint32_t k0, uint32_t k1, int first_hop,
+                         const DeferredArgs& fix, hipStream_t s) {
   const int f = h.fanout;
-#define GMB_LAUNCH_SAMPLE(G)                                                                       \
-  hipLaunchKernelGGL(k_sample<G>, dim3(grid_for(h.cap_dst * (G))), dim3(256), 0, s, g, ids, h.sizes, \
-                     h.indptr, h.nbr, table, status, f, h.layer, k0, k1, first_hop)
-  if (f <= 8) GMB_LAUNCH_SAMPLE(8);
-  else if (f <= 16) GMB_LAUNCH_SAMPLE(16);
-  else if (f <= 32) GMB_LAUNCH_SAMPLE(32);
-  else if (f <= 64) GMB_LAUNCH_SAMPLE(64);
-  else
-    hipLaunchKernelGGL(k_sample_wide, dim3(grid_for(h.cap_dst)), dim3(256), 0, s, g, ids, h.sizes,
-                       h.indptr, h.nbr, table, status, f, h.layer, k0, k1, first_hop);
+  const int64_t cap_dst = h.cap_dst < 1 ? 1 : h.cap_dst;   // ids and indptr hold >= 1 entry
+  auto threads = [&](int64_t per_dst) { return std::max(h.cap_dst * per_dst, fix.cap); };
+#define GMB_LAUNCH_SAMPLE(G)                                                                     \
+  if (g.wide)                                                                                     \
+    hipLaunchKernelGGL((k_sample<G, true>), dim3(grid_for(threads(G))), dim3(256), 0, s, g, ids,  \
+                       h.sizes, h.indptr, cap_dst, h.nbr, table, status, f, h.layer, k0, k1,      \
+                       first_hop, fix);                                                           \
+  else                                                                                            \
+    hipLaunchKernelGGL((k_sample<G, false>), dim3(grid_for(threads(G))), dim3(256), 0, s, g, ids, \
+                       h.sizes, h.indptr, cap_dst, h.nbr, table, status, f, h.layer, k0, k1,      \
+                       first_hop, fix)
+  if (f <= 8) {
+    GMB_LAUNCH_SAMPLE(8);
+  } else if (f <= 16) {
+    GMB_LAUNCH_SAMPLE(16);
+  } else if (f <= 32) {
+    GMB_LAUNCH_SAMPLE(32);
+  } else if (f <= 64) {
+    GMB_LAUNCH_SAMPLE(64);
+  } else
+    hipLaunchKernelGGL(k_sample_wide, dim3(grid_for(threads(1))), dim3(256), 0, s, g, ids, h.sizes,
+                       h.indptr, h.nbr, table, status, f, h.layer, k0, k1, first_hop, fix);
 #undef GMB_LAUNCH_SAMPLE
   return hipGetLastError();
 }
@@ -467,17 +525,20 @@ hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h,
 hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
                          int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s) {
   const unsigned grid = static_cast<unsigned>(scan_tiles(cap_nnz));
-#define GMB_ASSIGN(V) \
-  hipLaunchKernelGGL(k_assign<V>, dim3(grid), dim3(kScanBlock), 0, s, a, g, ids, table, status)
+#define GMB_ASSIGN(V)                                                                               \
+  if (g.wide)                                                                                       \
+    hipLaunchKernelGGL((k_assign<V, true>), dim3(grid), dim3(kScanBlock), 0, s, a, g, ids, table, status); \
+  else                                                                                              \
+    hipLaunchKernelGGL((k_assign<V, false>), dim3(grid), dim3(kScanBlock), 0, s, a, g, ids, table, status)
   switch (num_values) {
-    case 1: GMB_ASSIGN(1); break;
-    case 2: GMB_ASSIGN(2); break;
-    case 3: GMB_ASSIGN(3); break;
-    case 4: GMB_ASSIGN(4); break;
-    case 5: GMB_ASSIGN(5); break;
-    case 6: GMB_ASSIGN(6); break;
-    case 7: GMB_ASSIGN(7); break;
-    case 8: GMB_ASSIGN(8); break;
+    case 1: { GMB_ASSIGN(1); } break;
+    case 2: { GMB_ASSIGN(2); } break;
+    case 3: { GMB_ASSIGN(3); } break;
+    case 4: { GMB_ASSIGN(4); } break;
+    case 5: { GMB_ASSIGN(5); } break;
+    case 6: { GMB_ASSIGN(6); } break;
+    case 7: { GMB_ASSIGN(7); } break;
+    case 8: { GMB_ASSIGN(8); } break;
     default: return hipErrorInvalidValue;
   }
 #undef GMB_ASSIGN
@@ -485,9 +546,10 @@ hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, 
 }
 
 hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src,
-                          uint32_t* table, int64_t num_nodes, hipStream_t s) {
-  hipLaunchKernelGGL(k_cleanup, dim3(grid_for(cap_src)), dim3(256), 0, s, ids, final_sizes, table,
-                     num_nodes);
+                          uint32_t* table, int64_t num_nodes, const DeferredArgs& fix, hipStream_t s) {
+  const int64_t threads = std::max(cap_src, fix.cap);
+  hipLaunchKernelGGL(k_cleanup, dim3(grid_for(threads)), dim3(256), 0, s, ids,
+                     std::max<int64_t>(cap_src, 1), final_sizes, table, num_nodes, fix);
   return hipGetLastError();
 }
 

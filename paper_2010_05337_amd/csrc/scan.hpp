@@ -7,7 +7,9 @@
 // published an inclusive prefix.  Tiles are numbered in the order in which
 // workgroups start (an atomic ticket), so a tile only ever waits on tiles
 // that are already running, and every tile publishes its aggregate before
-// it waits: every wait ends.
+// it waits: every wait ends.  The wait is still bounded (kLookbackSpins
+// sleeps); a tile that runs out reports it, publishes a wrong prefix (so
+// its successors still finish) and goes on.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -17,6 +19,7 @@ namespace gmb {
 
 constexpr uint64_t kTileAggregate = 1ull << 62;
 constexpr uint64_t kTilePrefix = 2ull << 62;
+constexpr int kLookbackSpins = 1 << 22;
 
 __device__ __forceinline__ int32_t wave_inclusive_scan(int32_t x) {
   const int lane = threadIdx.x & 63;
@@ -28,63 +31,8 @@ __device__ __forceinline__ int32_t wave_inclusive_scan(int32_t x) {
   return x;
 }
 
-// Exclusive scan of one value per thread over a block of BLOCK threads;
-// `smem` holds BLOCK/64 ints.  Every thread of the block must call it.
-template <int BLOCK>
-__device__ __forceinline__ int32_t block_exclusive_scan(int32_t x, int32_t& total, int32_t* smem) {
-  const int32_t inc = wave_inclusive_scan(x);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (lane == 63) smem[wave] = inc;
-  __syncthreads();
-  int32_t before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < BLOCK / 64; ++w) {
-    const int32_t s = smem[w];
-    before += (w < wave) ? s : 0;
-    all += s;
-  }
-  __syncthreads();
-  total = all;
-  return before + inc - x;
-}
-
 __device__ __forceinline__ void publish_tile(uint64_t* tiles, int tile, uint64_t word) {
   __hip_atomic_store(&tiles[tile], word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Called by the whole first wave of a tile (threadIdx.x < 64).  Publishes
-// the tile's aggregate, resolves the tile's exclusive prefix from its
-// predecessors 64 at a time (lane i reads tile - 1 - i; a predecessor that
-// has published nothing yet is re-read until it has), publishes the
-// inclusive prefix and returns the exclusive one to every lane.  Values
-// are non-negative and below 2^31.
-__device__ int32_t tile_lookback_wave(uint64_t* tiles, int tile, int32_t aggregate) {
-  const int lane = threadIdx.x & 63;
-  if (tile == 0) {
-    if (lane == 0) publish_tile(tiles, 0, kTilePrefix | static_cast<uint32_t>(aggregate));
-    return 0;
-  }
-  if (lane == 0) publish_tile(tiles, tile, kTileAggregate | static_cast<uint32_t>(aggregate));
-  int32_t exclusive = 0;
-  for (int base = tile - 1;; base -= 64) {
-    const int t = base - lane;
-    uint64_t w = kTilePrefix;   // before tile 0: a prefix of 0
-    if (t >= 0) w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    while (__any((w >> 62) == 0)) {
-      __builtin_amdgcn_s_sleep(1);
-      if ((w >> 62) == 0) w = __hip_atomic_load(&tiles[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    const uint64_t prefixes = __ballot((w >> 62) == 2);
-    // lanes up to and including the nearest published prefix contribute
-    const int stop = prefixes ? __ffsll(static_cast<long long>(prefixes)) - 1 : 63;
-    int32_t v = lane <= stop ? static_cast<int32_t>(static_cast<uint32_t>(w)) : 0;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    exclusive += v;
-    if (prefixes) break;
-  }
-  if (lane == 0) publish_tile(tiles, tile, kTilePrefix | static_cast<uint32_t>(exclusive + aggregate));
-  return exclusive;
 }
 
 // Exclusive scans of NV values per thread over a block of BLOCK threads;
@@ -119,9 +67,14 @@ __device__ __forceinline__ void block_exclusive_scan_multi(const int32_t (&x)[NV
 
 // Decoupled look-back over NV independent scans at once (array a of the
 // look-back words starts at tiles + a * stride).  Called by the whole first
-// wave of a tile; the rules are those of tile_lookback_wave, per array.
+// wave of a tile.  Publishes the tile's aggregates, resolves the exclusive
+// prefixes from the predecessors 64 at a time (lane i reads tile - 1 - i; a
+// predecessor that has published nothing yet is re-read until it has),
+// publishes the inclusive prefixes and returns the exclusive ones to every
+// lane.  Values are non-negative and below 2^31.  Returns false if the wait
+// ran out.
 template <int NV>
-__device__ void tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
+__device__ bool tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
                                     const int32_t (&aggregate)[NV], int32_t (&exclusive)[NV]) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
@@ -132,7 +85,7 @@ __device__ void tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
       for (int a = 0; a < NV; ++a)
         publish_tile(tiles + a * stride, 0, kTilePrefix | static_cast<uint32_t>(aggregate[a]));
     }
-    return;
+    return true;
   }
   if (lane == 0) {
 #pragma unroll
@@ -142,7 +95,9 @@ __device__ void tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
   bool done[NV];
 #pragma unroll
   for (int a = 0; a < NV; ++a) done[a] = false;
-  for (int base = tile - 1;; base -= 64) {
+  int spins = 0;
+  bool ok = true;
+  for (int base = tile - 1; ok; base -= 64) {
     const int t = base - lane;
     uint64_t w[NV];
 #pragma unroll
@@ -154,6 +109,10 @@ __device__ void tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
 #pragma unroll
       for (int a = 0; a < NV; ++a) pending |= !done[a] && (w[a] >> 62) == 0;
       if (!__any(pending)) break;
+      if (++spins > kLookbackSpins) {
+        ok = false;
+        break;
+      }
       __builtin_amdgcn_s_sleep(1);
       // re-read the whole window of every open scan (a word only ever moves
       // from nothing to aggregate to prefix, so re-reading is harmless)
@@ -162,11 +121,13 @@ __device__ void tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
         if (!done[a] && t >= 0)
           w[a] = __hip_atomic_load(&tiles[a * stride + t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    if (!ok) break;
     bool all_done = true;
 #pragma unroll
     for (int a = 0; a < NV; ++a) {
       if (done[a]) continue;
       const uint64_t prefixes = __ballot((w[a] >> 62) == 2);
+      // lanes up to and including the nearest published prefix contribute
       const int stop = prefixes ? __ffsll(static_cast<long long>(prefixes)) - 1 : 63;
       int32_t v = lane <= stop ? static_cast<int32_t>(static_cast<uint32_t>(w[a])) : 0;
 #pragma unroll
@@ -182,6 +143,7 @@ __device__ void tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
     for (int a = 0; a < NV; ++a)
       publish_tile(tiles + a * stride, tile, kTilePrefix | static_cast<uint32_t>(exclusive[a] + aggregate[a]));
   }
+  return ok;
 }
 
 // Claims the next tile number for this workgroup (thread 0 takes a ticket,
