@@ -109,6 +109,35 @@ def summarize_profile(args):
     out.append(f"k_gather launches in the run: {len(g)}; pass B (isolated, launches {lo}..{hi - 1}): "
                f"{len(sel)} launches, average {sum(sel) / max(len(sel), 1) / 1e3:.2f} us, "
                f"min {min(sel) / 1e3:.2f} us, max {max(sel) / 1e3:.2f} us" if sel else "no pass-B launches")
+    # pass B step by step: kernels between the seed kernels that start each
+    # step, median duration of each position over the complete steps
+    gi = [i for i, r in enumerate(trace) if "k_gather" in r["Kernel_Name"]]
+    if len(gi) >= hi:
+        window = trace[gi[lo - 1] + 1:gi[hi - 1] + 1]
+        steps, cur = [], None
+        for r in window:
+            name = r["Kernel_Name"].replace("gmb::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+            if name.startswith("k_seed_scan"):
+                cur = []
+                steps.append(cur)
+            if cur is not None:
+                cur.append((name, int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+        if steps:
+            import statistics
+            n = statistics.mode(len(st) for st in steps[:-1] or steps)
+            full = [st for st in steps if len(st) == n]
+            out.append("")
+            out.append(f"Pass B, one stream: the kernels of a step in launch order, median over "
+                       f"{len(full)} complete steps:")
+            out.append("")
+            out.append("| # | kernel | median us |")
+            out.append("|---:|---|---:|")
+            tot = 0.0
+            for k in range(n):
+                m = statistics.median(st[k][1] for st in full) / 1e3
+                tot += m
+                out.append(f"| {k} | `{full[0][k][0]}` | {m:.2f} |")
+            out.append(f"| | sum | {tot:.1f} |")
     print("\n".join(out))
 
 
