@@ -357,8 +357,20 @@ __device__ __forceinline__ const float* pick(bool c, const float* a, const float
 // chunks; SPLIT = 4: the four waves share one 16-row tile, wave w takes the
 // chunks c = w (mod 4), and the partial sums meet in LDS (for layers with
 // few rows, where one wave per 16 rows would leave most SIMDs idle).
+// LDS bytes of one slab workgroup and the workgroups per CU that LDS
+// allows (at most 3: one to three waves per SIMD).
+constexpr int slab_lds_bytes(int nch, int j, int split) {
+  return nch * 16 * 16 * j * 4 + (split > 1 ? 4 * j * 64 * 16 : 16);
+}
+constexpr int slab_occupancy(int nch, int j, int split) {
+  const int by_lds = (160 * 1024) / slab_lds_bytes(nch, j, split);
+  return by_lds < 1 ? 1 : (by_lds > 3 ? 3 : by_lds);
+}
+
 template <int NCH, int J, int SPLIT>
-__global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(slab_occupancy(NCH, J, SPLIT), slab_occupancy(NCH, J, SPLIT))))
+void k_linear_f32_slab(const int32_t* sizes,
                                                          const float* __restrict__ Hs,
                                                          const float* __restrict__ Ag,
                                                          const float* __restrict__ Ws,
@@ -376,6 +388,22 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
   if (static_cast<int>(blockIdx.x) >= row_tiles) return;
   const int n0 = blockIdx.y * BN;
   const int K2 = 2 * K;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, r16 = lane & 15;
+  // A fragment i of row tile rt (a tile past the end reads row M-1: every
+  // load is unconditional)
+  auto tile_rows = [&](int rt, const float*& hrow, const float*& grow) {
+    const int row = SPLIT > 1 ? rt * 16 + r16 : rt * 64 + wave * 16 + r16;
+    const int64_t arow = row < M ? row : M - 1;
+    hrow = Hs + arow * K;
+    grow = Ag + arow * K;
+  };
+  auto load_frag = [&](const float* hrow, const float* grow, int i) -> float4 {
+    const int c = SPLIT > 1 ? wave + 4 * i : i;
+    const int k = c * 16 + 4 * q;
+    const int kk = k >= K2 ? 0 : (k < K ? k : k - K);
+    return *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
+  };
   auto slab_at = [&](int k, int n) -> float& {
     return Bp[((((k >> 4) * 4 + ((k >> 2) & 3)) * BN) + n) * 4 + (k & 3)];
   };
@@ -433,51 +461,63 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
     }
   }
   __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int q = lane >> 4, r16 = lane & 15;
-  // A fragments of row tile rt (a tile past the end reads row M-1: every
-  // load is unconditional)
-  auto load_tile = [&](int rt, float4 (&dst)[MYCH]) {
-    const int row = SPLIT > 1 ? rt * 16 + r16 : rt * 64 + wave * 16 + r16;
-    const int64_t arow = row < M ? row : M - 1;
-    const float* hrow = Hs + arow * K;
-    const float* grow = Ag + arow * K;
+  // the first tile's A fragments (after the fill: both at once would not
+  // fit the registers of three waves per SIMD)
+  float4 a[MYCH];
+  {
+    const float *hrow, *grow;
+    tile_rows(blockIdx.x, hrow, grow);
 #pragma unroll
-    for (int i = 0; i < MYCH; ++i) {
-      const int c = SPLIT > 1 ? wave + 4 * i : i;
-      const int k = c * 16 + 4 * q;
-      const int kk = k >= K2 ? 0 : (k < K ? k : k - K);
-      dst[i] = *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
-    }
-  };
-  // software pipeline over the workgroup's row tiles: the next tile's A
-  // reads are in flight while the current tile's MFMAs run
-  float4 a[MYCH], a_next[MYCH];
-  load_tile(blockIdx.x, a);
+    for (int i = 0; i < MYCH; ++i) a[i] = load_frag(hrow, grow, i);
+  }
+  // bias of this thread's output columns (fixed over the row tiles); with
+  // split K, thread t stores column block t / 64 (t < 64 J)
+  float bv[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int col = n0 + (SPLIT > 1 ? ((threadIdx.x >> 6) % J) : j) * 16 + r16;
+    bv[j] = bias[col < N ? col : N - 1];
+  }
+  // software pipeline over the workgroup's row tiles: as soon as chunk i's
+  // MFMAs are issued, a[i] is reloaded with the next tile's fragment i, so
+  // the next tile's reads are in flight during the rest of this tile
+  // without a second set of registers
   for (int rt = blockIdx.x; rt < row_tiles; rt += gridDim.x) {
-    load_tile(rt + gridDim.x, a_next);
-    // keep the scheduler from sinking each read next to its first use
-    __builtin_amdgcn_sched_barrier(0);
+    const float *hnext, *gnext;
+    tile_rows(rt + gridDim.x, hnext, gnext);
     floatx4 acc[J];
 #pragma unroll
     for (int j = 0; j < J; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // B fragments double-buffered: chunk i + 1's LDS reads are issued
+    // before chunk i's MFMAs, so a wave never waits on LDS between chunks
+    // (the waves of a SIMD run in step, so the other wave cannot cover it)
+    auto load_b = [&](int i, float4 (&b)[J]) {
+      const int c = SPLIT > 1 ? wave + 4 * i : i;
+      const int cc = c < NCH ? c : NCH - 1;
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        b[j] = *reinterpret_cast<const float4*>(&Bp[(((cc * 4 + q) * BN) + j * 16 + r16) * 4]);
+    };
+    float4 b0[J], b1[J];
+    load_b(0, b0);
 #pragma unroll
     for (int i = 0; i < MYCH; ++i) {
       const int c = SPLIT > 1 ? wave + 4 * i : i;
+      float4 (&bc)[J] = (i & 1) ? b1 : b0;
+      float4 (&bn)[J] = (i & 1) ? b0 : b1;
+      if (i + 1 < MYCH) load_b(i + 1, bn);
+      __builtin_amdgcn_sched_barrier(0);
       if (c < NCH) {   // uniform: depends on the wave index only
-        float4 b[J];
 #pragma unroll
-        for (int j = 0; j < J; ++j)
-          b[j] = *reinterpret_cast<const float4*>(&Bp[(((c * 4 + q) * BN) + j * 16 + r16) * 4]);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, bc[j].x, acc[j], 0, 0, 0);
 #pragma unroll
-        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, b[j].x, acc[j], 0, 0, 0);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, bc[j].y, acc[j], 0, 0, 0);
 #pragma unroll
-        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, b[j].y, acc[j], 0, 0, 0);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, bc[j].z, acc[j], 0, 0, 0);
 #pragma unroll
-        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, b[j].z, acc[j], 0, 0, 0);
-#pragma unroll
-        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, b[j].w, acc[j], 0, 0, 0);
+        for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, bc[j].w, acc[j], 0, 0, 0);
       }
+      a[i] = load_frag(hnext, gnext, i);
     }
     if constexpr (SPLIT > 1) {
       // partials of the four waves -> LDS; thread t then owns output entry
@@ -492,32 +532,48 @@ __global__ __launch_bounds__(256) void k_linear_f32_slab(const int32_t* sizes,
 #pragma unroll
         for (int w = 1; w < 4; ++w) sum += *reinterpret_cast<const floatx4*>(&Red[((w * J + j) * 64 + l) * 4]);
         const int col = n0 + j * 16 + (l & 15);
-        const float bv = bias[col < N ? col : N - 1];
+        const int row0 = rt * 16 + 4 * (l >> 4);
+        float* o = out + static_cast<int64_t>(row0) * N + col;
+        const bool full = row0 + 4 <= M && col < N;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int orow = rt * 16 + 4 * (l >> 4) + r;
-          float z = sum[r] + bv;
+          float z = sum[r] + bv[0];
           if (relu) z = z > 0.f ? z : 0.f;
-          if (orow < M && col < N) out[static_cast<int64_t>(orow) * N + col] = z;
+          if (full || (row0 + r < M && col < N)) o[static_cast<int64_t>(r) * N] = z;
         }
       }
       __syncthreads();
     } else {
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        const int col = n0 + j * 16 + r16;
-        const float bv = bias[col < N ? col : N - 1];
+      // one row pointer per accumulator row; a tile inside the matrix
+      // stores without per-element checks (column offsets fold into the
+      // store's immediate offset)
+      const int row0 = rt * 64 + wave * 16 + 4 * q;
+      float* o0 = out + static_cast<int64_t>(row0) * N + n0 + r16;
+      const bool full = row0 + 4 <= M && n0 + BN <= N;
+      if (full) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int orow = rt * 64 + wave * 16 + 4 * q + r;
-          float z = acc[j][r] + bv;
-          if (relu) z = z > 0.f ? z : 0.f;
-          if (orow < M && col < N) out[static_cast<int64_t>(orow) * N + col] = z;
+          float* o = o0 + static_cast<int64_t>(r) * N;
+#pragma unroll
+          for (int j = 0; j < J; ++j) {
+            float z = acc[j][r] + bv[j];
+            if (relu) z = z > 0.f ? z : 0.f;
+            o[j * 16] = z;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+          const int col = n0 + j * 16 + r16;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float z = acc[j][r] + bv[j];
+            if (relu) z = z > 0.f ? z : 0.f;
+            if (row0 + r < M && col < N) o0[static_cast<int64_t>(r) * N + j * 16] = z;
+          }
         }
       }
     }
-#pragma unroll
-    for (int i = 0; i < MYCH; ++i) a[i] = a_next[i];
   }
 }
 
