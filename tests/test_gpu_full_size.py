@@ -1,0 +1,154 @@
+"""GPU parity at the full sizes of the benchmark workloads.
+
+The 1M-node R-MAT graph (fp32 x100, fan-outs 15/10/5, batch 1000), the
+2.4M-node power-law graph (the benchmark's workload) and the same graph with
+100 hubs of in-degree 100k (bf16 x128, fan-outs 25/10, batch 4000), each run
+through the C ABI exactly as bench.py runs them (caller-owned workspaces,
+reused across batches).  Whole batches are compared with the oracle:
+sampling, relabel and gather bit for bit, the forward within 1e-4 (fp32) or
+2e-2 (bf16) row-wise relative error on every layer.
+"""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU on this machine", allow_module_level=True)
+
+import paper_2010_05337_amd as gmb  # noqa: E402
+from datagen.configs import make_workload  # noqa: E402
+from gpu_util import (assert_blocks_equal, rowwise_rel_err, tensor_bits, tensor_f64,  # noqa: E402
+                      to_torch_feats, to_torch_weights)
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+class Lane:
+    """One set of device buffers, sized for a full batch, as bench.py keeps
+    per stream."""
+
+    def __init__(self, csr, wl, feats, weights, stream=None):
+        cfg = wl.cfg
+        self.csr, self.stream = csr, stream
+        dev = torch.device("cuda")
+        self.ws_sample = gmb._aligned_bytes(gmb.sample_workspace_bytes(cfg.batch, list(cfg.fanouts),
+                                                                       cfg.num_nodes), dev)[1]
+        probe = gmb.sample_blocks(csr, torch.from_numpy(wl.batches[0]).cuda(), list(cfg.fanouts),
+                                  wl.batch_key(0), workspace=self.ws_sample)
+        self.x = torch.empty((probe.input_capacity, cfg.feat_dim), dtype=feats.dtype, device=dev)
+        self.ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1]
+        self.logits = torch.empty((cfg.batch, cfg.dims[-1]), dtype=torch.float32, device=dev)
+
+    def run(self, wl, feats, weights, b, seeds=None):
+        cfg = wl.cfg
+        s = torch.from_numpy(wl.batches[b] if seeds is None else seeds).cuda()
+        blocks = gmb.sample_blocks(self.csr, s, list(cfg.fanouts), wl.batch_key(b), workspace=self.ws_sample)
+        x = gmb.gather_features(blocks, feats, out=self.x)
+        logits, hidden = gmb.sage_forward(blocks, x, weights, workspace=self.ws_fwd,
+                                          logits=self.logits[:s.numel()], return_hidden=True)
+        return blocks, x, logits, hidden
+
+
+def host_blocks(blocks):
+    out = []
+    for b in blocks.blocks():
+        out.append(dict(n_dst=b.n_dst, n_src=b.n_src, nnz=b.nnz,
+                        indptr=b.indptr.cpu().numpy().astype(np.int64),
+                        local=b.indices.cpu().numpy().astype(np.int64),
+                        nbr=b.nbr.cpu().numpy().astype(np.int64),
+                        src=b.src_ids.cpu().numpy().astype(np.int64)))
+    return out
+
+
+def check_batch(orc, wl, lane, feats, weights, b, seeds=None):
+    cfg, g = wl.cfg, wl.graph
+    seeds_np = wl.batches[b] if seeds is None else seeds
+    print(f"{cfg.name}: batch {b}, {len(seeds_np)} seeds", flush=True)
+    blocks, x, logits, hidden = lane.run(wl, feats, weights, b, seeds)
+    host = host_blocks(blocks)
+    ref = orc.sample_blocks(g.indptr, g.indices, seeds_np, list(cfg.fanouts), wl.batch_key(b))
+    assert_blocks_equal(host, ref, f"{cfg.name} batch {b}")
+    X = orc.gather(wl.feats, ref[0].src)
+    got = tensor_bits(x)[:ref[0].n_src]
+    assert got.view(np.uint8).tobytes() == X.view(np.uint8).tobytes(), "gathered rows differ"
+    ws, wn, bs = wl.weights.as_f64()
+    ref_logits, ref_hidden = orc.sage_forward(ref, orc.widen(X, cfg.feat_dtype), ws, wn, bs)
+    errs = [rowwise_rel_err(tensor_f64(h), r) for h, r in zip(hidden, ref_hidden[:-1])]
+    errs.append(rowwise_rel_err(tensor_f64(logits), ref_logits))
+    print(f"  sizes {[(r.n_dst, r.n_src, r.nnz) for r in ref]}, forward errors {errs}", flush=True)
+    assert all(e <= TOL[cfg.feat_dtype] for e in errs), errs
+    return blocks, logits
+
+
+@pytest.fixture(scope="module", params=["rmat1m", "products2m", "hubs2m"])
+def setup(request):
+    wl = make_workload(request.param)
+    g = wl.graph
+    print(f"{request.param}: N={g.num_nodes} E={g.num_edges} max deg={g.degrees().max()}", flush=True)
+    ip = torch.from_numpy(g.indptr.astype(np.int32)).cuda()
+    ix = torch.from_numpy(g.indices).cuda()
+    csr = gmb.CSRGraph(ip, ix)
+    feats = to_torch_feats(wl.feats)
+    weights = to_torch_weights(wl.weights)
+    yield wl, csr, feats, weights, ip, ix
+    del csr, feats, weights
+    torch.cuda.empty_cache()
+
+
+def test_full_size_batches_match_the_oracle(orc, setup):
+    """First, middle and last (partial) batch of the epoch, one set of
+    reused buffers."""
+    wl, csr, feats, weights, _, _ = setup
+    lane = Lane(csr, wl, feats, weights)
+    nb = len(wl.batches)
+    for b in sorted({0, nb // 2, nb - 1}):
+        check_batch(orc, wl, lane, feats, weights, b)
+    csr.check_status()
+
+
+def test_hub_seeds(orc, setup):
+    """Every hub as a seed next to ordinary vertices (the hubs2m graph; on
+    the others, the 100 highest-degree vertices)."""
+    wl, csr, feats, weights, _, _ = setup
+    g = wl.graph
+    deg = g.degrees()
+    hubs = np.asarray(g.hubs) if getattr(g, "hubs", None) is not None and len(g.hubs) else \
+        np.argsort(-deg, kind="stable")[:100]
+    rest = wl.batches[0][~np.isin(wl.batches[0], hubs)][:wl.cfg.batch - len(hubs)]
+    seeds = np.concatenate([hubs.astype(np.int32), rest.astype(np.int32)])
+    assert len(np.unique(seeds)) == len(seeds)
+    lane = Lane(csr, wl, feats, weights)
+    check_batch(orc, wl, lane, feats, weights, 0, seeds=seeds)
+    csr.check_status()
+
+
+def test_streams_reproduce_one_stream(setup):
+    """Batches run four at a time on four streams (each stream with its own
+    sampler state and buffers, as in the benchmark) give the same blocks and
+    the same logits, bit for bit, as the same batches on one stream."""
+    wl, csr, feats, weights, ip, ix = setup
+    streams = [torch.cuda.Stream() for _ in range(4)]
+    lanes = [Lane(gmb.CSRGraph(ip, ix), wl, feats, weights, st) for st in streams]
+    single = Lane(csr, wl, feats, weights)
+    nb = min(8, len(wl.batches))
+    torch.cuda.synchronize()
+    for g0 in range(0, nb, 4):
+        group = []
+        for b in range(g0, min(g0 + 4, nb)):
+            ln = lanes[b % 4]
+            with torch.cuda.stream(ln.stream):
+                blocks, _, logits, _ = ln.run(wl, feats, weights, b)
+            group.append((b, blocks, logits))
+        torch.cuda.synchronize()
+        for b, blocks, logits in group:
+            got, lg = host_blocks(blocks), logits.clone()
+            blocks1, _, logits1, _ = single.run(wl, feats, weights, b)
+            ref = host_blocks(blocks1)
+            for l, (h, r) in enumerate(zip(got, ref)):
+                for k in ("n_dst", "n_src", "nnz", "indptr", "local", "nbr", "src"):
+                    assert np.array_equal(h[k], r[k]), f"batch {b} layer {l} {k}"
+            assert torch.equal(lg, logits1), f"batch {b} logits"
+    for ln in lanes:
+        ln.csr.check_status()
