@@ -51,6 +51,7 @@ struct HopPlan {
   int64_t cap_dst, cap_nnz, cap_src;
   size_t off_indptr, off_nbr, off_local;
   int64_t tiles_word, ticket_word, tile_stride;
+  int items;
 };
 
 struct SamplePlan {
@@ -96,7 +97,8 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
       return fail(GMB_EINVAL, "hop %d: capacity %lld edges / %lld sources exceeds 2^31-1", h,
                   static_cast<long long>(hp.cap_nnz), static_cast<long long>(hp.cap_src));
     // the relabel scan of hop h carries 1 + (later hops) values
-    hp.tile_stride = gmb::scan_tiles(hp.cap_nnz);
+    hp.items = gmb::scan_items_for(hp.cap_nnz);
+    hp.tile_stride = gmb::scan_tiles(hp.cap_nnz, hp.items);
     hp.tiles_word = zero_words;
     zero_words += hp.tile_stride * (num_layers - h);
     hp.ticket_word = zero_words++;
@@ -335,7 +337,7 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
       aa.indptr[v] = hops[h + v].indptr;
       aa.fanout[v] = hops[h + v].fanout;
     }
-    e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, ids, table, status, s);
+    e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, p.hop[h].items, ids, table, status, s);
     if (e != hipSuccess) return hip_fail(e, "relabel launch");
   }
   const gmb::HopArgs& last = hops[num_layers - 1];

@@ -28,16 +28,25 @@ struct HopArgs {
   uint64_t* tiles;       // look-back words of this hop's relabel scan
   uint32_t* ticket;
   int64_t tile_stride;   // words per scanned value
+  int items;             // relabel scan items per thread
   int64_t cap_dst, cap_nnz, cap_src;
   int fanout;
   int layer;
 };
 
 constexpr int kScanBlock = 256;
-constexpr int kScanItems = 8;
-constexpr int kScanTile = kScanBlock * kScanItems;
-
-inline int64_t scan_tiles(int64_t n) { return n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile; }
+// Items per thread of a relabel scan tile (kScanBlock threads): 2, 4, 8 or
+// 16.  Small hops take small tiles so that their random reads spread over
+// many CUs; large hops take large tiles, which cuts tickets and look-back.
+inline int64_t scan_tiles(int64_t n, int items) {
+  const int64_t tile = static_cast<int64_t>(kScanBlock) * items;
+  return n <= 0 ? 1 : (n + tile - 1) / tile;
+}
+inline int scan_items_for(int64_t cap_nnz) {
+  for (int items = 16; items > 2; items /= 2)
+    if (scan_tiles(cap_nnz, items) >= 128) return items;
+  return 2;
+}
 
 // Arguments of the seed kernel (segment 0: the seeds).  Per hop v:
 // indptr[v] its block row offsets, fanout[v] its fan-out.  totals[v] is
@@ -91,7 +100,7 @@ hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h,
                          uint32_t* status, uint32_t k0, uint32_t k1, int first_hop,
                          const DeferredArgs& fix, hipStream_t s);
 hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
-                         int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s);
+                         int items, int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s);
 hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src,
                           uint32_t* table, int64_t num_nodes, const DeferredArgs& fix, hipStream_t s);
 

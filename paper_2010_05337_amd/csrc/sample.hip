@@ -45,21 +45,27 @@ __device__ __forceinline__ int32_t clamp_degree(int64_t d, int fanout) {
   return static_cast<int32_t>(d < 0 ? 0 : (d < fanout ? d : fanout));
 }
 
-// Items [base, base + 8) of a scan tile.  Full groups are two 16-byte loads
-// (base is a multiple of 8 and the arrays are 256-byte aligned); the group
-// holding the end of the data reads element-wise, and entries at or past n
-// are left as 0 (the caller ignores them).
-__device__ __forceinline__ void load_items(const int32_t* a, int64_t base, int64_t n,
-                                           int32_t (&v)[kScanItems]) {
-  static_assert(kScanItems == 8, "two int4 loads per thread");
-  if (base + kScanItems <= n) {
-    const int4 x = *reinterpret_cast<const int4*>(a + base);
-    const int4 y = *reinterpret_cast<const int4*>(a + base + 4);
-    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-    v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+// Items [base, base + ITEMS) of a scan tile.  Full groups are 8- or
+// 16-byte loads (base is a multiple of ITEMS and the arrays are 256-byte
+// aligned); the group holding the end of the data reads element-wise, and
+// entries at or past n are left as 0 (the caller ignores them).
+template <int ITEMS>
+__device__ __forceinline__ void load_items(const int32_t* a, int64_t base, int64_t n, int32_t (&v)[ITEMS]) {
+  if (base + ITEMS <= n) {
+    if constexpr (ITEMS % 4 == 0) {
+#pragma unroll
+      for (int c = 0; c < ITEMS / 4; ++c) {
+        const int4 x = *reinterpret_cast<const int4*>(a + base + 4 * c);
+        v[4 * c] = x.x; v[4 * c + 1] = x.y; v[4 * c + 2] = x.z; v[4 * c + 3] = x.w;
+      }
+    } else {
+      static_assert(ITEMS == 2, "2, 4, 8 or 16 items");
+      const int2 x = *reinterpret_cast<const int2*>(a + base);
+      v[0] = x.x; v[1] = x.y;
+    }
   } else {
 #pragma unroll
-    for (int q = 0; q < kScanItems; ++q) v[q] = base + q < n ? a[base + q] : 0;
+    for (int q = 0; q < ITEMS; ++q) v[q] = base + q < n ? a[base + q] : 0;
   }
 }
 
@@ -321,13 +327,13 @@ __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* 
 // never their own tag, so their flag is 0 either way, and either one gives
 // them the right local id; so the table store needs no ordering within
 // this kernel.
-template <int NV, bool WIDE>
+template <int NV, bool WIDE, int ITEMS>
 __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga, int32_t* ids,
                                                        uint32_t* table, uint32_t* status) {
   __shared__ int s_tile;
   __shared__ int32_t s_excl[NV];
   __shared__ int32_t s_wave[NV * (kScanBlock / 64)];
-  __shared__ int32_t s_pos[kScanTile];
+  __shared__ int32_t s_pos[(kScanBlock * ITEMS)];
   const CsrView g = view(ga);
   // row offsets of hop h + v start after the edges of segments 0..h
   // (final before this kernel; read early, used after the look-back)
@@ -337,19 +343,19 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
   const int32_t n = load_size(&a.sizes[kNnz]);
   const int32_t n_dst = load_size(&a.sizes[kNDst]);
   const int tile = claim_tile(a.ticket, &s_tile);
-  const int num_tiles = n <= 0 ? 1 : (n + kScanTile - 1) / kScanTile;
+  const int num_tiles = n <= 0 ? 1 : (n + (kScanBlock * ITEMS) - 1) / (kScanBlock * ITEMS);
   if (tile >= num_tiles) return;
 
-  const int64_t tile_base = static_cast<int64_t>(tile) * kScanTile;
-  const int64_t base = tile_base + threadIdx.x * kScanItems;
-  int32_t u[kScanItems];
-  load_items(a.nbr, base, n, u);
+  const int64_t tile_base = static_cast<int64_t>(tile) * (kScanBlock * ITEMS);
+  const int64_t base = tile_base + threadIdx.x * ITEMS;
+  int32_t u[ITEMS];
+  load_items<ITEMS>(a.nbr, base, n, u);
   // table entries and (for the later hops) the degrees of every item, in
   // one round of reads; an invalid item reads vertex 0 and is dropped
-  uint32_t t[kScanItems];
-  int32_t deg[kScanItems];
+  uint32_t t[ITEMS];
+  int32_t deg[ITEMS];
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q) {
+  for (int q = 0; q < ITEMS; ++q) {
     const bool ok = (base + q < n) & valid_vertex(u[q], g.num_nodes);
     u[q] = ok ? u[q] : -1;
     const int32_t uc = u[q] < 0 ? 0 : u[q];
@@ -363,7 +369,7 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
   }
   uint32_t flags = 0;
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q)
+  for (int q = 0; q < ITEMS; ++q)
     if (u[q] >= 0 && t[q] == (kEdgeTag | static_cast<uint32_t>(base + q))) flags |= 1u << q;
   int32_t sum[NV], thr[NV], total[NV], excl[NV];
   sum[0] = __popc(flags);
@@ -371,7 +377,7 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
   for (int v = 1; v < NV; ++v) {
     sum[v] = 0;
 #pragma unroll
-    for (int q = 0; q < kScanItems; ++q) sum[v] += ((flags >> q) & 1u) ? clamp_degree(deg[q], a.fanout[v]) : 0;
+    for (int q = 0; q < ITEMS; ++q) sum[v] += ((flags >> q) & 1u) ? clamp_degree(deg[q], a.fanout[v]) : 0;
   }
   block_exclusive_scan_multi<kScanBlock, NV>(sum, thr, total, s_wave);
   if (threadIdx.x < 64) {
@@ -393,12 +399,12 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
 #pragma unroll
   for (int v = 1; v < NV; ++v) run[v] = basev[v] + excl[v] + thr[v];
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q) {
+  for (int q = 0; q < ITEMS; ++q) {
     if ((flags >> q) & 1u) {
       ids[r] = u[q];
       a.local[base + q] = r;
       table[u[q]] = static_cast<uint32_t>(r);   // read by later kernels only
-      s_pos[threadIdx.x * kScanItems + q] = r;
+      s_pos[threadIdx.x * ITEMS + q] = r;
 #pragma unroll
       for (int v = 1; v < NV; ++v) {
         a.indptr[v][r] = run[v];
@@ -409,7 +415,7 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
   }
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < kScanItems; ++q) {
+  for (int q = 0; q < ITEMS; ++q) {
     if (base + q >= n || ((flags >> q) & 1u)) continue;
     int32_t loc = 0;   // an invalid vertex (reported by the sampling) gets 0
     if (u[q] >= 0) {
@@ -523,13 +529,24 @@ hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h,
 }
 
 hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
-                         int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s) {
-  const unsigned grid = static_cast<unsigned>(scan_tiles(cap_nnz));
-#define GMB_ASSIGN(V)                                                                               \
-  if (g.wide)                                                                                       \
-    hipLaunchKernelGGL((k_assign<V, true>), dim3(grid), dim3(kScanBlock), 0, s, a, g, ids, table, status); \
-  else                                                                                              \
-    hipLaunchKernelGGL((k_assign<V, false>), dim3(grid), dim3(kScanBlock), 0, s, a, g, ids, table, status)
+                         int items, int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s) {
+  const unsigned grid = static_cast<unsigned>(scan_tiles(cap_nnz, items));
+#define GMB_ASSIGN_I(V, W, I) \
+  hipLaunchKernelGGL((k_assign<V, W, I>), dim3(grid), dim3(kScanBlock), 0, s, a, g, ids, table, status)
+#define GMB_ASSIGN_W(V, W)                       \
+  switch (items) {                               \
+    case 2: GMB_ASSIGN_I(V, W, 2); break;        \
+    case 4: GMB_ASSIGN_I(V, W, 4); break;        \
+    case 8: GMB_ASSIGN_I(V, W, 8); break;        \
+    case 16: GMB_ASSIGN_I(V, W, 16); break;      \
+    default: return hipErrorInvalidValue;        \
+  }
+#define GMB_ASSIGN(V)         \
+  if (g.wide) {               \
+    GMB_ASSIGN_W(V, true)     \
+  } else {                    \
+    GMB_ASSIGN_W(V, false)    \
+  }
   switch (num_values) {
     case 1: { GMB_ASSIGN(1); } break;
     case 2: { GMB_ASSIGN(2); } break;
@@ -542,6 +559,8 @@ hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, 
     default: return hipErrorInvalidValue;
   }
 #undef GMB_ASSIGN
+#undef GMB_ASSIGN_W
+#undef GMB_ASSIGN_I
   return hipGetLastError();
 }
 
