@@ -416,7 +416,7 @@ int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_wei
     const bool last = (l == L - 1);
     void* h_out = last ? static_cast<void*>(logits) : static_cast<void*>(base + p.off_hidden[l]);
     hipError_t e = gmb::launch_mean_aggregate(bk.sizes, bk.indptr, bk.indices, h_in, d_in, bf16, agg,
-                                              bk.cap_dst, s);
+                                              bk.cap_dst, bk.fanout, s);
     if (e != hipSuccess) return hip_fail(e, "mean-aggregation launch");
     e = gmb::launch_sage_linear(bk.sizes, h_in, agg, weights->w_self[l], weights->w_neigh[l],
                                 weights->bias[l], d_in, d_out, bf16, last ? 0 : 1,

@@ -4,7 +4,8 @@
 //
 //   k_mean    m_v = (1/k_v) sum_e H[local[e]], fp32 accumulation; a group of
 //             G lanes per destination row, 16-byte chunks of the feature
-//             row per lane, four neighbour rows in flight per lane.
+//             row per lane; the group reads the row's local ids in one
+//             access and then up to U neighbour rows in one batch.
 //   k_linear  out = act([H_dst | M] [W_self; W_neigh] + b): one GEMM with
 //             K = 2 d_in on the matrix cores (v_mfma_f32_16x16x4_f32 for
 //             fp32, v_mfma_f32_16x16x32_bf16 for bf16 with fp32
@@ -94,69 +95,103 @@ __device__ __forceinline__ void store_chunk(uint16_t* p, const float (&v)[VEC]) 
   }
 }
 
-template <typename T, int VEC, int G>
+template <typename T, int VEC, int G, int U>
 __global__ __launch_bounds__(256) void k_mean(const int32_t* sizes, const int32_t* __restrict__ indptr,
                                               const int32_t* __restrict__ local,
-                                              const T* __restrict__ H, int d, T* __restrict__ M) {
-  const int32_t n_dst = load_size(&sizes[kNDst]);
+                                              const T* __restrict__ H, int d, T* __restrict__ M,
+                                              int64_t cap_rows) {
   const int64_t row = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
-  if (row >= n_dst) return;
   const int lane = threadIdx.x & (G - 1);
-  const int32_t beg = indptr[row], end = indptr[row + 1];
+  // independent first reads, the row offsets first (the compiler keeps
+  // later reads behind the size word's atomic read); a row past the
+  // capacity reads the last one
+  const int64_t rc = row < cap_rows ? row : cap_rows - 1;
+  const int32_t beg = indptr[rc], end = indptr[rc + 1];
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  if (row >= n_dst) return;   // the whole group leaves together
   const int32_t k = end - beg;
   const int chunks = d / VEC;
-  for (int c = lane; c < chunks; c += G) {
+  const int passes = (chunks + G - 1) / G;
+  for (int cc = 0; cc < passes; ++cc) {
+    const int c = cc * G + lane;
+    const int cl = c < chunks ? c : chunks - 1;
     float acc[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
-    // A negative local id only exists after a data error (vertex id out of
-    // range); it is read as row 0 so that every access stays in bounds.
-    int32_t e = beg;
-    for (; e + 4 <= end; e += 4) {
-      float x0[VEC], x1[VEC], x2[VEC], x3[VEC];
-      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e], 0)) * d + c * VEC, x0);
-      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e + 1], 0)) * d + c * VEC, x1);
-      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e + 2], 0)) * d + c * VEC, x2);
-      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e + 3], 0)) * d + c * VEC, x3);
+    // the group reads G local ids at once (lane i: edge base + i), then
+    // its rows U at a time (U >= the fan-out where possible, so one batch
+    // per row) with every read unconditional; past the row's end a slot
+    // re-reads the first id and is dropped.  A negative local id only
+    // exists after a data error; it is read as row 0.
+    for (int32_t base = 0; base < k; base += G) {
+      const int32_t n_here = k - base < G ? k - base : G;
+      const int32_t mine = max(local[beg + base + (lane < n_here ? lane : 0)], 0);
+      for (int u0 = 0; u0 < n_here; u0 += U) {
+        int32_t id[U];
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) acc[i] += x0[i] + x1[i] + x2[i] + x3[i];
-    }
-    for (; e < end; ++e) {
-      float x0[VEC];
-      load_chunk<VEC>(H + static_cast<int64_t>(max(local[e], 0)) * d + c * VEC, x0);
+        for (int u = 0; u < U; ++u) id[u] = __shfl(mine, u0 + u < n_here ? u0 + u : 0, G);
+        float x[U][VEC];
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) acc[i] += x0[i];
+        for (int u = 0; u < U; ++u)
+          load_chunk<VEC>(H + static_cast<int64_t>(id[u]) * d + cl * VEC, x[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const bool in = u0 + u < n_here;
+#pragma unroll
+          for (int i = 0; i < VEC; ++i) {
+            float xv = x[u][i];
+            opaque(xv);
+            acc[i] += in ? xv : 0.f;
+          }
+        }
+      }
     }
     if (k > 0) {
       const float kf = static_cast<float>(k);
 #pragma unroll
       for (int i = 0; i < VEC; ++i) acc[i] = acc[i] / kf;
     }
-    store_chunk<VEC>(M + row * d + c * VEC, acc);
+    if (c < chunks) store_chunk<VEC>(M + row * d + c * VEC, acc);
   }
 }
 
 template <typename T, int VEC>
 hipError_t mean_dispatch(const int32_t* sizes, const int32_t* indptr, const int32_t* local, const void* h,
-                         int d, void* m, int64_t cap_dst, hipStream_t s) {
+                         int d, void* m, int64_t cap_dst, int fanout, hipStream_t s) {
   const int chunks = d / VEC;
   int G = 64;
   if (chunks <= 4) G = 4;
   else if (chunks <= 8) G = 8;
   else if (chunks <= 16) G = 16;
   else if (chunks <= 32) G = 32;
+  // rows in flight per lane: the fan-out rounded up to 8, 16 or 32 (16 at
+  // most for chunks wider than four values)
+  const int U = fanout <= 8 ? 8 : (fanout <= 16 || VEC > 4 ? 16 : 32);
   int64_t blocks = (cap_dst * G + 255) / 256;
   if (blocks < 1) blocks = 1;
   const dim3 grid(static_cast<unsigned>(blocks)), block(256);
   const T* H = static_cast<const T*>(h);
   T* M = static_cast<T*>(m);
-  switch (G) {
-    case 4: hipLaunchKernelGGL((k_mean<T, VEC, 4>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
-    case 8: hipLaunchKernelGGL((k_mean<T, VEC, 8>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
-    case 16: hipLaunchKernelGGL((k_mean<T, VEC, 16>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
-    case 32: hipLaunchKernelGGL((k_mean<T, VEC, 32>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
-    default: hipLaunchKernelGGL((k_mean<T, VEC, 64>), grid, block, 0, s, sizes, indptr, local, H, d, M); break;
+  const int64_t cap = cap_dst < 1 ? 1 : cap_dst;   // indptr holds cap_dst + 1 >= 1 entries
+#define GMB_MEAN(GG, UU) \
+  hipLaunchKernelGGL((k_mean<T, VEC, GG, UU>), grid, block, 0, s, sizes, indptr, local, H, d, M, cap)
+#define GMB_MEAN_G(UU)                \
+  switch (G) {                        \
+    case 4: GMB_MEAN(4, UU); break;   \
+    case 8: GMB_MEAN(8, UU); break;   \
+    case 16: GMB_MEAN(16, UU); break; \
+    case 32: GMB_MEAN(32, UU); break; \
+    default: GMB_MEAN(64, UU); break; \
   }
+  if (U == 8) {
+    GMB_MEAN_G(8)
+  } else if (U == 16) {
+    GMB_MEAN_G(16)
+  } else {
+    GMB_MEAN_G(32)
+  }
+#undef GMB_MEAN_G
+#undef GMB_MEAN
   return hipGetLastError();
 }
 
@@ -628,14 +663,16 @@ void launch_slab_for(const int32_t* sizes, const float* hs, const float* ag, con
 
 hipError_t launch_mean_aggregate(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                  const void* h, int d, int bf16, void* agg, int64_t cap_dst,
-                                 hipStream_t s) {
+                                 int fanout, hipStream_t s) {
   const uintptr_t align = reinterpret_cast<uintptr_t>(h) | reinterpret_cast<uintptr_t>(agg);
   if (bf16) {
-    if (d % 8 == 0 && align % 16 == 0) return mean_dispatch<uint16_t, 8>(sizes, indptr, local, h, d, agg, cap_dst, s);
-    return mean_dispatch<uint16_t, 1>(sizes, indptr, local, h, d, agg, cap_dst, s);
+    if (d % 8 == 0 && align % 16 == 0)
+      return mean_dispatch<uint16_t, 8>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
+    return mean_dispatch<uint16_t, 1>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
   }
-  if (d % 4 == 0 && align % 16 == 0) return mean_dispatch<float, 4>(sizes, indptr, local, h, d, agg, cap_dst, s);
-  return mean_dispatch<float, 1>(sizes, indptr, local, h, d, agg, cap_dst, s);
+  if (d % 4 == 0 && align % 16 == 0)
+    return mean_dispatch<float, 4>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
+  return mean_dispatch<float, 1>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
 }
 
 hipError_t launch_sage_linear(const int32_t* sizes, const void* h_self, const void* agg,
