@@ -9,6 +9,10 @@
 #include "common.hpp"
 #include "kernels.hpp"
 
+#ifndef GMB_GATHER_MAX_BLOCKS
+#define GMB_GATHER_MAX_BLOCKS 8192
+#endif
+
 namespace gmb {
 
 namespace {
@@ -88,7 +92,7 @@ hipError_t dispatch(const int32_t* ids, const int32_t* n_dev, int64_t n_cap, con
   else if (cpr <= 32) G = 32;
   const int64_t rows_per_block = (256 / G) * U;
   int64_t blocks = (n_cap + rows_per_block - 1) / rows_per_block;
-  if (blocks > 8192) blocks = 8192;
+  if (blocks > GMB_GATHER_MAX_BLOCKS) blocks = GMB_GATHER_MAX_BLOCKS;
   if (blocks < 1) blocks = 1;
   const dim3 grid(static_cast<unsigned>(blocks)), block(256);
   const V* f = static_cast<const V*>(feats);
