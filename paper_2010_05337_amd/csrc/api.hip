@@ -315,7 +315,7 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
     sa.fanout[h] = hops[h].fanout;
   }
   const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
-  hipError_t e = gmb::launch_seed_scan(sa, num_layers, g, table, status, s);
+  hipError_t e = gmb::launch_seed_scan(sa, num_layers, g, s);
   if (e != hipSuccess) return hip_fail(e, "seed launch");
   for (int h = 0; h < num_layers; ++h) {
     // the first hop has nothing deferred: word 3 of a block's sizes is 0
@@ -341,7 +341,7 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
     if (e != hipSuccess) return hip_fail(e, "relabel launch");
   }
   const gmb::HopArgs& last = hops[num_layers - 1];
-  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, table, csr->num_nodes,
+  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, num_seeds, table, csr->num_nodes, status,
                           gmb::DeferredArgs{last.local, last.sizes, std::max<int64_t>(last.cap_nnz, 1)}, s);
   if (e != hipSuccess) return hip_fail(e, "cleanup launch");
   *out = res;

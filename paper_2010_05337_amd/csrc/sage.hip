@@ -659,6 +659,168 @@ void launch_slab_for(const int32_t* sizes, const float* hs, const float* ag, con
     launch_slab<NCH, 2, 4>(sizes, hs, ag, ws, wn, bias, K, N, relu, out, cap_rows, s);
 }
 
+// bf16 with the weight slab resident in LDS (same scheme as the fp32 slab
+// kernel, on v_mfma_f32_16x16x32_bf16).  Lane l (q = l/16) supplies
+// A[l%16][32c + 8q .. +7] and B[32c + 8q .. +7][l%16] of chunk c and holds
+// C[4q + r][l%16].  The slab keeps the workgroup's BN = 16 J columns of
+// [W_self; W_neigh] for all 2 d_in rows (zero past 2 d_in and past d_out)
+// in operand order, Bp[((c * 4 + q) * BN + n) * 8 + s] = W[32c + 8q + s][n],
+// so a lane reads its eight k values with one 16-byte LDS read; its A
+// operand is one 16-byte global read (d_in % 8 == 0, so a group of eight k
+// never straddles [h_v | mean]).  Each wave computes 16 rows x BN columns,
+// the workgroup 64 rows, persistent over row tiles with the next tile's A
+// reads issued as soon as each chunk's MFMAs are; fp32 accumulation, bias
+// and ReLU, then fp32 or bf16 (round to nearest even) output.
+template <int NCH, int J>
+__global__ __launch_bounds__(256) void k_linear_bf16_slab(const int32_t* sizes,
+                                                          const uint16_t* __restrict__ Hs,
+                                                          const uint16_t* __restrict__ Ag,
+                                                          const uint16_t* __restrict__ Ws,
+                                                          const uint16_t* __restrict__ Wn,
+                                                          const float* __restrict__ bias, int K, int N,
+                                                          int relu, int out_f32, int wvec,
+                                                          void* __restrict__ out) {
+  constexpr int BN = 16 * J;
+  __shared__ __attribute__((aligned(16))) uint16_t Bp[NCH * 4 * BN * 8];
+  const int32_t M = load_size(&sizes[kNDst]);
+  const int row_tiles = (M + 63) / 64;
+  if (static_cast<int>(blockIdx.x) >= row_tiles) return;
+  const int n0 = blockIdx.y * BN;
+  const int K2 = 2 * K;
+  // slab fill: thread item = (k, 8 consecutive columns); one 16-byte read
+  // of a weight row when the row is vector-aligned and inside the matrix,
+  // else element-wise with zero padding
+  constexpr int kItems = NCH * 32 * (BN / 8);
+  for (int base = 0; base < kItems; base += 256 * 4) {
+    uint4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + u * 256 + threadIdx.x;
+      const int k = idx / (BN / 8), n8 = idx % (BN / 8);
+      const int gn = n0 + 8 * n8;
+      const bool in_k = idx < kItems && k < K2;
+      const uint16_t* row = (k < K ? Ws + static_cast<int64_t>(k) * N
+                                   : Wn + static_cast<int64_t>(in_k ? k - K : 0) * N);
+      // every read is unconditional (clamped column), zeros selected after
+      if (wvec) {   // uniform: N % 8 == 0 and 16-byte aligned rows
+        uint4 x = *reinterpret_cast<const uint4*>(row + (gn < N ? gn : 0));
+        asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+        v[u] = (in_k && gn < N) ? x : make_uint4(0u, 0u, 0u, 0u);
+      } else {
+        uint32_t e[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) e[i] = row[gn + i < N ? gn + i : N - 1];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          asm volatile("" : "+v"(e[i]));
+          e[i] = (in_k && gn + i < N) ? e[i] : 0u;
+        }
+        v[u] = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + u * 256 + threadIdx.x;
+      if (idx >= kItems) continue;
+      const int k = idx / (BN / 8), n8 = idx % (BN / 8);
+      const int c = k >> 5, q = (k >> 3) & 3, sl = k & 7;
+      const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        Bp[((c * 4 + q) * BN + 8 * n8 + i) * 8 + sl] = static_cast<uint16_t>(w[i >> 1] >> (16 * (i & 1)));
+    }
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, r16 = lane & 15;
+  auto tile_rows = [&](int rt, const uint16_t*& hrow, const uint16_t*& grow) {
+    const int row = rt * 64 + wave * 16 + r16;
+    const int64_t arow = row < M ? row : M - 1;
+    hrow = Hs + arow * K;
+    grow = Ag + arow * K;
+  };
+  auto load_frag = [&](const uint16_t* hrow, const uint16_t* grow, int c) -> bf16x8 {
+    const int k = 32 * c + 8 * q;
+    const bool in = k < K2;
+    const uint16_t* p = (k < K ? hrow + k : grow + (in ? k - K : 0));
+    uint4 x = *reinterpret_cast<const uint4*>(p);
+    asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+    if (!in) x = make_uint4(0u, 0u, 0u, 0u);
+    return __builtin_bit_cast(bf16x8, x);
+  };
+  bf16x8 a[NCH];
+  {
+    const uint16_t *hrow, *grow;
+    tile_rows(blockIdx.x, hrow, grow);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) a[c] = load_frag(hrow, grow, c);
+  }
+  float bv[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int col = n0 + j * 16 + r16;
+    bv[j] = bias[col < N ? col : N - 1];
+  }
+  for (int rt = blockIdx.x; rt < row_tiles; rt += gridDim.x) {
+    const uint16_t *hnext, *gnext;
+    tile_rows(rt + gridDim.x, hnext, gnext);
+    floatx4 acc[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    auto load_b = [&](int c, bf16x8 (&b)[J]) {
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        b[j] = *reinterpret_cast<const bf16x8*>(&Bp[((c * 4 + q) * BN + j * 16 + r16) * 8]);
+    };
+    bf16x8 b0[J], b1[J];
+    load_b(0, b0);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      bf16x8 (&bc)[J] = (c & 1) ? b1 : b0;
+      bf16x8 (&bn)[J] = (c & 1) ? b0 : b1;
+      if (c + 1 < NCH) load_b(c + 1, bn);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < J; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[c], bc[j], acc[j], 0, 0, 0);
+      a[c] = load_frag(hnext, gnext, c);
+    }
+    const int row0 = rt * 64 + wave * 16 + 4 * q;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int col = n0 + j * 16 + r16;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float z = acc[j][r] + bv[j];
+        if (relu) z = z > 0.f ? z : 0.f;
+        if (row0 + r < M && col < N) {
+          const int64_t o = static_cast<int64_t>(row0 + r) * N + col;
+          if (out_f32) static_cast<float*>(out)[o] = z;
+          else static_cast<uint16_t*>(out)[o] = f32_to_bf16(z);
+        }
+      }
+    }
+  }
+}
+
+template <int NCH>
+void launch_bf16_slab(const int32_t* sizes, const uint16_t* hs, const uint16_t* ag, const uint16_t* ws,
+                      const uint16_t* wn, const float* bias, int K, int N, int relu, int out_f32,
+                      void* out, int64_t cap_rows, hipStream_t s) {
+  constexpr int J = 4, BN = 64;
+  constexpr int lds = NCH * 4 * BN * 8 * 2;
+  constexpr int by_lds = (160 * 1024) / lds;
+  const int per_cu = by_lds < 1 ? 1 : (by_lds > 2 ? 2 : by_lds);
+  const int col_tiles = (N + BN - 1) / BN;
+  int64_t rows = (cap_rows + 63) / 64;
+  const int64_t want = (256 * per_cu + col_tiles - 1) / col_tiles;
+  if (rows > want) rows = want;
+  if (rows < 1) rows = 1;
+  const uintptr_t walign = reinterpret_cast<uintptr_t>(ws) | reinterpret_cast<uintptr_t>(wn);
+  const int wvec = (N % 8 == 0 && walign % 16 == 0) ? 1 : 0;
+  hipLaunchKernelGGL((k_linear_bf16_slab<NCH, J>), dim3(static_cast<unsigned>(rows), col_tiles), dim3(256), 0,
+                     s, sizes, hs, ag, ws, wn, bias, K, N, relu, out_f32, wvec, out);
+}
+
 }  // namespace
 
 hipError_t launch_mean_aggregate(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
@@ -683,9 +845,27 @@ hipError_t launch_sage_linear(const int32_t* sizes, const void* h_self, const vo
   if (gm < 1) gm = 1;
   const dim3 grid(static_cast<unsigned>(gm), static_cast<unsigned>((d_out + kBN - 1) / kBN)), block(256);
   if (bf16) {
-    hipLaunchKernelGGL(k_linear_bf16, grid, block, 0, s, sizes, static_cast<const uint16_t*>(h_self),
-                       static_cast<const uint16_t*>(agg), static_cast<const uint16_t*>(w_self),
-                       static_cast<const uint16_t*>(w_neigh), bias, d_in, d_out, relu, out_f32, out);
+    const uint16_t* hs = static_cast<const uint16_t*>(h_self);
+    const uint16_t* ag = static_cast<const uint16_t*>(agg);
+    const uint16_t* ws = static_cast<const uint16_t*>(w_self);
+    const uint16_t* wn = static_cast<const uint16_t*>(w_neigh);
+    const uintptr_t align = reinterpret_cast<uintptr_t>(hs) | reinterpret_cast<uintptr_t>(ag);
+    const int nch = (2 * d_in + 31) / 32;
+    if (d_in % 8 == 0 && align % 16 == 0 && nch <= 40) {
+#define GMB_SLAB16(C) \
+  launch_bf16_slab<C>(sizes, hs, ag, ws, wn, bias, d_in, d_out, relu, out_f32, out, cap_rows, s)
+      if (nch <= 2) GMB_SLAB16(2);
+      else if (nch <= 4) GMB_SLAB16(4);
+      else if (nch <= 8) GMB_SLAB16(8);
+      else if (nch <= 16) GMB_SLAB16(16);
+      else if (nch <= 24) GMB_SLAB16(24);
+      else if (nch <= 32) GMB_SLAB16(32);
+      else GMB_SLAB16(40);
+#undef GMB_SLAB16
+      return hipGetLastError();
+    }
+    hipLaunchKernelGGL(k_linear_bf16, grid, block, 0, s, sizes, hs, ag, ws, wn, bias, d_in, d_out, relu,
+                       out_f32, out);
   } else {
     if (!out_f32) return hipErrorInvalidValue;
     const float* hs = static_cast<const float*>(h_self);

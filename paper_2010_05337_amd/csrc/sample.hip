@@ -15,9 +15,9 @@
 // within its segment; hop h's block row offsets are then the segment's
 // offsets plus the totals of the earlier segments.  So no hop needs a
 // degree pass of its own:
-//   k_seed_scan   (one workgroup) seeds -> ids and table; degree scans of
-//                 segment 0 for all hops; clears the look-back words; the
-//                 first hop's sampling checks that every seed owns its slot
+//   k_seed_scan   (one workgroup) seeds -> ids; degree scans of segment 0
+//                 for all hops; clears the look-back words; the first
+//                 hop's sampling writes the seeds' table slots
 //   k_sample(h)   Floyd's algorithm per destination, one lane per draw,
 //                 Philox-keyed draws; sampled slots ranked in the group and
 //                 written in slot order; each vertex's first edge position
@@ -25,7 +25,9 @@
 //   k_assign(h)   scan of the "first occurrence" flags (new vertex number
 //                 n_dst + rank) together with the degree scans of the new
 //                 vertices for the later hops; writes every edge's local id
-//   k_cleanup     table entries of every vertex of the batch back to empty
+//   k_cleanup     table entries of every vertex of the batch back to empty;
+//                 a seed whose slot does not hold its position was listed
+//                 twice
 #include <algorithm>
 
 #include "common.hpp"
@@ -79,39 +81,41 @@ __global__ __launch_bounds__(256) void k_state_init(uint32_t* table, uint32_t* s
 // One workgroup.  Seeds -> ids[0:B] and their table slots (atomicMin, so a
 // vertex listed twice keeps its first position); segment 0's degree scans
 // for every hop; clears the look-back words and the size words.
-constexpr int kSeedBlock = 512;
 constexpr int kSeedItems = 4;
+// one workgroup: 1024 threads while the register budget allows (NV <= 4)
+template <int NV>
+constexpr int seed_block() { return NV <= 4 ? 1024 : 512; }
 
-template <int NV, bool WIDE>
-__global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga, uint32_t* table,
-                                                          uint32_t* status) {
-  __shared__ int32_t s_wave[NV * (kSeedBlock / 64)];
+// Every store of this kernel follows its reads: on gfx9 the same counter
+// tracks outstanding loads and stores, so a store issued before a load
+// would add its own latency to the wait for that load.
+template <int NV, bool WIDE, int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_seed_scan(SeedArgs a, CsrArgs ga) {
+  __shared__ int32_t s_wave[NV * (BLOCK / 64)];
   const CsrView g = view(ga);
   const int tid = threadIdx.x;
-  for (int64_t i = tid; i < a.num_zero; i += kSeedBlock) a.zero[i] = 0;
-  for (int i = tid; i < a.num_size_words; i += kSeedBlock) a.sizes[i] = 0;
   const int32_t B = a.num_seeds;
-  for (int32_t p = tid; p < B; p += kSeedBlock) {
-    const int32_t s = a.seeds[p];
-    a.ids[p] = s;
-    if (valid_vertex(s, g.num_nodes))
-      atomicMin(&table[s], static_cast<uint32_t>(p));
-    else
-      raise_status(status, GMB_STATUS_ERANGE);
-  }
-
   int32_t running[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) running[v] = 0;
-  for (int32_t base = 0; base < B; base += kSeedBlock * kSeedItems) {
+  // each thread takes kSeedItems consecutive seeds: one batch of reads (the
+  // seeds, then their row offsets), the degree scans, then the stores:
+  // block row offsets and ids (the seeds' table slots are written by the
+  // first hop's sampling, spread over its workgroups)
+  for (int32_t base = 0; base < B; base += BLOCK * kSeedItems) {
+    int32_t sd[kSeedItems];
+#pragma unroll
+    for (int q = 0; q < kSeedItems; ++q) {
+      const int32_t p = base + tid * kSeedItems + q;
+      sd[q] = a.seeds[p < B ? p : B - 1];
+    }
     int32_t deg[kSeedItems];
 #pragma unroll
     for (int q = 0; q < kSeedItems; ++q) {
       const int32_t p = base + tid * kSeedItems + q;
-      const int32_t s = a.seeds[p < B ? p : (B > 0 ? B - 1 : 0)];
-      const bool ok = p < B && valid_vertex(s, g.num_nodes);
+      const bool ok = p < B && valid_vertex(sd[q], g.num_nodes);
       int64_t b, e;
-      row_range_t<WIDE>(g, ok ? s : 0, b, e);
+      row_range_t<WIDE>(g, ok ? sd[q] : 0, b, e);
       deg[q] = ok ? static_cast<int32_t>(e - b) : 0;
     }
     int32_t sum[NV], excl[NV], total[NV];
@@ -121,7 +125,7 @@ __global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga
 #pragma unroll
       for (int q = 0; q < kSeedItems; ++q) sum[v] += clamp_degree(deg[q], a.fanout[v]);
     }
-    block_exclusive_scan_multi<kSeedBlock, NV>(sum, excl, total, s_wave);
+    block_exclusive_scan_multi<BLOCK, NV>(sum, excl, total, s_wave);
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       int32_t run = running[v] + excl[v];
@@ -133,7 +137,16 @@ __global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga
       }
       running[v] += total[v];
     }
+#pragma unroll
+    for (int q = 0; q < kSeedItems; ++q) {
+      const int32_t p = base + tid * kSeedItems + q;
+      if (p < B) a.ids[p] = sd[q];
+    }
   }
+  // look-back words and tickets of the relabel scans, size words
+  for (int64_t i = tid; i < a.num_zero; i += BLOCK) a.zero[i] = 0;
+  for (int i = tid; i < a.num_size_words; i += BLOCK) a.sizes[i] = 0;
+  __syncthreads();
   if (tid == 0) {
 #pragma unroll
     for (int v = 0; v < NV; ++v) a.totals[v] = running[v];   // segment 0's edges of hop v
@@ -153,10 +166,13 @@ __global__ __launch_bounds__(kSeedBlock) void k_seed_scan(SeedArgs a, CsrArgs ga
 #endif
 __device__ __forceinline__ void emit_edge(int32_t pos, int32_t u, int32_t* nbr, uint32_t* table,
                                           int64_t num_nodes, uint32_t* status) {
+  // the table read goes out before the store (one counter tracks both)
+  const bool ok = valid_vertex(u, num_nodes);
+  const uint32_t tag = kEdgeTag | static_cast<uint32_t>(pos);
+  const uint32_t seen = GMB_EMIT_PREREAD ? table[ok ? u : 0] : kEmpty;
   nbr[pos] = u;
-  if (valid_vertex(u, num_nodes)) {
-    const uint32_t tag = kEdgeTag | static_cast<uint32_t>(pos);
-    if (!GMB_EMIT_PREREAD || table[u] > tag) atomicMin(&table[u], tag);
+  if (ok) {
+    if (seen > tag) atomicMin(&table[u], tag);
   } else {
     raise_status(status, GMB_STATUS_ERANGE);
   }
@@ -219,14 +235,19 @@ __global__ __launch_bounds__(256) void k_sample(CsrArgs ga, const int32_t* ids, 
   const bool valid = valid_vertex(v, g.num_nodes);
   const int32_t vc = valid ? v : 0;
   deferred_fetch(fix, it);
-  const uint32_t slot = check_seeds ? table[vc] : 0u;
   int64_t begin, end;
   row_range_t<WIDE>(g, vc, begin, end);
   deferred_store(fix, tid, it);
-  if (p >= n_dst || !valid) return;   // an invalid vertex's clamped degree was 0
-  // first hop: every seed owns its table slot unless the seed list holds
-  // the vertex twice (the slot then names the first copy)
-  if (check_seeds && lane == 0 && slot != static_cast<uint32_t>(p)) raise_status(status, GMB_STATUS_EDUP);
+  if (p >= n_dst) return;
+  // first hop: the seed's table slot is its position.  A plain store: the
+  // edges emitted meanwhile lower slots to tags >= 2^31 only, so the slot
+  // ends at p whatever the order; a seed listed twice leaves one of its
+  // copies disagreeing with the slot, which the cleanup reports.
+  if (check_seeds && lane == 0) {
+    if (valid) table[v] = static_cast<uint32_t>(p);
+    else raise_status(status, GMB_STATUS_ERANGE);
+  }
+  if (!valid) return;   // an invalid vertex's clamped degree was 0
   const int64_t d = end - begin;
 
   int32_t pos = -1, u = 0;
@@ -279,8 +300,11 @@ __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* 
   const int32_t n_dst = load_size(&sizes[kNDst]);
   if (p >= n_dst) return;
   const int32_t v = ids[p];
+  if (check_seeds) {   // the seed's table slot (see k_sample)
+    if (valid_vertex(v, g.num_nodes)) table[v] = static_cast<uint32_t>(p);
+    else raise_status(status, GMB_STATUS_ERANGE);
+  }
   if (!valid_vertex(v, g.num_nodes)) return;
-  if (check_seeds && table[v] != static_cast<uint32_t>(p)) raise_status(status, GMB_STATUS_EDUP);
   int64_t begin, end;
   row_range(g, v, begin, end);
   const int64_t d = end - begin;
@@ -448,16 +472,21 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
 
 // Resets the table entries of every vertex of the batch and resolves the
 // last hop's deferred local ids (the table is not read for those).
-__global__ __launch_bounds__(256) void k_cleanup(const int32_t* ids, int64_t cap_src,
+__global__ __launch_bounds__(256) void k_cleanup(const int32_t* ids, int64_t cap_src, int32_t num_seeds,
                                                  const int32_t* final_sizes, uint32_t* table,
-                                                 int64_t num_nodes, DeferredArgs fix) {
+                                                 int64_t num_nodes, uint32_t* status, DeferredArgs fix) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   DeferredItem it = deferred_read(fix, i);
   const int32_t n = load_size(&final_sizes[kNSrc]);
   const int32_t u = ids[i < cap_src ? i : cap_src - 1];
+  const bool ok = i < n && valid_vertex(u, num_nodes);
+  // a seed's slot still holds its position unless the seed list holds the
+  // vertex twice (no later step writes a seed's slot)
+  const uint32_t slot = (ok && i < num_seeds) ? table[u] : static_cast<uint32_t>(i);
   deferred_fetch(fix, it);
   deferred_store(fix, i, it);
-  if (i < n && valid_vertex(u, num_nodes)) table[u] = kEmpty;
+  if (slot != static_cast<uint32_t>(i)) raise_status(status, GMB_STATUS_EDUP);
+  if (ok) table[u] = kEmpty;
 }
 
 inline unsigned grid_for(int64_t threads, int block = 256) {
@@ -476,13 +505,14 @@ hipError_t launch_state_init(uint32_t* table, uint32_t* status, int64_t num_node
   return hipGetLastError();
 }
 
-hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, uint32_t* table,
-                            uint32_t* status, hipStream_t s) {
-#define GMB_SEED(V)                                                                                \
-  if (g.wide)                                                                                      \
-    hipLaunchKernelGGL((k_seed_scan<V, true>), dim3(1), dim3(kSeedBlock), 0, s, a, g, table, status); \
-  else                                                                                             \
-    hipLaunchKernelGGL((k_seed_scan<V, false>), dim3(1), dim3(kSeedBlock), 0, s, a, g, table, status)
+hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, hipStream_t s) {
+#define GMB_SEED(V)                                                                          \
+  if (g.wide)                                                                                \
+    hipLaunchKernelGGL((k_seed_scan<V, true, seed_block<V>()>), dim3(1), dim3(seed_block<V>()), \
+                       0, s, a, g);                                                           \
+  else                                                                                       \
+    hipLaunchKernelGGL((k_seed_scan<V, false, seed_block<V>()>), dim3(1), dim3(seed_block<V>()), \
+                       0, s, a, g)
   switch (num_values) {
     case 1: { GMB_SEED(1); } break;
     case 2: { GMB_SEED(2); } break;
@@ -564,11 +594,12 @@ hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, 
   return hipGetLastError();
 }
 
-hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src,
-                          uint32_t* table, int64_t num_nodes, const DeferredArgs& fix, hipStream_t s) {
+hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src, int32_t num_seeds,
+                          uint32_t* table, int64_t num_nodes, uint32_t* status, const DeferredArgs& fix,
+                          hipStream_t s) {
   const int64_t threads = std::max(cap_src, fix.cap);
   hipLaunchKernelGGL(k_cleanup, dim3(grid_for(threads)), dim3(256), 0, s, ids,
-                     std::max<int64_t>(cap_src, 1), final_sizes, table, num_nodes, fix);
+                     std::max<int64_t>(cap_src, 1), num_seeds, final_sizes, table, num_nodes, status, fix);
   return hipGetLastError();
 }
 

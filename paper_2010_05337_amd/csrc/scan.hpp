@@ -104,6 +104,7 @@ __device__ bool tile_lookback_multi(uint64_t* tiles, int64_t stride, int tile,
     for (int a = 0; a < NV; ++a)
       w[a] = t >= 0 ? __hip_atomic_load(&tiles[a * stride + t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
                     : kTilePrefix;
+
     for (;;) {
       bool pending = false;
 #pragma unroll

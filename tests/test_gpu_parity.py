@@ -202,6 +202,18 @@ def test_forward_bf16(orc, dg, tiny):
     _forward_case(orc, dg, tiny, feats, w, seeds, [25, 10], 8, TOL_BF16)
 
 
+@pytest.mark.parametrize("dims,fanouts", [([12, 40, 5], [3, 6]), ([64, 256, 47], [10, 4]),
+                                          ([256, 64, 130], [2, 3])])
+def test_forward_bf16_shapes(orc, dg, tiny, dims, fanouts):
+    """bf16 layers on the LDS-slab kernel (d_in a multiple of 8: 40, 64, 256,
+    K up to 512, output widths 5, 47, 130) and on the general kernel
+    (d_in = 12)."""
+    feats = dg.features(10000, dims[0], 41, "bf16")
+    w = dg.sage_weights(dims, 42, "bf16")
+    seeds = dg.permutation(10000, 43)[:300]
+    _forward_case(orc, dg, tiny, feats, w, seeds, fanouts, 44, TOL_BF16)
+
+
 def test_forward_wide_model_f32(orc, dg):
     """The paper's model shape (3 layers, hidden 256, fan-outs 15/10/5) on a
     small power-law graph: many rows of the 64-row tiles, K = 200 and 512."""
