@@ -190,6 +190,12 @@ def sage_weights(dims, seed: int, dtype: str = "f32") -> Weights:
     return Weights(list(dims), ws, wn, bs, dtype)
 
 
+def labels(n: int, num_classes: int, seed: int) -> np.ndarray:
+    """A class label per vertex, uniform in [0, num_classes), int32."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.integers(0, num_classes, size=n).astype(np.int32)
+
+
 def permutation(n: int, seed: int) -> np.ndarray:
     rng = np.random.Generator(np.random.PCG64(seed))
     return rng.permutation(n).astype(np.int32)

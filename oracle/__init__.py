@@ -21,6 +21,10 @@ Parity status per function:
   mean_aggregate    pinned: dense D^-1 A H with numpy
   sage_forward      pinned: full-neighbourhood special case == full-graph
                     dense GraphSAGE (numpy)
+  softmax_xent,     pinned: central finite differences of the loss in every
+  sage_backward     parameter (fp64), and the full-neighbourhood special
+                    case == torch autograd (fp64, CPU) of the dense
+                    full-graph model
 """
 from __future__ import annotations
 
@@ -50,7 +54,7 @@ def build(force: bool = False) -> str:
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-Wall", _SRC,
-                               "-o", tmp])
+                               "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -87,6 +91,14 @@ def lib():
         L.orc_mean_aggregate.argtypes = [i64, vp, vp, vp, i64, vp]
         L.orc_sage_linear.restype = None
         L.orc_sage_linear.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, ctypes.c_int, vp]
+        L.orc_softmax_xent.restype = ctypes.c_double
+        L.orc_softmax_xent.argtypes = [i64, i64, vp, vp, vp]
+        L.orc_sage_linear_backward.restype = None
+        L.orc_sage_linear_backward.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_mean_backward.restype = None
+        L.orc_mean_backward.argtypes = [i64, vp, vp, vp, i64, vp]
+        L.orc_relu_backward.restype = None
+        L.orc_relu_backward.argtypes = [i64, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -226,3 +238,89 @@ def sage_forward(blocks, X: np.ndarray, w_self, w_neigh, bias):
         H = sage_linear(H[:blk.n_dst], m, w_self[l], w_neigh[l], bias[l], relu=(l < L - 1))
         outs.append(H)
     return H, outs
+
+
+# ---------------------------------------------------------------- O7
+
+def softmax_xent(logits: np.ndarray, labels) -> tuple:
+    """Mean softmax cross-entropy of the rows against labels and its
+    gradient dL/dlogits.  Returns (loss, dlogits)."""
+    z = np.ascontiguousarray(logits, dtype=np.float64)
+    y = np.ascontiguousarray(labels, dtype=np.int64)
+    n, C = z.shape
+    if y.shape != (n,) or (n and (y.min() < 0 or y.max() >= C)):
+        raise ValueError("labels must be [n] in [0, C)")
+    dz = np.zeros_like(z)
+    loss = lib().orc_softmax_xent(n, C, _p(z), _p(y), _p(dz))
+    return float(loss), dz
+
+
+def sage_forward_train(blocks, X: np.ndarray, w_self, w_neigh, bias):
+    """The forward of sage_forward that also keeps each layer's mean.
+    Returns (logits, [H_1, ..., H_L], [m_0, ..., m_{L-1}])."""
+    H = np.ascontiguousarray(X, dtype=np.float64)
+    outs, means = [], []
+    L = len(blocks)
+    for l, blk in enumerate(blocks):
+        m = mean_aggregate(blk, H)
+        H = sage_linear(H[:blk.n_dst], m, w_self[l], w_neigh[l], bias[l], relu=(l < L - 1))
+        outs.append(H)
+        means.append(m)
+    return H, outs, means
+
+
+def sage_backward(blocks, X: np.ndarray, w_self, w_neigh, hidden, means, dlogits):
+    """Gradients of the loss in every parameter, from dL/dlogits back to
+    layer 0 (the input features are not trained).  hidden and means come
+    from sage_forward_train.  Returns (dW_self, dW_neigh, db), lists by
+    layer."""
+    L = len(blocks)
+    dWs, dWn, dbs = [None] * L, [None] * L, [None] * L
+    dOut = np.ascontiguousarray(dlogits, dtype=np.float64)
+    for l in range(L - 1, -1, -1):
+        blk = blocks[l]
+        Hin = np.ascontiguousarray(X if l == 0 else hidden[l - 1], dtype=np.float64)
+        ws = np.ascontiguousarray(w_self[l], dtype=np.float64)
+        wn = np.ascontiguousarray(w_neigh[l], dtype=np.float64)
+        d_in, d_out = ws.shape
+        n = blk.n_dst
+        if l == L - 1:
+            dZ = dOut
+        else:
+            out = np.ascontiguousarray(hidden[l], dtype=np.float64)
+            dZ = np.zeros_like(out)
+            lib().orc_relu_backward(out.size, _p(out), _p(dOut), _p(dZ))
+        dZ = np.ascontiguousarray(dZ)
+        dWs[l] = np.zeros((d_in, d_out))
+        dWn[l] = np.zeros((d_in, d_out))
+        dbs[l] = np.zeros(d_out)
+        Hd = np.ascontiguousarray(Hin[:n])
+        m = np.ascontiguousarray(means[l], dtype=np.float64)
+        if l > 0:
+            dH = np.zeros((blk.n_src, d_in))
+            dM = np.zeros((n, d_in))
+            dHd = np.zeros((n, d_in))
+            lib().orc_sage_linear_backward(n, d_in, d_out, _p(Hd), _p(m), _p(ws), _p(wn), _p(dZ),
+                                           _p(dWs[l]), _p(dWn[l]), _p(dbs[l]), _p(dHd), _p(dM))
+            dH[:n] = dHd
+            lib().orc_mean_backward(n, _p(blk.indptr), _p(blk.local), _p(dM), d_in, _p(dH))
+            dOut = dH
+        else:
+            lib().orc_sage_linear_backward(n, d_in, d_out, _p(Hd), _p(m), _p(ws), _p(wn), _p(dZ),
+                                           _p(dWs[l]), _p(dWn[l]), _p(dbs[l]), None, None)
+    return dWs, dWn, dbs
+
+
+def sgd(params, grads, lr: float):
+    """p - lr * g for every array."""
+    return [np.asarray(p, dtype=np.float64) - lr * np.asarray(g, dtype=np.float64)
+            for p, g in zip(params, grads)]
+
+
+def sage_train_step(blocks, X: np.ndarray, w_self, w_neigh, bias, labels, lr: float):
+    """Forward, loss, backward and one SGD step.  Returns (loss, logits,
+    (dW_self, dW_neigh, db), (new W_self, new W_neigh, new b))."""
+    logits, hidden, means = sage_forward_train(blocks, X, w_self, w_neigh, bias)
+    loss, dz = softmax_xent(logits, labels)
+    dWs, dWn, dbs = sage_backward(blocks, X, w_self, w_neigh, hidden, means, dz)
+    return loss, logits, (dWs, dWn, dbs), (sgd(w_self, dWs, lr), sgd(w_neigh, dWn, lr), sgd(bias, dbs, lr))

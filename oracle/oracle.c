@@ -40,6 +40,7 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#include <math.h>
 
 /* ------------------------------------------------------------------ */
 /* O1: Philox4x32-10 (Salmon et al., SC'11, Section 4 and Table 2).     */
@@ -326,4 +327,86 @@ void orc_sage_linear(int64_t n_dst, int64_t d_in, int64_t d_out, const double* H
       out[v * d_out + o] = (relu && z < 0.0) ? 0.0 : z;
     }
   }
+}
+
+/* ------------------------------------------------------------------ */
+/* O7: one training step on the mini-batch (the trainer's iteration of    */
+/* Section III-E: forward, backward, gradient update).  The loss is the   */
+/* mean softmax cross-entropy of the targets' logits against their labels */
+/* (node classification, the task of Section IV; the paper prints no loss */
+/* formula, so this is the standard reading).  Gradients follow Eq. (1)   */
+/* by the chain rule, layer by layer from the last.                       */
+
+/* loss = (1/n) sum_v -log softmax(z_v)[y_v];  dz_v = (softmax(z_v) - e_{y_v}) / n.
+ * z, dz are [n, C] row-major.  Returns the loss. */
+double orc_softmax_xent(int64_t n, int64_t C, const double* z, const int64_t* y, double* dz) {
+  double loss = 0.0;
+  for (int64_t v = 0; v < n; ++v) {
+    const double* row = z + v * C;
+    double mx = row[0];
+    for (int64_t c = 1; c < C; ++c) mx = row[c] > mx ? row[c] : mx;
+    double sum = 0.0;
+    for (int64_t c = 0; c < C; ++c) sum += exp(row[c] - mx);
+    loss += -(row[y[v]] - mx - log(sum));
+    for (int64_t c = 0; c < C; ++c) {
+      const double p = exp(row[c] - mx) / sum;
+      dz[v * C + c] = (p - (c == y[v] ? 1.0 : 0.0)) / (double)n;
+    }
+  }
+  return n > 0 ? loss / (double)n : 0.0;
+}
+
+/* Backward of out = H W_self + m W_neigh + b over n rows, given dZ = dL/d(out)
+ * [n, d_out] (the activation already applied):
+ *   dW_self = H^T dZ, dW_neigh = m^T dZ  [d_in, d_out];  db = column sums of dZ;
+ *   dH = dZ W_self^T, dM = dZ W_neigh^T  [n, d_in]  (skipped when NULL). */
+void orc_sage_linear_backward(int64_t n, int64_t d_in, int64_t d_out, const double* H,
+                              const double* m, const double* w_self, const double* w_neigh,
+                              const double* dZ, double* dW_self, double* dW_neigh, double* db,
+                              double* dH, double* dM) {
+  for (int64_t c = 0; c < d_in; ++c)
+    for (int64_t o = 0; o < d_out; ++o) {
+      double s = 0.0, t = 0.0;
+      for (int64_t v = 0; v < n; ++v) {
+        s += H[v * d_in + c] * dZ[v * d_out + o];
+        t += m[v * d_in + c] * dZ[v * d_out + o];
+      }
+      dW_self[c * d_out + o] = s;
+      dW_neigh[c * d_out + o] = t;
+    }
+  for (int64_t o = 0; o < d_out; ++o) {
+    double s = 0.0;
+    for (int64_t v = 0; v < n; ++v) s += dZ[v * d_out + o];
+    db[o] = s;
+  }
+  if (!dH || !dM) return;
+  for (int64_t v = 0; v < n; ++v)
+    for (int64_t c = 0; c < d_in; ++c) {
+      double s = 0.0, t = 0.0;
+      for (int64_t o = 0; o < d_out; ++o) {
+        s += dZ[v * d_out + o] * w_self[c * d_out + o];
+        t += dZ[v * d_out + o] * w_neigh[c * d_out + o];
+      }
+      dH[v * d_in + c] = s;
+      dM[v * d_in + c] = t;
+    }
+}
+
+/* Backward of the mean: every edge (v <- u) of the block passes dM[v] / k_v
+ * to its source, dH[local[e]] += dM[v] / k_v (dH accumulates). */
+void orc_mean_backward(int64_t n_dst, const int64_t* indptr, const int64_t* local,
+                       const double* dM, int64_t d, double* dH) {
+  for (int64_t v = 0; v < n_dst; ++v) {
+    const int64_t k = indptr[v + 1] - indptr[v];
+    for (int64_t e = indptr[v]; e < indptr[v + 1]; ++e) {
+      double* h = dH + local[e] * d;
+      for (int64_t c = 0; c < d; ++c) h[c] += dM[v * d + c] / (double)k;
+    }
+  }
+}
+
+/* Backward of out = max(z, 0) through the output: dZ = dOut where out > 0,
+ * else 0 (the derivative at 0 is taken as 0). */
+void orc_relu_backward(int64_t n, const double* out, const double* dOut, double* dZ) {
+  for (int64_t i = 0; i < n; ++i) dZ[i] = out[i] > 0.0 ? dOut[i] : 0.0;
 }

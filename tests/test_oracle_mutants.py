@@ -16,6 +16,7 @@ import pytest
 import test_oracle_blocks as tb
 import test_oracle_rng as tr
 import test_oracle_sampling as ts
+import test_oracle_train as tt
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -47,6 +48,18 @@ MUTANTS = {
                               "int64_t u = indices[indptr[v] + (d - 1 - slots[q])];"),
     # sampling: fan-out of the wrong layer (hop index instead of layer index)
     "sample_wrong_layer_fanout": ("int64_t f = fanouts[l];", "int64_t f = fanouts[hop];"),
+    # backward: ReLU mask dropped
+    "bwd_no_relu_mask": ("dZ[i] = out[i] > 0.0 ? dOut[i] : 0.0;", "dZ[i] = dOut[i];"),
+    # backward: mean's 1/k missing on the way back
+    "bwd_mean_unscaled": ("h[c] += dM[v * d + c] / (double)k;", "h[c] += dM[v * d + c];"),
+    # backward: input gradient through W_self transposed
+    "bwd_self_transposed": ("s += dZ[v * d_out + o] * w_self[c * d_out + o];",
+                            "s += dZ[v * d_out + o] * w_self[o * d_in + c];"),
+    # backward: loss gradient not divided by the batch size
+    "bwd_xent_not_mean": ("dz[v * C + c] = (p - (c == y[v] ? 1.0 : 0.0)) / (double)n;",
+                          "dz[v * C + c] = (p - (c == y[v] ? 1.0 : 0.0));"),
+    # backward: neighbour weight gradient taken from the self input
+    "bwd_neigh_from_self": ("t += m[v * d_in + c] * dZ[v * d_out + o];", "t += H[v * d_in + c] * dZ[v * d_out + o];"),
 }
 
 
@@ -62,7 +75,7 @@ def _build_mutant(tmpdir, name):
     # a file name of its own: a shared object is matched by name when another
     # library asks for it, so the mutant must not be called liboracle.so
     so = os.path.join(d, f"liboracle_{name}.so")
-    subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-w", path, "-o", so])
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-w", path, "-o", so, "-lm"])
     spec = importlib.util.spec_from_file_location(f"oracle_mutant_{name}",
                                                   os.path.join(ROOT, "oracle", "__init__.py"))
     mod = importlib.util.module_from_spec(spec)
@@ -109,6 +122,9 @@ def test_pins_catch_mutant(name, tmp_path, dg):
         "rmat": lambda: tb.test_rmat_blocks_invariants_with_hubs(mut, dg),
         "mean": lambda: tb.test_mean_aggregate_matches_dense(mut, dg, tiny),
         "dense": lambda: tb.test_full_neighbourhood_equals_dense_sage(mut, dg, 2),
+        "xent": lambda: tt.test_softmax_xent_value_and_gradient(mut),
+        "train_fd": lambda: tt.test_backward_matches_finite_differences(mut, dg),
+        "train_dense": lambda: tt.test_full_neighbourhood_gradients_equal_dense_autograd(mut, dg, 2),
     }
     caught = next((k for k, fn in checks.items() if _fails(fn)), None)
     assert caught is not None, f"mutant {name} passed every pin"
