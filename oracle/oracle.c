@@ -364,15 +364,16 @@ void orc_sage_linear_backward(int64_t n, int64_t d_in, int64_t d_out, const doub
                               const double* m, const double* w_self, const double* w_neigh,
                               const double* dZ, double* dW_self, double* dW_neigh, double* db,
                               double* dH, double* dM) {
-  for (int64_t c = 0; c < d_in; ++c)
-    for (int64_t o = 0; o < d_out; ++o) {
-      double s = 0.0, t = 0.0;
-      for (int64_t v = 0; v < n; ++v) {
-        s += H[v * d_in + c] * dZ[v * d_out + o];
-        t += m[v * d_in + c] * dZ[v * d_out + o];
+  /* dW[c][o] = sum over v = 0, 1, ..., n-1 in that order; v is the outer
+   * loop so that every pass reads two rows of the inputs */
+  for (int64_t i = 0; i < d_in * d_out; ++i) dW_self[i] = dW_neigh[i] = 0.0;
+  for (int64_t v = 0; v < n; ++v)
+    for (int64_t c = 0; c < d_in; ++c) {
+      const double hc = H[v * d_in + c], mc = m[v * d_in + c];
+      for (int64_t o = 0; o < d_out; ++o) {
+        dW_self[c * d_out + o] += hc * dZ[v * d_out + o];
+        dW_neigh[c * d_out + o] += mc * dZ[v * d_out + o];
       }
-      dW_self[c * d_out + o] = s;
-      dW_neigh[c * d_out + o] = t;
     }
   for (int64_t o = 0; o < d_out; ++o) {
     double s = 0.0;

@@ -59,7 +59,8 @@ MUTANTS = {
     "bwd_xent_not_mean": ("dz[v * C + c] = (p - (c == y[v] ? 1.0 : 0.0)) / (double)n;",
                           "dz[v * C + c] = (p - (c == y[v] ? 1.0 : 0.0));"),
     # backward: neighbour weight gradient taken from the self input
-    "bwd_neigh_from_self": ("t += m[v * d_in + c] * dZ[v * d_out + o];", "t += H[v * d_in + c] * dZ[v * d_out + o];"),
+    "bwd_neigh_from_self": ("const double hc = H[v * d_in + c], mc = m[v * d_in + c];",
+                            "const double hc = H[v * d_in + c], mc = H[v * d_in + c];"),
 }
 
 
