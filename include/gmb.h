@@ -212,7 +212,8 @@ size_t gmb_forward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weig
 int64_t gmb_forward_hidden_offset(const gmb_blocks* blocks, const gmb_sage_weights* weights,
                                   int32_t layer);
 
-/* Runs the L layers over the blocks.
+/* Runs the L layers over the blocks (the workspace keeps every layer's
+ * mean and hidden output, which gmb_sage_backward reads).
  *   x       device [blocks->blk[0].cap_src, dims[0]] in weights->dtype: the
  *           gathered input features of block 0's sources (rows beyond
  *           n_src are not read).
@@ -225,6 +226,59 @@ int64_t gmb_forward_hidden_offset(const gmb_blocks* blocks, const gmb_sage_weigh
  * the hidden activations are rounded to bf16 before the next product. */
 int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
                      float* logits, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- training step (the trainer's iteration of Section III-E) ---------- */
+
+/* Gradient arrays of an L-layer model, one per weight array, fp32 and laid
+ * out like the weights (d_self[l], d_neigh[l]: [dims[l]][dims[l+1]],
+ * d_bias[l]: [dims[l+1]]).  Device pointers, caller-owned. */
+typedef struct {
+  int32_t num_layers;
+  int32_t reserved;
+  float* d_self[GMB_MAX_LAYERS];
+  float* d_neigh[GMB_MAX_LAYERS];
+  float* d_bias[GMB_MAX_LAYERS];
+} gmb_sage_grads;
+
+/* Bytes of workspace gmb_sage_backward needs (0 for bad arguments,
+ * including a model the training step does not support: bf16 weights,
+ * hidden dims not a multiple of 4, a dims[l] above 640 for l >= 2). */
+size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights);
+
+/* Gradients of the loss L = (1/B) sum over the B seeds of the softmax
+ * cross-entropy of the seed's logits against its label, in every weight
+ * and bias (the input features are not trained).  Node classification is
+ * the task the paper trains (Section IV); its loss is not printed, this is
+ * the standard one.  The backward follows Eq. (1) layer by layer from the
+ * last: with dZ the gradient at a layer's pre-activation (ReLU passes it
+ * where the layer's output is > 0), dW_self = H_dst^T dZ, dW_neigh = M^T dZ,
+ * db = the column sums of dZ, and the layer input receives dZ W_self^T on
+ * its destination rows plus, over every block edge (v <- u), its share
+ * (dZ W_neigh^T)[v] / k_v of the mean.
+ *   blocks, x, weights  as given to the gmb_sage_forward call that produced
+ *                       `logits`; fp32 only.
+ *   logits   device fp32 [num_seeds, dims[L]] from that call.
+ *   labels   device int32 [num_seeds], the class of each seed in
+ *            [0, dims[L]) (a label outside it is a data error: that row's
+ *            loss term is 0 and its gradient unspecified, in bounds).
+ *   fwd_ws   that call's workspace (it keeps every layer's mean and hidden
+ *            output), unchanged since; fwd_ws_bytes its size.
+ *   grads    where the gradients go (overwritten).
+ *   loss     device fp32 scalar receiving L, or NULL.
+ *   ws       device workspace of >= gmb_backward_workspace_bytes() bytes,
+ *            256-byte aligned.
+ * Each weight gradient is summed over the rows in a fixed order (no
+ * atomics), so the last layer's gradients are the same on every run; the
+ * gradient that flows into the input of layers >= 1 accumulates with fp32
+ * atomic adds, so the gradients of the layers below the last can differ in
+ * their last bits between runs. */
+int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
+                      const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
+                      const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, void* stream);
+
+/* One SGD step: every weight array W -= lr * dW, every bias b -= lr * db,
+ * in place on the device arrays that `weights` points to (fp32). */
+int gmb_sgd_update(const gmb_sage_weights* weights, const gmb_sage_grads* grads, float lr, void* stream);
 
 #ifdef __cplusplus
 }

@@ -31,7 +31,8 @@ EXPORTS = (
     "gmb_abi_version", "gmb_last_error", "gmb_sampler_state_bytes", "gmb_sampler_state_init",
     "gmb_state_status_word", "gmb_read_status", "gmb_sample_workspace_bytes", "gmb_sample_blocks",
     "gmb_read_sizes", "gmb_gather_features", "gmb_forward_workspace_bytes",
-    "gmb_forward_hidden_offset", "gmb_sage_forward",
+    "gmb_forward_hidden_offset", "gmb_sage_forward", "gmb_backward_workspace_bytes",
+    "gmb_sage_backward", "gmb_sgd_update",
 )
 
 
@@ -65,6 +66,13 @@ class WeightsStruct(ctypes.Structure):
                 ("w_self", ctypes.c_void_p * GMB_MAX_LAYERS),
                 ("w_neigh", ctypes.c_void_p * GMB_MAX_LAYERS),
                 ("bias", ctypes.c_void_p * GMB_MAX_LAYERS)]
+
+
+class GradsStruct(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("d_self", ctypes.c_void_p * GMB_MAX_LAYERS),
+                ("d_neigh", ctypes.c_void_p * GMB_MAX_LAYERS),
+                ("d_bias", ctypes.c_void_p * GMB_MAX_LAYERS)]
 
 
 _lib = None
@@ -108,6 +116,15 @@ def lib() -> ctypes.CDLL:
         L.gmb_sage_forward.restype = ctypes.c_int
         L.gmb_sage_forward.argtypes = [ctypes.POINTER(BlocksStruct), vp, ctypes.POINTER(WeightsStruct),
                                        vp, vp, sz, vp]
+        L.gmb_backward_workspace_bytes.restype = sz
+        L.gmb_backward_workspace_bytes.argtypes = [ctypes.POINTER(BlocksStruct),
+                                                   ctypes.POINTER(WeightsStruct)]
+        L.gmb_sage_backward.restype = ctypes.c_int
+        L.gmb_sage_backward.argtypes = [ctypes.POINTER(BlocksStruct), vp, ctypes.POINTER(WeightsStruct), vp, vp,
+                                        vp, sz, ctypes.POINTER(GradsStruct), vp, vp, sz, vp]
+        L.gmb_sgd_update.restype = ctypes.c_int
+        L.gmb_sgd_update.argtypes = [ctypes.POINTER(WeightsStruct), ctypes.POINTER(GradsStruct),
+                                     ctypes.c_float, vp]
         _lib = L
     return _lib
 
@@ -377,3 +394,60 @@ def sage_forward(blocks: Blocks, feats: torch.Tensor, weights: SageWeights,
         h = workspace[off:off + n * d * es].view(weights.torch_dtype).view(n, d)
         hidden.append(h)
     return logits, hidden
+
+
+# ---------------------------------------------------------------- training
+
+class SageGrads:
+    """fp32 gradient arrays laid out like the weights (device tensors)."""
+
+    def __init__(self, weights: SageWeights):
+        dev = weights.w_self[0].device
+        self.d_self = [torch.zeros(w.shape, dtype=torch.float32, device=dev) for w in weights.w_self]
+        self.d_neigh = [torch.zeros(w.shape, dtype=torch.float32, device=dev) for w in weights.w_neigh]
+        self.d_bias = [torch.zeros(b.shape, dtype=torch.float32, device=dev) for b in weights.bias]
+        g = GradsStruct()
+        g.num_layers = len(self.d_self)
+        for l in range(g.num_layers):
+            g.d_self[l] = self.d_self[l].data_ptr()
+            g.d_neigh[l] = self.d_neigh[l].data_ptr()
+            g.d_bias[l] = self.d_bias[l].data_ptr()
+        self.struct = g
+
+
+def backward_workspace_bytes(blocks: Blocks, weights: SageWeights) -> int:
+    return lib().gmb_backward_workspace_bytes(ctypes.byref(blocks.struct), ctypes.byref(weights.struct))
+
+
+def sage_backward(blocks: Blocks, feats: torch.Tensor, weights: SageWeights, logits: torch.Tensor,
+                  labels: torch.Tensor, fwd_workspace: torch.Tensor, grads: SageGrads | None = None,
+                  loss: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+    """Gradients of the mean softmax cross-entropy of `logits` (from the
+    sage_forward call that used `fwd_workspace`) against `labels` (device
+    int32, one per seed).  Returns (grads, loss) with loss a 1-element
+    float32 device tensor."""
+    _require_cuda(labels, "labels")
+    if labels.dtype != torch.int32 or labels.numel() < blocks.num_seeds:
+        raise TypeError("labels must be int32 with one entry per seed")
+    need = backward_workspace_bytes(blocks, weights)
+    if need == 0:
+        _check(-1)
+    if workspace is None or workspace.numel() < need or workspace.data_ptr() % 256:
+        _, workspace = _aligned_bytes(need, feats.device)
+    if grads is None:
+        grads = SageGrads(weights)
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=feats.device)
+    _check(lib().gmb_sage_backward(ctypes.byref(blocks.struct), ctypes.c_void_p(feats.data_ptr()),
+                                   ctypes.byref(weights.struct), ctypes.c_void_p(logits.data_ptr()),
+                                   ctypes.c_void_p(labels.data_ptr()),
+                                   ctypes.c_void_p(fwd_workspace.data_ptr()), fwd_workspace.numel(),
+                                   ctypes.byref(grads.struct), ctypes.c_void_p(loss.data_ptr()),
+                                   ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream_handle()))
+    return grads, loss
+
+
+def sgd_update(weights: SageWeights, grads: SageGrads, lr: float):
+    """W -= lr * dW and b -= lr * db in place (fp32 weights)."""
+    _check(lib().gmb_sgd_update(ctypes.byref(weights.struct), ctypes.byref(grads.struct), float(lr),
+                                _stream_handle()))

@@ -130,7 +130,7 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
 // ---- forward workspace plan --------------------------------------------
 
 struct ForwardPlan {
-  size_t off_agg;
+  size_t off_agg[GMB_MAX_LAYERS];      // every layer's mean (kept for the backward)
   size_t off_hidden[GMB_MAX_LAYERS];
   size_t total;
 };
@@ -167,12 +167,11 @@ int plan_forward(const gmb_blocks* b, const gmb_sage_weights* w, ForwardPlan* pl
                   static_cast<long long>(b->blk[l - 1].cap_dst));
   const size_t es = w->dtype == GMB_BF16 ? 2 : 4;
   ForwardPlan p{};
-  size_t agg = 0;
-  for (int l = 0; l < w->num_layers; ++l)
-    agg = std::max(agg, static_cast<size_t>(std::max<int64_t>(b->blk[l].cap_dst, 1)) * w->dims[l] * es);
   size_t off = 0;
-  p.off_agg = off;
-  off = align_up(off + agg);
+  for (int l = 0; l < w->num_layers; ++l) {
+    p.off_agg[l] = off;
+    off = align_up(off + static_cast<size_t>(std::max<int64_t>(b->blk[l].cap_dst, 1)) * w->dims[l] * es);
+  }
   for (int l = 0; l + 1 < w->num_layers; ++l) {
     p.off_hidden[l] = off;
     off = align_up(off + static_cast<size_t>(std::max<int64_t>(b->blk[l].cap_dst, 1)) * w->dims[l + 1] * es);
@@ -408,10 +407,10 @@ int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_wei
   const int L = weights->num_layers;
   const int bf16 = weights->dtype == GMB_BF16;
   char* base = static_cast<char*>(ws);
-  void* agg = base + p.off_agg;
   const void* h_in = x;
   for (int l = 0; l < L; ++l) {
     const gmb_block& bk = blocks->blk[l];
+    void* agg = base + p.off_agg[l];
     const int d_in = weights->dims[l], d_out = weights->dims[l + 1];
     const bool last = (l == L - 1);
     void* h_out = last ? static_cast<void*>(logits) : static_cast<void*>(base + p.off_hidden[l]);
@@ -424,6 +423,157 @@ int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_wei
     if (e != hipSuccess) return hip_fail(e, "linear launch");
     h_in = h_out;
   }
+  return ok();
+}
+
+}  // extern "C"
+
+// ---- training step ------------------------------------------------------
+
+namespace {
+
+struct BackwardPlan {
+  int ldz[GMB_MAX_LAYERS];   // row stride of dZ of layer l (floats, multiple of 4)
+  size_t off_a, off_b, off_dm, off_part, off_partdb, off_lossrows;
+  size_t total;
+};
+
+int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* plan) {
+  ForwardPlan fp;
+  int st = plan_forward(b, w, &fp);
+  if (st != GMB_OK) return st;
+  if (w->dtype != GMB_F32) return fail(GMB_EINVAL, "the training step is fp32 only");
+  const int L = w->num_layers;
+  for (int l = 1; l < L; ++l)
+    if (w->dims[l] % 4) return fail(GMB_EINVAL, "hidden dims[%d]=%d is not a multiple of 4", l, w->dims[l]);
+  for (int l = 1; l < L; ++l)
+    if (w->dims[l + 1] > 640) return fail(GMB_EINVAL, "dims[%d]=%d above 640 (input-gradient kernel)", l + 1, w->dims[l + 1]);
+  BackwardPlan p{};
+  size_t buf = 0, dm = 0, part = 0, partdb = 0;
+  for (int l = 0; l < L; ++l) {
+    const int d_in = w->dims[l], d_out = w->dims[l + 1];
+    const gmb_block& k = b->blk[l];
+    p.ldz[l] = (l == L - 1) ? (d_out + 3) / 4 * 4 : d_out;
+    buf = std::max(buf, static_cast<size_t>(std::max<int64_t>(k.cap_dst, 1)) * p.ldz[l]);
+    if (l > 0) {
+      buf = std::max(buf, static_cast<size_t>(std::max<int64_t>(k.cap_src, 1)) * d_in);
+      dm = std::max(dm, static_cast<size_t>(std::max<int64_t>(k.cap_dst, 1)) * d_in);
+    }
+    const size_t parts = gmb::wgrad_parts(std::max<int64_t>(k.cap_dst, 1), d_in, d_out);
+    part = std::max(part, parts * gmb::wgrad_k2p(d_in) * d_out);
+    partdb = std::max(partdb, parts * d_out);
+  }
+  size_t off = 0;
+  p.off_a = off;
+  off = align_up(off + 4 * buf);
+  p.off_b = off;
+  off = align_up(off + 4 * buf);
+  p.off_dm = off;
+  off = align_up(off + 4 * std::max<size_t>(dm, 1));
+  p.off_part = off;
+  off = align_up(off + 4 * part);
+  p.off_partdb = off;
+  off = align_up(off + 4 * partdb);
+  p.off_lossrows = off;
+  off = align_up(off + 4 * static_cast<size_t>(std::max(b->num_seeds, 1)));
+  p.total = off;
+  *plan = p;
+  return GMB_OK;
+}
+
+int check_grads(const gmb_sage_grads* g, const gmb_sage_weights* w) {
+  if (!g) return fail(GMB_EINVAL, "grads is NULL");
+  if (g->num_layers != w->num_layers)
+    return fail(GMB_EINVAL, "grads have %d layers, weights %d", g->num_layers, w->num_layers);
+  for (int l = 0; l < w->num_layers; ++l)
+    if (!g->d_self[l] || !g->d_neigh[l] || !g->d_bias[l]) return fail(GMB_EINVAL, "layer %d gradient is NULL", l);
+  return GMB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights) {
+  BackwardPlan p;
+  if (plan_backward(blocks, weights, &p) != GMB_OK) return 0;
+  return p.total;
+}
+
+int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
+                      const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
+                      const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, void* stream) {
+  BackwardPlan p;
+  int st = plan_backward(blocks, weights, &p);
+  if (st != GMB_OK) return st;
+  ForwardPlan fp;
+  plan_forward(blocks, weights, &fp);
+  st = check_grads(grads, weights);
+  if (st != GMB_OK) return st;
+  if (!x || !logits || (!labels && blocks->num_seeds > 0)) return fail(GMB_EINVAL, "x, logits or labels is NULL");
+  if (!fwd_ws || fwd_ws_bytes < fp.total) return fail(GMB_ENOSPC, "forward workspace missing or too small");
+  if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign || reinterpret_cast<uintptr_t>(fwd_ws) % kAlign)
+    return fail(GMB_EINVAL, "workspaces must be 256-byte aligned");
+  if (ws_bytes < p.total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p.total);
+  const hipStream_t s = as_stream(stream);
+  const int L = weights->num_layers;
+  char* base = static_cast<char*>(ws);
+  const char* fbase = static_cast<const char*>(fwd_ws);
+  float* cur = reinterpret_cast<float*>(base + p.off_a);
+  float* other = reinterpret_cast<float*>(base + p.off_b);
+  float* dM = reinterpret_cast<float*>(base + p.off_dm);
+  float* part = reinterpret_cast<float*>(base + p.off_part);
+  float* partdb = reinterpret_cast<float*>(base + p.off_partdb);
+  hipError_t e = gmb::launch_xent(logits, labels, blocks->num_seeds, weights->dims[L], p.ldz[L - 1], cur,
+                                  reinterpret_cast<float*>(base + p.off_lossrows), loss, s);
+  if (e != hipSuccess) return hip_fail(e, "loss launch");
+  for (int l = L - 1; l >= 0; --l) {
+    const gmb_block& bk = blocks->blk[l];
+    const int d_in = weights->dims[l], d_out = weights->dims[l + 1];
+    const float* h_in = l == 0 ? static_cast<const float*>(x)
+                               : reinterpret_cast<const float*>(fbase + fp.off_hidden[l - 1]);
+    const float* m = reinterpret_cast<const float*>(fbase + fp.off_agg[l]);
+    e = gmb::launch_wgrad(bk.sizes, h_in, m, d_in, cur, p.ldz[l], d_out, std::max<int64_t>(bk.cap_dst, 1), part,
+                          partdb, grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], s);
+    if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
+    if (l == 0) break;
+    e = gmb::launch_dgrad(bk.sizes, cur, p.ldz[l], d_out, static_cast<const float*>(weights->w_self[l]),
+                          static_cast<const float*>(weights->w_neigh[l]), d_in, other, dM, bk.cap_dst, s);
+    if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
+    e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, dM, d_in, other, bk.cap_dst, bk.cap_src, s);
+    if (e != hipSuccess) return hip_fail(e, "mean-backward launch");
+    const gmb_block& below = blocks->blk[l - 1];
+    e = gmb::launch_relu_mask(below.sizes, h_in, d_in, other, below.cap_dst, s);
+    if (e != hipSuccess) return hip_fail(e, "activation-backward launch");
+    std::swap(cur, other);
+  }
+  return ok();
+}
+
+int gmb_sgd_update(const gmb_sage_weights* weights, const gmb_sage_grads* grads, float lr, void* stream) {
+  if (!weights) return fail(GMB_EINVAL, "weights is NULL");
+  if (weights->dtype != GMB_F32) return fail(GMB_EINVAL, "the update is fp32 only");
+  if (weights->num_layers < 1 || weights->num_layers > GMB_MAX_LAYERS)
+    return fail(GMB_EINVAL, "num_layers=%d outside 1..%d", weights->num_layers, GMB_MAX_LAYERS);
+  int st = check_grads(grads, weights);
+  if (st != GMB_OK) return st;
+  gmb::SgdArgs a{};
+  for (int l = 0; l < weights->num_layers; ++l) {
+    const int64_t n = static_cast<int64_t>(weights->dims[l]) * weights->dims[l + 1];
+    if (!weights->w_self[l] || !weights->w_neigh[l] || !weights->bias[l]) return fail(GMB_EINVAL, "layer %d weight is NULL", l);
+    a.w[a.count] = static_cast<float*>(const_cast<void*>(weights->w_self[l]));
+    a.g[a.count] = grads->d_self[l];
+    a.n[a.count++] = n;
+    a.w[a.count] = static_cast<float*>(const_cast<void*>(weights->w_neigh[l]));
+    a.g[a.count] = grads->d_neigh[l];
+    a.n[a.count++] = n;
+    a.w[a.count] = const_cast<float*>(weights->bias[l]);
+    a.g[a.count] = grads->d_bias[l];
+    a.n[a.count++] = weights->dims[l + 1];
+  }
+  hipError_t e = gmb::launch_sgd(a, lr, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "update launch");
   return ok();
 }
 

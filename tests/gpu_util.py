@@ -69,3 +69,63 @@ def tensor_bits(t: torch.Tensor) -> np.ndarray:
 
 def tensor_f64(t: torch.Tensor) -> np.ndarray:
     return t.float().cpu().numpy().astype(np.float64)
+
+
+# ---------------------------------------------------------------- training
+
+TOL_LOSS = 1e-5
+TOL_GRAD = 1e-4
+
+
+def max_rel(got, ref):
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    return float(np.abs(np.asarray(got, dtype=np.float64) - ref).max() / max(np.abs(ref).max(), 1e-30))
+
+
+def run_train_step(csr, seeds, fanouts, key, ft, wt, labels, lr):
+    """Sample, gather, forward, loss + backward and one SGD step through the
+    binding (the weights in wt are updated in place)."""
+    blocks, host = gpu_blocks(csr, seeds, fanouts, key)
+    x = gmb.gather_features(blocks, ft)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+    logits, hidden = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd, return_hidden=True)
+    y = torch.from_numpy(np.ascontiguousarray(labels, dtype=np.int32)).cuda()
+    grads, loss = gmb.sage_backward(blocks, x, wt, logits, y, ws_fwd)
+    before = [[t.clone() for t in arrs] for arrs in (wt.w_self, wt.w_neigh, wt.bias)]
+    gmb.sgd_update(wt, grads, lr)
+    torch.cuda.synchronize()
+    return dict(blocks=blocks, host=host, x=x, ws_fwd=ws_fwd, y=y, logits=logits, hidden=hidden,
+                grads=grads, loss=float(loss.item()), before=before)
+
+
+def compare_train_step(orc, out, ref_blocks, X, w, labels, lr, wt, exact_hidden):
+    """The loss, every gradient and the SGD result of run_train_step against
+    the oracle's fp64 step on the same blocks and inputs (w: the weights
+    before the step)."""
+    ws, wn, bs = w.as_f64()
+    loss, logits, (dWs, dWn, dbs), (nws, nwn, nbs) = orc.sage_train_step(ref_blocks, X, ws, wn, bs, labels, lr)
+    if exact_hidden:
+        _, ref_hidden, _ = orc.sage_forward_train(ref_blocks, X, ws, wn, bs)
+        for l, (h, r) in enumerate(zip(out["hidden"], ref_hidden[:-1])):
+            assert np.array_equal(h.cpu().numpy(), r.astype(np.float32)), f"hidden layer {l} not exact"
+    assert abs(out["loss"] - loss) <= TOL_LOSS * max(1.0, abs(loss)), (out["loss"], loss)
+    g = out["grads"]
+    errs = {}
+    for l in range(len(ws)):
+        for name, got, want in (("W_self", g.d_self[l], dWs[l]), ("W_neigh", g.d_neigh[l], dWn[l]),
+                                ("b", g.d_bias[l], dbs[l])):
+            errs[f"{name}{l}"] = max_rel(got.cpu().numpy(), want)
+    print(f"loss {out['loss']:.7g} (oracle {loss:.7g}); gradient errors {errs}", flush=True)
+    assert all(e <= TOL_GRAD for e in errs.values()), errs
+    # the update: W - lr dW, each array within lr * its gradient error bound
+    # plus one fp32 rounding of the result
+    for arrs, news, olds, grads_ in ((wt.w_self, nws, out["before"][0], dWs), (wt.w_neigh, nwn, out["before"][1], dWn),
+                                     (wt.bias, nbs, out["before"][2], dbs)):
+        for l, (a, want, old, gr) in enumerate(zip(arrs, news, olds, grads_)):
+            got = a.cpu().numpy().astype(np.float64)
+            bound = lr * TOL_GRAD * max(np.abs(gr).max(), 1e-30) + 2.0 ** -23 * np.abs(want).max()
+            assert np.abs(got - want).max() <= bound, (l, np.abs(got - want).max(), bound)
+            assert not torch.equal(a, old) or np.abs(gr).max() == 0.0
+    return errs

@@ -6,8 +6,11 @@ The 1M-node R-MAT graph (fp32 x100, fan-outs 15/10/5, batch 1000), the
 through the C ABI exactly as bench.py runs them (caller-owned workspaces,
 reused across batches).  Whole batches are compared with the oracle:
 sampling, relabel and gather bit for bit, the forward within 1e-4 (fp32) or
-2e-2 (bf16) row-wise relative error on every layer.
+2e-2 (bf16) row-wise relative error on every layer, and on the fp32
+workloads one whole training step (loss, every gradient, the SGD update).
 """
+import types
+
 import numpy as np
 import pytest
 import torch
@@ -19,8 +22,8 @@ if not torch.cuda.is_available():
 
 import paper_2010_05337_amd as gmb  # noqa: E402
 from datagen.configs import make_workload  # noqa: E402
-from gpu_util import (assert_blocks_equal, rowwise_rel_err, tensor_bits, tensor_f64,  # noqa: E402
-                      to_torch_feats, to_torch_weights)
+from gpu_util import (assert_blocks_equal, compare_train_step, rowwise_rel_err, tensor_bits,  # noqa: E402
+                      tensor_f64, to_torch_feats, to_torch_weights)
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
@@ -152,3 +155,57 @@ def test_streams_reproduce_one_stream(setup):
             assert torch.equal(lg, logits1), f"batch {b} logits"
     for ln in lanes:
         ln.csr.check_status()
+
+
+def margin_biases(orc, ref, X, w):
+    """Hidden-layer biases that keep every pre-activation of this batch away
+    from zero by at least half of its column's largest magnitude (column c
+    positive for even c, negative for odd c): the forward's fp32 error (at
+    most 1e-4 of a row's largest value) then cannot move any value across
+    the ReLU, and the fp32 and fp64 masks agree.  Checked from the oracle's
+    values."""
+    ws, wn, _ = w.as_f64()
+    bias = [b.copy() for b in w.bias]
+    H = X
+    for l, blk in enumerate(ref[:-1]):
+        m = orc.mean_aggregate(blk, H)
+        z = H[:blk.n_dst] @ ws[l] + m @ wn[l]
+        spread = np.abs(z).max(axis=0, initial=0.0)
+        sign = np.where(np.arange(z.shape[1]) % 2 == 0, 1.0, -1.0)
+        bias[l] = (sign * (1.5 * spread + 0.5)).astype(np.float32)
+        pre = z + bias[l].astype(np.float64)
+        assert np.abs(pre).min(initial=1.0) > 1e-3 * np.abs(pre).max(initial=0.0), l
+        H = np.maximum(pre, 0.0)
+    return bias
+
+
+def test_full_size_training_step(orc, dg, setup):
+    """Batch 0 of the epoch: sample, gather, forward, loss, backward and one
+    SGD step on the device, in the buffers bench.py's training mode uses,
+    against the oracle's fp64 step."""
+    wl, csr, feats, _, _, _ = setup
+    cfg, g = wl.cfg, wl.graph
+    if cfg.feat_dtype != "f32":
+        pytest.skip("the training step is fp32 only")
+    seeds = wl.batches[0]
+    ref = orc.sample_blocks(g.indptr, g.indices, seeds, list(cfg.fanouts), wl.batch_key(0))
+    X = orc.gather(wl.feats, ref[0].src).astype(np.float64)
+    w = types.SimpleNamespace(**vars(wl.weights))
+    w.bias = margin_biases(orc, ref, X, wl.weights)
+    w.as_f64 = lambda: ([a.astype(np.float64) for a in w.w_self], [a.astype(np.float64) for a in w.w_neigh],
+                        [b.astype(np.float64) for b in w.bias])
+    wt = to_torch_weights(w)
+    lane = Lane(csr, wl, feats, wt)
+    print(f"{cfg.name}: training step on batch 0, {len(seeds)} seeds", flush=True)
+    blocks, x, logits, hidden = lane.run(wl, feats, wt, 0)
+    assert_blocks_equal(host_blocks(blocks), ref, f"{cfg.name} batch 0")
+    labels = dg.labels(g.num_nodes, cfg.dims[-1], 7)[seeds]
+    y = torch.from_numpy(labels).cuda()
+    grads, loss = gmb.sage_backward(blocks, x, wt, logits, y, lane.ws_fwd)
+    before = [[t.clone() for t in arrs] for arrs in (wt.w_self, wt.w_neigh, wt.bias)]
+    lr = 0.1
+    gmb.sgd_update(wt, grads, lr)
+    torch.cuda.synchronize()
+    out = dict(hidden=hidden, grads=grads, loss=float(loss.item()), before=before)
+    compare_train_step(orc, out, ref, X, w, labels, lr, wt, exact_hidden=False)
+    csr.check_status()

@@ -1,0 +1,186 @@
+"""GPU parity of the training step (softmax cross-entropy, the backward
+through the GraphSAGE-mean layers, SGD) against the oracle's fp64 step.
+
+The ReLU mask is a decision taken on floating-point values, and an fp32
+pre-activation within rounding of zero can fall on the other side of it than
+the fp64 one.  These cases remove the ambiguity by making the forward exact
+in fp32: integer features, weights and biases that are multiples of 1/16,
+fan-outs that are powers of two with every in-degree 0 or >= the largest
+fan-out (so every neighbour count is a power of two and every mean is
+exact), and sizes for which every partial sum of a hidden layer stays below
+2^24 times its granularity (asserted from the oracle's values).  The hidden
+activations then agree bit for bit and so do the masks; the gradients differ
+only by the rounding of the fp32 backward.
+
+Tolerances: the loss within 1e-5 relative; every gradient array within 1e-4
+of its largest magnitude (fp32 sums of at most a few thousand terms, split
+into partial sums; the layer-input gradients also pass through fp32 atomic
+adds); the SGD result within lr * that error plus one fp32 rounding.
+"""
+import types
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU on this machine", allow_module_level=True)
+
+import paper_2010_05337_amd as gmb  # noqa: E402
+from gpu_util import (assert_blocks_equal, compare_train_step, csr_on_device, gpu_blocks, max_rel,  # noqa: E402
+                      run_train_step, to_torch_weights)
+
+from gpu_util import TOL_GRAD  # noqa: E402
+
+
+def exact_graph(n, seed, min_deg=8, spread=9):
+    """In-degree 0 for every 7th vertex, else min_deg .. min_deg+spread-1
+    distinct sources (no self-loops)."""
+    rng = np.random.default_rng(seed)
+    deg = np.where(np.arange(n) % 7 == 0, 0, min_deg + rng.integers(0, spread, n))
+    indptr = np.zeros(n + 1, dtype=np.int64)
+    indptr[1:] = np.cumsum(deg)
+    rows = []
+    for v, d in enumerate(deg):
+        u = rng.choice(n - 1, int(d), replace=False)
+        u[u >= v] += 1
+        rows.append(np.sort(u))
+    indices = np.concatenate(rows).astype(np.int32) if rows else np.zeros(0, np.int32)
+    return types.SimpleNamespace(num_nodes=n, indptr=indptr, indices=indices)
+
+
+def exact_model(dg, n, dims, seed):
+    rng = np.random.default_rng(seed)
+    feats = rng.integers(-2, 3, (n, dims[0])).astype(np.float32)
+    ws, wn, bs = [], [], []
+    for l in range(len(dims) - 1):
+        ws.append((rng.integers(-2, 3, (dims[l], dims[l + 1])) / 16).astype(np.float32))
+        wn.append((rng.integers(-2, 3, (dims[l], dims[l + 1])) / 16).astype(np.float32))
+        bs.append((rng.integers(-2, 3, dims[l + 1]) / 16).astype(np.float32))
+    return feats, dg.Weights(list(dims), ws, wn, bs, "f32")
+
+
+def assert_hidden_exact(orc, ref_blocks, X, w):
+    """Every partial sum of every hidden layer is a multiple of the layer's
+    granularity below 2^24 times it, so fp32 computes it exactly in any
+    order."""
+    ws, wn, bs = w.as_f64()
+    H, gran = X, 1.0
+    for l, blk in enumerate(ref_blocks[:-1]):
+        # the sums of up to 8 neighbour rows behind the mean
+        assert np.abs(H).max(initial=0.0) * 8 < 2.0 ** 24 * gran, (l, np.abs(H).max())
+        m = orc.mean_aggregate(blk, H)
+        gran = gran / 8 / 16
+        bound = np.abs(H[:blk.n_dst]) @ np.abs(ws[l]) + np.abs(m) @ np.abs(wn[l]) + np.abs(bs[l])
+        assert bound.max(initial=0.0) < 2.0 ** 24 * gran, (l, bound.max(), gran)
+        H = np.maximum(H[:blk.n_dst] @ ws[l] + m @ wn[l] + bs[l], 0.0)
+
+
+CASES = [
+    # dims, fan-outs, seeds
+    ([16, 32, 8], [4, 2], 64),
+    ([10, 12, 7], [8, 4], 37),             # ragged input width, 7 classes (padded dZ rows)
+    ([24, 64, 640, 10], [2, 4, 8], 50),    # 640-wide hidden layer, three layers
+    ([100, 256, 256, 47], [8, 4, 2], 200), # the benchmark model's widths
+    ([12, 5], [4], 33),                    # one layer: no ReLU, no input gradient
+    ([8, 16, 4], [2, 2], 1),               # one seed
+]
+
+
+@pytest.mark.parametrize("dims,fanouts,n_seeds", CASES)
+def test_train_step_matches_the_oracle(orc, dg, dims, fanouts, n_seeds):
+    n = 3000
+    g = exact_graph(n, 11 + len(dims))
+    feats, w = exact_model(dg, n, dims, 12 + dims[1])
+    seeds = dg.permutation(n, 13)[:n_seeds]
+    labels = dg.labels(n, dims[-1], 14)[seeds]
+    key, lr = 15, 0.25
+    print(f"dims {dims} fan-outs {fanouts} seeds {n_seeds}", flush=True)
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    ft = torch.from_numpy(feats).cuda()
+    out = run_train_step(csr, seeds, fanouts, key, ft, wt, labels, lr)
+    ref_blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, key)
+    assert_blocks_equal(out["host"], ref_blocks)
+    X = orc.gather(feats, ref_blocks[0].src).astype(np.float64)
+    assert_hidden_exact(orc, ref_blocks, X, w)
+    compare_train_step(orc, out, ref_blocks, X, w, labels, lr, wt, exact_hidden=True)
+    csr.check_status()
+
+
+def test_repeated_backward(orc, dg):
+    """The last layer's gradients are summed in a fixed order: identical bits
+    on every run; the layers below take the fp32 atomic adds of the mean's
+    backward and agree within the tolerance."""
+    n, dims, fanouts = 3000, [16, 32, 32, 6], [4, 4, 8]
+    g = exact_graph(n, 21)
+    feats, w = exact_model(dg, n, dims, 22)
+    seeds = dg.permutation(n, 23)[:120]
+    labels = torch.from_numpy(dg.labels(n, dims[-1], 24)[seeds]).cuda()
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    ft = torch.from_numpy(feats).cuda()
+    blocks, _ = gpu_blocks(csr, seeds, fanouts, 25)
+    x = gmb.gather_features(blocks, ft)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+    logits = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd)
+    g1, l1 = gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd)
+    first = [[t.clone() for t in a] for a in (g1.d_self, g1.d_neigh, g1.d_bias)]
+    g2, l2 = gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd)
+    assert torch.equal(l1, l2)
+    L = len(dims) - 1
+    for a, b in zip(first, (g2.d_self, g2.d_neigh, g2.d_bias)):
+        assert torch.equal(a[L - 1], b[L - 1])
+        for l in range(L - 1):
+            assert max_rel(b[l].cpu().numpy(), a[l].cpu().numpy().astype(np.float64)) <= TOL_GRAD
+
+
+def test_sgd_steps_lower_the_loss(dg):
+    """Five GPU training steps on one batch of Gaussian data: the loss goes
+    down at every step."""
+    n, dims, fanouts = 10000, [32, 64, 64, 10], [5, 10, 15]
+    g = dg.er_directed(n, 12.0, 31)
+    feats = dg.features(n, dims[0], 32, "f32")
+    w = dg.sage_weights(dims, 33)
+    seeds = dg.permutation(n, 34)[:256]
+    labels = torch.from_numpy(dg.labels(n, dims[-1], 35)[seeds]).cuda()
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    ft = torch.from_numpy(feats).cuda()
+    blocks, _ = gpu_blocks(csr, seeds, fanouts, 36)
+    x = gmb.gather_features(blocks, ft)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+    losses = []
+    for _ in range(6):
+        logits = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd)
+        grads, loss = gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd)
+        gmb.sgd_update(wt, grads, 0.5)
+        losses.append(float(loss.item()))
+    print("losses", losses, flush=True)
+    assert all(b < a for a, b in zip(losses, losses[1:])), losses
+
+
+def test_backward_rejects_unsupported_models(dg):
+    """bf16 weights and hidden widths that are not a multiple of 4 are
+    refused before any launch."""
+    n = 2000
+    g = dg.er_directed(n, 8.0, 41)
+    csr = csr_on_device(g)
+    seeds = dg.permutation(n, 42)[:16]
+    blocks, _ = gpu_blocks(csr, seeds, [3, 3], 43)
+    labels = torch.zeros(16, dtype=torch.int32, device="cuda")
+    for dims, dtype in (([8, 6, 4], "f32"), ([8, 8, 4], "bf16")):
+        w = dg.sage_weights(dims, 44, dtype)
+        wt = to_torch_weights(w)
+        ft = torch.from_numpy(dg.features(n, dims[0], 45, dtype).view(np.int16) if dtype == "bf16"
+                              else dg.features(n, dims[0], 45, dtype)).cuda()
+        if dtype == "bf16":
+            ft = ft.view(torch.bfloat16)
+        x = gmb.gather_features(blocks, ft)
+        ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+        logits = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd)
+        assert gmb.backward_workspace_bytes(blocks, wt) == 0
+        with pytest.raises(gmb.GmbError):
+            gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd)
