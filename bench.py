@@ -10,6 +10,12 @@ workload: the 2.4M-node power-law graph (shape of Table I's product graph),
 fp32 features of dim 100, model 100-256-256-47, fan-outs 15/10/5, batch 1000,
 one epoch over a random 8% training set (196 batches).
 
+--mode train times the whole training iteration instead: the same
+sampling and gather, run ahead on loader streams, then forward, softmax
+cross-entropy, backward and SGD on one compute stream (the overlap of
+sampling with training of Section III-D), with per-stage event times of a
+one-stream pass and the oracle's training iteration as CPU baseline.
+
 Prints one JSON line.  value = seeds/s over the timed steps; sampled edges/s
 and gather GB/s ride along; `roofline` covers the dominant kernel, measured
 with HIP events on the stream the kernels run on; `cpu_baseline` times the
@@ -52,6 +58,10 @@ def parse():
     ap.add_argument("--streams", type=int, default=4,
                     help="mini-batches in flight: batch i runs on stream i %% streams, each stream "
                          "with its own sampler state and workspaces")
+    ap.add_argument("--mode", choices=("infer", "train"), default="infer",
+                    help="infer: sample + gather + forward (the default); train: the whole "
+                         "training iteration, + loss, backward and SGD (fp32 workloads)")
+    ap.add_argument("--lr", type=float, default=0.01, help="SGD step size of --mode train")
     return ap.parse_args()
 
 
@@ -275,6 +285,12 @@ def main():
     fanouts = list(cfg.fanouts)
     batches = [torch.from_numpy(b).to(dev) for b in wl.batches]
     nb = len(batches)
+    if args.mode == "train":
+        if bf16:
+            print("--mode train runs fp32 workloads only", file=sys.stderr)
+            sys.exit(2)
+        run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen)
+        return
 
     # one set of buffers per stream, sized for a full batch and reused by
     # every step that runs on that stream
@@ -449,6 +465,184 @@ def main():
         res["cpu_baseline"], res["parity"] = cpu_baseline(args, wl, csr, batches, fanouts, feats,
                                                           weights, ws_sample, x_buf, ws_fwd)
     print(json.dumps(res), flush=True)
+
+
+def backward_flops(sizes, dims) -> int:
+    """The products of the backward: per layer [H | M]^T dZ, and for layers
+    >= 1 also dZ [W_self; W_neigh]^T."""
+    total = 0
+    for l, (n_dst, _, _) in enumerate(sizes):
+        total += 2 * n_dst * 2 * dims[l] * dims[l + 1]
+        if l > 0:
+            total += 2 * n_dst * 2 * dims[l] * dims[l + 1]
+    return total
+
+
+def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
+    """Training iterations: sample + gather of batch i on loader stream
+    i % S (its own sampler state and buffers), then forward, loss, backward
+    and SGD on one compute stream (each step needs the weights the previous
+    one left).  Events order the two: the compute stream waits for the
+    batch's gather, a loader stream waits until the compute stream is done
+    with the buffers it is about to reuse."""
+    import torch
+    import paper_2010_05337_amd as gmb
+    from datagen import labels as vertex_labels
+    cfg, g = wl.cfg, wl.graph
+    dev = feats.device
+    fanouts = list(cfg.fanouts)
+    nb = len(batches)
+    C = cfg.dims[-1]
+    lab_all = vertex_labels(g.num_nodes, C, cfg.seeds[2] + 1)
+    labels = [torch.from_numpy(lab_all[b]).to(dev) for b in wl.batches]
+    S = max(1, args.streams)
+    comp = torch.cuda.current_stream()
+    lanes = []
+    for k in range(S):
+        c = csr if k == 0 else gmb.CSRGraph(ip, ix)
+        ws_s = gmb._aligned_bytes(gmb.sample_workspace_bytes(cfg.batch, fanouts, g.num_nodes), dev)[1]
+        probe = gmb.sample_blocks(c, batches[0], fanouts, wl.batch_key(0), workspace=ws_s)
+        lanes.append(dict(csr=c, ws_sample=ws_s, stream=torch.cuda.Stream(),
+                          x=torch.empty((probe.input_capacity, cfg.feat_dim), dtype=feats.dtype, device=dev),
+                          ready=torch.cuda.Event(), done=torch.cuda.Event()))
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1]
+    ws_bwd = gmb._aligned_bytes(gmb.backward_workspace_bytes(probe, weights), dev)[1]
+    logits = torch.empty((cfg.batch, C), dtype=torch.float32, device=dev)
+    grads = gmb.SageGrads(weights)
+    K, W = args.steps, args.warmup
+    losses = torch.zeros(W + 2 * K, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    def model(blocks, x, b, i):
+        lg = gmb.sage_forward(blocks, x, weights, workspace=ws_fwd, logits=logits[:batches[b].numel()])
+        gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
+                          workspace=ws_bwd)
+        gmb.sgd_update(weights, grads, args.lr)
+
+    def step(i):
+        b = i % nb
+        ln = lanes[i % S]
+        st = ln["stream"]
+        with torch.cuda.stream(st):
+            st.wait_event(ln["done"])
+            blocks = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b), workspace=ln["ws_sample"])
+            x = gmb.gather_features(blocks, feats, out=ln["x"])
+            ln["ready"].record(st)
+        comp.wait_event(ln["ready"])
+        model(blocks, x, b, i)
+        ln["done"].record(comp)
+
+    for i in range(W):
+        step(i)
+    torch.cuda.synchronize()
+    # pass A (the figure): K iterations, loaders S batches ahead
+    t0 = time.perf_counter()
+    for i in range(W, W + K):
+        step(i)
+    torch.cuda.synchronize()
+    T = time.perf_counter() - t0
+    for ln in lanes:
+        ln["csr"].check_status()
+    # pass B: the same iterations on the compute stream alone, events
+    # around every stage
+    names = ("sample", "gather", "forward", "backward", "sgd")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(K)]
+    ln0 = lanes[0]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for j in range(K):
+        i = W + K + j
+        b = i % nb
+        e = evs[j]
+        e[0].record(comp)
+        blocks = gmb.sample_blocks(ln0["csr"], batches[b], fanouts, wl.batch_key(b), workspace=ln0["ws_sample"])
+        e[1].record(comp)
+        x = gmb.gather_features(blocks, feats, out=ln0["x"])
+        e[2].record(comp)
+        lg = gmb.sage_forward(blocks, x, weights, workspace=ws_fwd, logits=logits[:batches[b].numel()])
+        e[3].record(comp)
+        gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
+                          workspace=ws_bwd)
+        e[4].record(comp)
+        gmb.sgd_update(weights, grads, args.lr)
+        e[5].record(comp)
+    torch.cuda.synchronize()
+    T1 = time.perf_counter() - t1
+    csr.check_status()
+    stage = {n: sum(e[k].elapsed_time(e[k + 1]) for e in evs) for k, n in enumerate(names)}
+    loss_h = losses.cpu().numpy()
+    if not np.isfinite(loss_h).all():
+        raise RuntimeError("non-finite loss in the training run")
+
+    seeds_total = edges_total = 0
+    b_gather = fwd_flops = bwd_flops = 0
+    for j in range(K):
+        b = (W + j) % nb
+        blocks = gmb.sample_blocks(csr, batches[b], fanouts, wl.batch_key(b), workspace=lanes[0]["ws_sample"])
+        sizes = blocks.sizes()
+        seeds_total += batches[b].numel()
+        edges_total += sum(s[2] for s in sizes)
+        b_gather += alg_gather_bytes(sizes[0][1], cfg.feat_dim, 4)
+        fwd_flops += linear_flops(sizes, cfg.dims)
+        bwd_flops += backward_flops(sizes, cfg.dims)
+    tf, tb = stage["forward"] / 1e3, stage["backward"] / 1e3
+    res = {
+        "metric": "seeds/s of the training iteration (sample+gather+SAGE fwd+loss+bwd+SGD)",
+        "value": seeds_total / T,
+        "unit": "seeds/s",
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": 1e3 * T / K,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {cfg.num_nodes}-node graph, {g.num_edges} edges, feats f32 "
+                               f"x{cfg.feat_dim}, SAGE {'-'.join(map(str, cfg.dims))}, fanouts {fanouts}, batch "
+                               f"{cfg.batch}, {nb} batches per epoch, SGD lr {args.lr}",
+                   "batch": cfg.batch, "fanouts": fanouts, "dims": list(cfg.dims), "batches_per_epoch": nb,
+                   "mode": "train"},
+        "epoch_s": nb * T / K,
+        "sampled_edges_per_s": edges_total / T,
+        "loader_streams": S,
+        "single_stream": {"seeds_per_s": seeds_total / T1, "ms_per_step": 1e3 * T1 / K,
+                          "stage_ms_per_step": {k: v / K for k, v in stage.items()}},
+        "forward_linear_TFLOPs_lower_bound": fwd_flops / tf / 1e12,
+        "backward_products_TFLOPs_lower_bound": bwd_flops / tb / 1e12,
+        "mfma_peak_TFLOPs": FP32_MFMA_PEAK_TFLOPS,
+        "gather_GBps": b_gather / (stage["gather"] / 1e3) / 1e9,
+        "loss": {"first": float(loss_h[0]), "last_of_pass_A": float(loss_h[W + K - 1]),
+                 "last": float(loss_h[-1])},
+        "datagen_s": t_gen,
+    }
+    # the gather is the one kernel of the iteration bracketed alone by events
+    res["roofline"] = {"kernel": "k_gather", "bound": "hbm", "achieved": res["gather_GBps"],
+                       "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": res["gather_GBps"] / HBM_PEAK_GBPS,
+                       "traffic": None, "alg_bytes_per_launch": b_gather / K,
+                       "avg_launch_ms": stage["gather"] / K}
+    if args.cpu_batches > 0:
+        res["cpu_baseline"] = cpu_baseline_train(args, wl, fanouts)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline_train(args, wl, fanouts):
+    """The oracle's training iteration (plain C, fp64, one thread) on the
+    first batches of the epoch, timed end to end."""
+    import oracle
+    from datagen import labels as vertex_labels
+    g, w, cfg = wl.graph, wl.weights, wl.cfg
+    ws, wn, bs = w.as_f64()
+    lab_all = vertex_labels(g.num_nodes, cfg.dims[-1], cfg.seeds[2] + 1)
+    n = min(args.cpu_batches, len(wl.batches))
+    seeds_done, t = 0, 0.0
+    for b in range(n):
+        seeds_np = wl.batches[b]
+        t0 = time.perf_counter()
+        ref = oracle.sample_blocks(g.indptr, g.indices, seeds_np, fanouts, wl.batch_key(b))
+        X = oracle.gather(wl.feats, ref[0].src).astype(np.float64)
+        _, _, _, (ws, wn, bs) = oracle.sage_train_step(ref, X, ws, wn, bs, lab_all[seeds_np], args.lr)
+        t += time.perf_counter() - t0
+        seeds_done += len(seeds_np)
+    return {"value": seeds_done / t, "unit": "seeds/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} of {len(wl.batches)} batches of the epoch ({seeds_done} seeds), "
+                      f"sample+gather+forward+loss+backward+SGD in fp64 plain C, {t:.1f} s"}
 
 
 def cpu_baseline(args, wl, csr, batches, fanouts, feats, weights, ws_sample, x_buf, ws_fwd):
