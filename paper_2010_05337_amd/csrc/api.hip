@@ -434,7 +434,9 @@ namespace {
 
 struct BackwardPlan {
   int ldz[GMB_MAX_LAYERS];   // row stride of dZ of layer l (floats, multiple of 4)
-  size_t off_a, off_b, off_dm, off_part, off_partdb, off_lossrows;
+  size_t off_a, off_b, off_dm, off_part, off_lossrows;
+  size_t off_cnt, off_off, off_pos, off_csc;   // the transpose of a block
+  int64_t cnt_len;                             // ints of the edge counters
   size_t total;
 };
 
@@ -449,7 +451,7 @@ int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* 
   for (int l = 1; l < L; ++l)
     if (w->dims[l + 1] > 640) return fail(GMB_EINVAL, "dims[%d]=%d above 640 (input-gradient kernel)", l + 1, w->dims[l + 1]);
   BackwardPlan p{};
-  size_t buf = 0, dm = 0, part = 0, partdb = 0;
+  size_t buf = 0, dm = 0, part = 0, src = 1, nnz = 1;
   for (int l = 0; l < L; ++l) {
     const int d_in = w->dims[l], d_out = w->dims[l + 1];
     const gmb_block& k = b->blk[l];
@@ -458,10 +460,11 @@ int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* 
     if (l > 0) {
       buf = std::max(buf, static_cast<size_t>(std::max<int64_t>(k.cap_src, 1)) * d_in);
       dm = std::max(dm, static_cast<size_t>(std::max<int64_t>(k.cap_dst, 1)) * d_in);
+      src = std::max(src, static_cast<size_t>(k.cap_src));
+      nnz = std::max(nnz, static_cast<size_t>(k.cap_nnz));
     }
     const size_t parts = gmb::wgrad_parts(std::max<int64_t>(k.cap_dst, 1), d_in, d_out);
-    part = std::max(part, parts * gmb::wgrad_k2p(d_in) * d_out);
-    partdb = std::max(partdb, parts * d_out);
+    part = std::max(part, parts * (2 * static_cast<size_t>(d_in) + 1) * gmb::wgrad_ldp(d_out));
   }
   size_t off = 0;
   p.off_a = off;
@@ -472,10 +475,17 @@ int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* 
   off = align_up(off + 4 * std::max<size_t>(dm, 1));
   p.off_part = off;
   off = align_up(off + 4 * part);
-  p.off_partdb = off;
-  off = align_up(off + 4 * partdb);
   p.off_lossrows = off;
   off = align_up(off + 4 * static_cast<size_t>(std::max(b->num_seeds, 1)));
+  p.cnt_len = static_cast<int64_t>(src);
+  p.off_cnt = off;
+  off = align_up(off + 4 * src);
+  p.off_off = off;
+  off = align_up(off + 4 * (src + 1));
+  p.off_pos = off;
+  off = align_up(off + 4 * src);
+  p.off_csc = off;
+  off = align_up(off + 8 * nnz);
   p.total = off;
   *plan = p;
   return GMB_OK;
@@ -524,9 +534,12 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
   float* other = reinterpret_cast<float*>(base + p.off_b);
   float* dM = reinterpret_cast<float*>(base + p.off_dm);
   float* part = reinterpret_cast<float*>(base + p.off_part);
-  float* partdb = reinterpret_cast<float*>(base + p.off_partdb);
+  int32_t* cnt = reinterpret_cast<int32_t*>(base + p.off_cnt);
+  int32_t* offs = reinterpret_cast<int32_t*>(base + p.off_off);
+  int32_t* pos = reinterpret_cast<int32_t*>(base + p.off_pos);
+  int2* csc = reinterpret_cast<int2*>(base + p.off_csc);
   hipError_t e = gmb::launch_xent(logits, labels, blocks->num_seeds, weights->dims[L], p.ldz[L - 1], cur,
-                                  reinterpret_cast<float*>(base + p.off_lossrows), loss, s);
+                                  reinterpret_cast<float*>(base + p.off_lossrows), loss, cnt, p.cnt_len, s);
   if (e != hipSuccess) return hip_fail(e, "loss launch");
   for (int l = L - 1; l >= 0; --l) {
     const gmb_block& bk = blocks->blk[l];
@@ -535,17 +548,20 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
                                : reinterpret_cast<const float*>(fbase + fp.off_hidden[l - 1]);
     const float* m = reinterpret_cast<const float*>(fbase + fp.off_agg[l]);
     e = gmb::launch_wgrad(bk.sizes, h_in, m, d_in, cur, p.ldz[l], d_out, std::max<int64_t>(bk.cap_dst, 1), part,
-                          partdb, grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], s);
+                          grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], s);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
     if (l == 0) break;
+    // dZ [W_self; W_neigh]^T: dH_self into `other`, dM; the block's
+    // in-edge counts per source on the way
     e = gmb::launch_dgrad(bk.sizes, cur, p.ldz[l], d_out, static_cast<const float*>(weights->w_self[l]),
-                          static_cast<const float*>(weights->w_neigh[l]), d_in, other, dM, bk.cap_dst, s);
+                          static_cast<const float*>(weights->w_neigh[l]), d_in, other, dM, bk.cap_dst, bk.indptr,
+                          bk.indices, bk.cap_nnz, cnt, s);
     if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
-    e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, dM, d_in, other, bk.cap_dst, bk.cap_src, s);
+    // the mean's backward through the block's transpose, the ReLU of the
+    // layer below on the way out: `other` becomes that layer's dZ
+    e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, bk.cap_nnz, dM, h_in, d_in, other, bk.cap_dst,
+                                  bk.cap_src, cnt, offs, pos, csc, s);
     if (e != hipSuccess) return hip_fail(e, "mean-backward launch");
-    const gmb_block& below = blocks->blk[l - 1];
-    e = gmb::launch_relu_mask(below.sizes, h_in, d_in, other, below.cap_dst, s);
-    if (e != hipSuccess) return hip_fail(e, "activation-backward launch");
     std::swap(cur, other);
   }
   return ok();

@@ -126,18 +126,19 @@ struct SgdArgs {
   int64_t n[3 * GMB_MAX_LAYERS];
 };
 hipError_t launch_xent(const float* logits, const int32_t* labels, int n, int C, int ldz, float* dz,
-                       float* loss_rows, float* loss, hipStream_t s);
+                       float* loss_rows, float* loss, int32_t* clear, int64_t clear_n, hipStream_t s);
+int wgrad_ldp(int d_out);
 int wgrad_parts(int64_t cap_rows, int d_in, int d_out);
-int wgrad_k2p(int d_in);
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
-                        int d_out, int64_t cap_rows, float* partial, float* partial_db, float* d_self,
-                        float* d_neigh, float* d_bias, hipStream_t s);
+                        int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
+                        float* d_bias, hipStream_t s);
 hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_out, const float* ws,
-                        const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows, hipStream_t s);
-hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local, const float* dM,
-                                int d, float* dH, int64_t cap_dst, int64_t cap_src, hipStream_t s);
-hipError_t launch_relu_mask(const int32_t* sizes, const float* out, int d, float* dH, int64_t cap_rows,
-                            hipStream_t s);
+                        const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
+                        const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t* cnt, hipStream_t s);
+hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
+                                int64_t cap_nnz, const float* dM, const float* out, int d, float* dH,
+                                int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
+                                int2* csc, hipStream_t s);
 hipError_t launch_sgd(const SgdArgs& a, float lr, hipStream_t s);
 
 }  // namespace gmb

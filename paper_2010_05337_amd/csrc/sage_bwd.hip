@@ -3,25 +3,33 @@
 // trainer's iteration of Section III-E), and the SGD update.  fp32.
 //
 //   k_xent         softmax cross-entropy per target row (one wave per row):
-//                  dZ = (softmax(z) - e_y) / B, and the row's loss term
+//                  dZ = (softmax(z) - e_y) / B, and the row's loss term; also
+//                  clears the per-source edge counters of the transposes
 //   k_loss_sum     the mean loss, one workgroup, fixed order
 //   k_wgrad        [dW_self; dW_neigh] = [H | M]^T dZ and db = sum of dZ rows:
 //                  v_mfma_f32_16x16x4_f32 with the rows of the block as the
-//                  reduction dimension, split over workgroups (each writes
-//                  its partial sums; no atomics, so the result is the same
-//                  on every run)
+//                  reduction dimension; a workgroup owns a 64 x 64 tile of
+//                  the output and a range of rows, its four waves split the
+//                  rows and are summed through LDS, and every workgroup
+//                  writes its partial sums (no atomics: the same result on
+//                  every run)
 //   k_wgrad_reduce sums the partials in a fixed order into the gradients
 //   k_dgrad        [dH_self | dM] = dZ [W_self; W_neigh]^T: the weights'
 //                  transpose for 64 output columns resident in LDS in MFMA
-//                  operand order, 64-row tiles, persistent over row tiles
-//   k_scatter_mean dH[local[e]] += dM[v] / k_v over the block's edges
-//                  (hardware fp32 atomic adds)
-//   k_relu_mask    dZ of the layer below = dH where its output is > 0
+//                  operand order, 64-row tiles, persistent over row tiles;
+//                  also counts every source's in-edges in the block
+//   k_csc_scan     exclusive scan of the counts: the transpose's row offsets
+//   k_csc_fill     the transpose's entries (v, 1/k_v), one per block edge
+//   k_pull_mean    dH[u] = relu'(below) * (dH_self[u] + sum over the block
+//                  edges (v <- u) of dM[v] / k_v), one pass per source row:
+//                  the mean's backward as a gather over the transpose, with
+//                  the ReLU of the layer below applied on the way out
 //   k_sgd          W -= lr dW over every parameter array
 #include <algorithm>
 
 #include "common.hpp"
 #include "kernels.hpp"
+#include "scan.hpp"
 
 namespace gmb {
 
@@ -31,13 +39,18 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 // ---- loss ---------------------------------------------------------------
 
-// Row v of z [n, C] (row stride ldz): dz row (stride ldz, columns C..ldz-1
+// Row v of z [n, C] (row stride C): dz row (stride ldz, columns C..ldz-1
 // written as 0) and the row's loss term log(sum exp z) - z_y.  A label
 // outside [0, C) is a data error: its row gets the softmax as gradient and
-// no loss term (every access stays in bounds).
+// no loss term (every access stays in bounds).  The grid also clears
+// clear[0 .. clear_n).
 __global__ __launch_bounds__(256) void k_xent(const float* __restrict__ z, const int32_t* __restrict__ y,
                                               int n, int C, int ldz, float* __restrict__ dz,
-                                              float* __restrict__ loss_rows) {
+                                              float* __restrict__ loss_rows, int32_t* __restrict__ clear,
+                                              int64_t clear_n) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < clear_n;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    clear[i] = 0;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n) return;
@@ -78,176 +91,319 @@ __global__ __launch_bounds__(256) void k_loss_sum(const float* __restrict__ rows
 
 // ---- weight gradient ------------------------------------------------------
 
-// Workgroup (p, y, z): rows [p R, (p + 1) R) of the block's destinations,
-// output columns [64 y, 64 y + 64), rows i of [dW_self; dW_neigh] in the
-// i-blocks 16 (4 z + w + 4 t) .. +15 of wave w, t < 4.  Lane l supplies
-// A^T[i][k] = X[k][i] with i = i0 + l%16, k = k0 + l/16 (X = [H | M]) and
-// B[k][o] = dZ[k][o0 + l%16]; the MFMA sums over four rows.  Rows at or past
-// the end read row r0 and are zeroed; the partial of a workgroup with no
-// rows is zero.  Wave 0 of the z = 0 workgroups also sums the dZ rows (db).
-constexpr int kWgradIB = 4;   // i-blocks per wave
+// Workgroup (p, y, z) owns 64 rows of [dW_self; dW_neigh] -- columns
+// [64 z', 64 z' + 64) of H (z < TI = ceil(d_in / 64), z' = z) or of M
+// (z' = z - TI), the output rows d_in + those -- and output columns
+// [64 y, 64 y + 64), over the block rows [p R, (p + 1) R); wave w takes the
+// 16-row steps w, w + 4, ... of that range.  Lane (q, c) = (l / 16, l % 16)
+// owns the four columns 64 z' + 4c + t of its array and o = 64 y + 4c + j of
+// dZ, and reads each as one 16-byte load (VEC; else four scalar loads).
+// MFMA (t, j) multiplies A[m][k] = X[row k][64 z' + 4m + t] by
+// B[k][n] = dZ[row k][64 y + 4n + j] over four rows, so its accumulator
+// register r of lane (q, c) holds the sum for column 64 z' + 16q + 4r + t of
+// X and column 64 y + 4c + j of dZ.  Rows at or past the end of the range
+// read its last row and their dZ is zeroed before the product (the columns
+// past the arrays' ends feed only outputs that are never written).  The
+// four waves' sums meet in LDS in a fixed order; workgroup p writes its
+// partial to partial[p][i][o] (row stride ldp = d_out rounded up to 4; row
+// 2 d_in: the column sums of dZ, written by the z = 0 workgroups).  Every
+// array of this kernel has fewer than 2^32 bytes (checked by the launcher),
+// so loads take a uniform base and a 32-bit byte offset.
+constexpr int kWgradRed = 2 * 64 * 64;   // LDS floats of the cross-wave sum
 
+template <bool VEC>
 __global__ __launch_bounds__(256) void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
                                                const float* __restrict__ M, int d_in,
-                                               const float* __restrict__ dZ, int ldz, int d_out,
-                                               int rows_per_part, int k2p, float* __restrict__ partial,
-                                               float* __restrict__ partial_db) {
+                                               const float* __restrict__ dZ, int ldz, int ldp,
+                                               int rows_per_part, float* __restrict__ partial) {
+  __shared__ float red[kWgradRed];
+  __shared__ float red_db[4][64];
   const int32_t n = load_size(&sizes[kNDst]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, c16 = lane & 15;
   const int p = blockIdx.x;
-  const int o0 = blockIdx.y * 64;
-  const int ib0 = blockIdx.z * 16 + wave;   // i-blocks ib0 + 4 t
   const int K2 = 2 * d_in;
+  const int TI = (d_in + 63) / 64;
+  const bool from_m = static_cast<int>(blockIdx.z) >= TI;
+  const int zc = from_m ? blockIdx.z - TI : blockIdx.z;
+  const char* X = reinterpret_cast<const char*>(from_m ? M : H);   // uniform per workgroup
+  const char* Zb = reinterpret_cast<const char*>(dZ);
+  const int cb = zc * 64 + 4 * c16;           // this lane's first column of X
+  const int ob = blockIdx.y * 64 + 4 * c16;   // this lane's first column of dZ
+  const uint32_t xrow = static_cast<uint32_t>(d_in) * 4u, zrow = static_cast<uint32_t>(ldz) * 4u;
+  const uint32_t ocol = static_cast<uint32_t>(ob < ldz ? ob : 0) * 4u;
+  uint32_t xcol[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) xcol[t] = static_cast<uint32_t>(VEC ? (cb < d_in ? cb : 0) : (cb + t < d_in ? cb + t : 0)) * 4u;
   const int r0 = p * rows_per_part;
   const int r1 = min(r0 + rows_per_part, n);
-  floatx4 acc[kWgradIB][4];
+  floatx4 acc[4][4];
 #pragma unroll
-  for (int t = 0; t < kWgradIB; ++t)
+  for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[t][j] = floatx4{0.f, 0.f, 0.f, 0.f};
   float dbs[4] = {0.f, 0.f, 0.f, 0.f};
-  // per lane: the columns it reads, clamped into the arrays
-  int icol[kWgradIB];
-  bool iok[kWgradIB], from_m[kWgradIB];
-#pragma unroll
-  for (int t = 0; t < kWgradIB; ++t) {
-    const int i = (ib0 + 4 * t) * 16 + c16;
-    iok[t] = i < K2;
-    from_m[t] = i >= d_in;
-    icol[t] = iok[t] ? (from_m[t] ? i - d_in : i) : 0;
-  }
-  int ocol[4];
-  bool ook[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int o = o0 + j * 16 + c16;
-    ook[j] = o < d_out;
-    ocol[j] = ook[j] ? o : 0;
-  }
-  for (int k0 = r0; k0 < r1; k0 += 16) {
-    float a[4][kWgradIB], b[4][4];
+
+  auto load = [&](int k0, float4 (&xa)[4], float4 (&zb)[4]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const int row = k0 + 4 * s + q;
-      const int rc = row < r1 ? row : r0;
-      const float* hr = H + static_cast<int64_t>(rc) * d_in;
-      const float* mr = M + static_cast<int64_t>(rc) * d_in;
-      const float* zr = dZ + static_cast<int64_t>(rc) * ldz;
-#pragma unroll
-      for (int t = 0; t < kWgradIB; ++t) a[s][t] = (from_m[t] ? mr : hr)[icol[t]];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[s][j] = zr[ocol[j]];
+      const uint32_t rc = static_cast<uint32_t>(row < r1 ? row : r1 - 1);
+      if (VEC) {
+        xa[s] = *reinterpret_cast<const float4*>(X + (rc * xrow + xcol[0]));
+      } else {
+        xa[s] = make_float4(*reinterpret_cast<const float*>(X + (rc * xrow + xcol[0])),
+                            *reinterpret_cast<const float*>(X + (rc * xrow + xcol[1])),
+                            *reinterpret_cast<const float*>(X + (rc * xrow + xcol[2])),
+                            *reinterpret_cast<const float*>(X + (rc * xrow + xcol[3])));
+      }
+      zb[s] = *reinterpret_cast<const float4*>(Zb + (rc * zrow + ocol));
     }
+  };
+  auto compute = [&](int k0, const float4 (&xa)[4], const float4 (&zb)[4]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const bool in = k0 + 4 * s + q < r1;
+      const float a[4] = {xa[s].x, xa[s].y, xa[s].z, xa[s].w};
+      const float b[4] = {in ? zb[s].x : 0.f, in ? zb[s].y : 0.f, in ? zb[s].z : 0.f, in ? zb[s].w : 0.f};
 #pragma unroll
-      for (int t = 0; t < kWgradIB; ++t) a[s][t] = (in && iok[t]) ? a[s][t] : 0.f;
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[s][j] = (in && ook[j]) ? b[s][j] : 0.f;
+        for (int j = 0; j < 4; ++j) acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t], b[j], acc[t][j], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dbs[j] += b[j];
     }
+  };
+
+  int k0 = r0 + 16 * wave;
+  if (k0 < r1) {
+    float4 xa[4], zb[4];
+    load(k0, xa, zb);
+    for (;;) {
+      const int kn = k0 + 64;
+      if (kn < r1) {
+        float4 xn[4], zn[4];
+        load(kn, xn, zn);
+        compute(k0, xa, zb);
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int t = 0; t < kWgradIB; ++t)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s][t], b[s][j], acc[t][j], 0, 0, 0);
-    if (wave == 0) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) dbs[j] += b[0][j] + b[1][j] + b[2][j] + b[3][j];
-    }
-  }
-  // partial[p][i][o], i < k2p
-#pragma unroll
-  for (int t = 0; t < kWgradIB; ++t) {
-    const int ib = ib0 + 4 * t;
-    if (ib * 16 >= k2p) continue;   // uniform per wave
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int o = o0 + j * 16 + c16;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = ib * 16 + 4 * q + r;
-        if (o < d_out) partial[(static_cast<int64_t>(p) * k2p + i) * d_out + o] = acc[t][j][r];
+        for (int s = 0; s < 4; ++s) {
+          xa[s] = xn[s];
+          zb[s] = zn[s];
+        }
+        k0 = kn;
+      } else {
+        compute(k0, xa, zb);
+        break;
       }
     }
   }
-  if (wave == 0 && blockIdx.z == 0) {
+  // column sums of dZ: over the lane's rows, then over q
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float v = dbs[j];
-      v += __shfl_xor(v, 16, 64);
-      v += __shfl_xor(v, 32, 64);
-      const int o = o0 + j * 16 + c16;
-      if (q == 0 && o < d_out) partial_db[static_cast<int64_t>(p) * d_out + o] = v;
+  for (int j = 0; j < 4; ++j) {
+    dbs[j] += __shfl_xor(dbs[j], 16, 64);
+    dbs[j] += __shfl_xor(dbs[j], 32, 64);
+  }
+  // waves 2, 3 -> LDS; waves 0, 1 add; wave 1 -> LDS; wave 0 adds:
+  // ((w0 + w2) + (w1 + w3)), the same order on every run
+  auto put = [&](int slot) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[(slot * 64 + (t * 16 + j * 4 + r)) * 64 + lane] = acc[t][j][r];
+  };
+  auto add = [&](int slot) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[t][j][r] += red[(slot * 64 + (t * 16 + j * 4 + r)) * 64 + lane];
+  };
+  if (wave >= 2) put(wave - 2);
+  if (q == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) red_db[wave][4 * c16 + j] = dbs[j];
+  }
+  __syncthreads();
+  if (wave < 2) add(wave);
+  __syncthreads();
+  if (wave == 1) put(0);
+  __syncthreads();
+  if (wave != 0) return;
+  add(0);
+  float* part = partial + static_cast<int64_t>(p) * (K2 + 1) * ldp;
+  if (ob < ldp) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int c = zc * 64 + 16 * q + 4 * r + t;
+        if (c < d_in)
+          *reinterpret_cast<float4*>(part + static_cast<int64_t>(from_m ? d_in + c : c) * ldp + ob) =
+              make_float4(acc[t][0][r], acc[t][1][r], acc[t][2][r], acc[t][3][r]);
+      }
+    if (blockIdx.z == 0 && q == 0) {
+      float v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        v[j] = (red_db[0][4 * c16 + j] + red_db[2][4 * c16 + j]) + (red_db[1][4 * c16 + j] + red_db[3][4 * c16 + j]);
+      *reinterpret_cast<float4*>(part + static_cast<int64_t>(K2) * ldp + ob) = make_float4(v[0], v[1], v[2], v[3]);
     }
   }
 }
 
-__global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ partial,
-                                                      const float* __restrict__ partial_db, int parts,
-                                                      int k2p, int d_in, int d_out, float* __restrict__ d_self,
+// One float4 of output per thread group of four: group g sums the parts
+// p = g, g + 4, ... in ascending order, the four groups meet in LDS in a
+// fixed order.  Rows i < 2 d_in go to dW_self / dW_neigh, row 2 d_in to db.
+__global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ partial, int parts, int d_in,
+                                                      int d_out, int ldp, float* __restrict__ d_self,
                                                       float* __restrict__ d_neigh, float* __restrict__ d_bias) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int64_t nw = static_cast<int64_t>(2 * d_in) * d_out;
-  if (idx < nw) {
-    const int i = static_cast<int>(idx / d_out), o = static_cast<int>(idx % d_out);
-    float s = 0.f;
-    for (int p = 0; p < parts; ++p) s += partial[(static_cast<int64_t>(p) * k2p + i) * d_out + o];
-    if (i < d_in) d_self[static_cast<int64_t>(i) * d_out + o] = s;
-    else d_neigh[static_cast<int64_t>(i - d_in) * d_out + o] = s;
-  } else if (idx < nw + d_out) {
-    const int o = static_cast<int>(idx - nw);
-    float s = 0.f;
-    for (int p = 0; p < parts; ++p) s += partial_db[static_cast<int64_t>(p) * d_out + o];
-    d_bias[o] = s;
+  __shared__ float4 red[3][64];
+  const int K2 = 2 * d_in;
+  const int per_row = ldp / 4;
+  const int64_t total = static_cast<int64_t>(K2 + 1) * per_row;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 64 + (threadIdx.x & 63);
+  const int g = threadIdx.x >> 6;
+  const bool live = idx < total;
+  const int64_t stride = static_cast<int64_t>(K2 + 1) * ldp;
+  const float* src = partial + (live ? idx * 4 : 0);
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+  int p = g;
+  for (; p + 4 < parts; p += 8) {
+    const float4 x = *reinterpret_cast<const float4*>(src + p * stride);
+    const float4 y = *reinterpret_cast<const float4*>(src + (p + 4) * stride);
+    a.x += x.x; a.y += x.y; a.z += x.z; a.w += x.w;
+    b.x += y.x; b.y += y.y; b.z += y.z; b.w += y.w;
   }
+  if (p < parts) {
+    const float4 x = *reinterpret_cast<const float4*>(src + p * stride);
+    a.x += x.x; a.y += x.y; a.z += x.z; a.w += x.w;
+  }
+  a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+  if (g > 0) red[g - 1][threadIdx.x & 63] = a;
+  __syncthreads();
+  if (g != 0 || !live) return;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const float4 x = red[k][threadIdx.x];
+    a.x += x.x; a.y += x.y; a.z += x.z; a.w += x.w;
+  }
+  const int i = static_cast<int>(idx / per_row);
+  const int o = static_cast<int>(idx % per_row) * 4;
+  float* dst = i < d_in ? d_self + static_cast<int64_t>(i) * d_out
+                        : (i < K2 ? d_neigh + static_cast<int64_t>(i - d_in) * d_out : d_bias);
+  const float v[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (o + j < d_out) dst[o + j] = v[j];
 }
 
 // ---- input gradient -------------------------------------------------------
+
+// The block's edges visited by destination row, e in [indptr[v],
+// indptr[v+1]) clamped to [0, cap_nnz), sources outside [0, n_src) skipped
+// (only after a data error): the count and the fill below see the same
+// edges, so every source's slots are filled exactly once.
+struct EdgeView {
+  const int32_t* indptr;
+  const int32_t* local;
+  int64_t cap_nnz;
+};
+
+__device__ __forceinline__ void edge_range(const EdgeView& ev, int64_t v, int32_t& b, int32_t& e) {
+  b = ev.indptr[v];
+  e = ev.indptr[v + 1];
+  b = b < 0 ? 0 : (b > ev.cap_nnz ? static_cast<int32_t>(ev.cap_nnz) : b);
+  e = e < b ? b : (e > ev.cap_nnz ? static_cast<int32_t>(ev.cap_nnz) : e);
+}
 
 // out = dZ [W_self; W_neigh]^T over the block's n_dst rows: K = d_out (in
 // NCH chunks of 16), output column nn < d_in goes to dH, d_in <= nn < 2 d_in
 // to dM (both with row stride d_in).  The slab holds B[k][nn] = W[nn][k]
 // for the workgroup's 64 columns in operand order (as the forward's slab
-// kernel); lane l (q = l/16) of a wave reads B[16c + 4q .. +3][nn] with one
-// 16-byte LDS read and A = dZ[row][16c + 4q .. +3] (ldz % 4 == 0, zero past
-// d_out) with one 16-byte global read.
-template <int NCH>
+// kernel), filled with 16-byte loads and stores when d_out % 4 == 0 (VEC);
+// lane l (q = l/16) of a wave reads B[16c + 4q .. +3][nn] with one 16-byte
+// LDS read and A = dZ[row][16c + 4q .. +3] (ldz % 4 == 0, zero past d_out)
+// with one 16-byte global read.  Before that, every thread of the grid
+// counts in-edges of the block's sources into cnt (grid-stride over the
+// destination rows).
+template <int NCH, bool VEC>
 __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes, const float* __restrict__ dZ,
                                                int ldz, int d_out, const float* __restrict__ Ws,
                                                const float* __restrict__ Wn, int d_in,
-                                               float* __restrict__ dH, float* __restrict__ dM) {
+                                               float* __restrict__ dH, float* __restrict__ dM, EdgeView ev,
+                                               int32_t* __restrict__ cnt) {
   constexpr int BN = 64;
   __shared__ __attribute__((aligned(16))) float Bp[NCH * 16 * BN];
   const int32_t M = load_size(&sizes[kNDst]);
+  {
+    const int32_t n_src = load_size(&sizes[kNSrc]);
+    const int64_t nthreads = static_cast<int64_t>(gridDim.x) * gridDim.y * blockDim.x;
+    for (int64_t v = (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x;
+         v < M; v += nthreads) {
+      int32_t b, e;
+      edge_range(ev, v, b, e);
+      for (int32_t k = b; k < e; ++k) {
+        const int32_t u = ev.local[k];
+        if (u >= 0 && u < n_src) atomicAdd(&cnt[u], 1);
+      }
+    }
+  }
   const int row_tiles = (M + 63) / 64;
   if (static_cast<int>(blockIdx.x) >= row_tiles) return;
   const int n0 = blockIdx.y * BN;
   const int K2 = 2 * d_in;
-  // fill: item (nn, k) with k fastest, so a weight row is read contiguously
-  constexpr int kItems = BN * NCH * 16;
-  for (int base = 0; base < kItems; base += 256 * 8) {
-    float v[8];
+  if (VEC) {
+    // item (nn, k4): W[n0 + nn][4 k4 .. 4 k4 + 3], k4 fastest
+    constexpr int kPer = BN * NCH * 4 / 256;   // float4 items per thread
+    constexpr int kBatch = kPer < 8 ? kPer : 8;  // kPer is a multiple of it
+    for (int u0 = 0; u0 < kPer; u0 += kBatch) {
+      float4 v[kBatch];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int idx = base + u * 256 + threadIdx.x;
-      const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
-      const int gn = n0 + nn;
-      const bool in = idx < kItems && gn < K2 && k < d_out;
-      const float* w = gn < d_in ? Ws + static_cast<int64_t>(gn) * d_out
-                                 : Wn + static_cast<int64_t>(in ? gn - d_in : 0) * d_out;
-      float x = w[in ? k : 0];
-      asm volatile("" : "+v"(x));
-      v[u] = in ? x : 0.f;
+      for (int u = 0; u < kBatch; ++u) {
+        const int idx = (u0 + u) * 256 + threadIdx.x;
+        const int nn = idx / (NCH * 4), k4 = idx % (NCH * 4);
+        const int gn = n0 + nn;
+        const bool in = gn < K2 && 4 * k4 < d_out;
+        const float* w = gn < d_in ? Ws + static_cast<int64_t>(gn) * d_out
+                                   : Wn + static_cast<int64_t>(in ? gn - d_in : 0) * d_out;
+        float4 x = *reinterpret_cast<const float4*>(w + (in ? 4 * k4 : 0));
+        asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+        v[u] = in ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int idx = (u0 + u) * 256 + threadIdx.x;
+        const int nn = idx / (NCH * 4), k4 = idx % (NCH * 4);
+        *reinterpret_cast<float4*>(&Bp[(((k4 >> 2) * 4 + (k4 & 3)) * BN + nn) * 4]) = v[u];
+      }
     }
+  } else {
+    // item (nn, k) with k fastest, so a weight row is read contiguously
+    constexpr int kItems = BN * NCH * 16;
+    for (int base = 0; base < kItems; base += 256 * 8) {
+      float v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int idx = base + u * 256 + threadIdx.x;
-      if (idx >= kItems) continue;
-      const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
-      Bp[(((k >> 4) * 4 + ((k >> 2) & 3)) * BN + nn) * 4 + (k & 3)] = v[u];
+      for (int u = 0; u < 8; ++u) {
+        const int idx = base + u * 256 + threadIdx.x;
+        const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
+        const int gn = n0 + nn;
+        const bool in = idx < kItems && gn < K2 && k < d_out;
+        const float* w = gn < d_in ? Ws + static_cast<int64_t>(gn) * d_out
+                                   : Wn + static_cast<int64_t>(in ? gn - d_in : 0) * d_out;
+        float x = w[in ? k : 0];
+        asm volatile("" : "+v"(x));
+        v[u] = in ? x : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int idx = base + u * 256 + threadIdx.x;
+        if (idx >= kItems) continue;
+        const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
+        Bp[(((k >> 4) * 4 + ((k >> 2) & 3)) * BN + nn) * 4 + (k & 3)] = v[u];
+      }
     }
   }
   __syncthreads();
@@ -294,59 +450,109 @@ __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes
   }
 }
 
-// ---- mean backward, ReLU, zero fill, SGD ----------------------------------
+// ---- mean backward: the block's transpose -----------------------------------
 
-// rows [n_dst, n_src) of dH (row stride d) := 0
-__global__ __launch_bounds__(256) void k_zero_tail(const int32_t* __restrict__ sizes, float* __restrict__ dH, int d) {
-  const int64_t n_dst = load_size(&sizes[kNDst]), n_src = load_size(&sizes[kNSrc]);
-  const int64_t total = (n_src - n_dst) * d;
-  float* base = dH + n_dst * d;
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-    base[i] = 0.f;
+// One workgroup: off[u] = sum of cnt[0 .. u), off[n_src] = the total,
+// pos[u] = off[u] (the fill's cursors), and cnt cleared for the next layer.
+__global__ __launch_bounds__(1024) void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt,
+                                                   int32_t* __restrict__ off, int32_t* __restrict__ pos) {
+  __shared__ int32_t smem[16];
+  const int32_t n = load_size(&sizes[kNSrc]);
+  int32_t carry = 0;
+  for (int32_t base = 0; base < n; base += 4096) {
+    const int32_t i0 = base + 4 * static_cast<int32_t>(threadIdx.x);
+    int32_t c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = i0 + j < n ? cnt[i0 + j] : 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (i0 + j < n) cnt[i0 + j] = 0;
+    const int32_t x[1] = {c[0] + c[1] + c[2] + c[3]};
+    int32_t excl[1], total[1];
+    block_exclusive_scan_multi<1024, 1>(x, excl, total, smem);
+    int32_t o = carry + excl[0];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (i0 + j < n) {
+        off[i0 + j] = o;
+        pos[i0 + j] = o;
+      }
+      o += c[j];
+    }
+    carry += total[0];
+  }
+  if (threadIdx.x == 0) off[n] = carry;
 }
 
-// G lanes per destination row v; lane c covers columns 4c .. 4c+3 (d % 4 == 0)
-template <int G>
-__global__ __launch_bounds__(256) void k_scatter_mean(const int32_t* __restrict__ sizes,
-                                                      const int32_t* __restrict__ indptr,
-                                                      const int32_t* __restrict__ local,
-                                                      const float* __restrict__ dM, int d,
-                                                      float* __restrict__ dH) {
+// Thread per destination row v: every edge (v <- u) takes the next slot of
+// u and stores (v, 1/k_v) there.
+__global__ __launch_bounds__(256) void k_csc_fill(const int32_t* __restrict__ sizes, EdgeView ev,
+                                                  int32_t* __restrict__ pos, const int32_t* __restrict__ off,
+                                                  int2* __restrict__ csc) {
   const int32_t n_dst = load_size(&sizes[kNDst]);
   const int32_t n_src = load_size(&sizes[kNSrc]);
-  const int64_t v = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
-  const int lane = threadIdx.x & (G - 1);
+  const int64_t v = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (v >= n_dst) return;
-  const int32_t beg = indptr[v], end = indptr[v + 1];
-  const int32_t k = end - beg;
-  if (k <= 0) return;
-  const float inv = 1.f / static_cast<float>(k);
-  const int chunks = d / 4;
-  for (int c = lane; c < chunks; c += G) {
-    float4 g = *reinterpret_cast<const float4*>(dM + v * d + 4 * c);
-    g.x *= inv; g.y *= inv; g.z *= inv; g.w *= inv;
-    for (int32_t e = beg; e < end; ++e) {
-      const int32_t u = local[e];
-      if (u < 0 || u >= n_src) continue;   // only after a data error
-      float* h = dH + static_cast<int64_t>(u) * d + 4 * c;
-      unsafeAtomicAdd(h, g.x);
-      unsafeAtomicAdd(h + 1, g.y);
-      unsafeAtomicAdd(h + 2, g.z);
-      unsafeAtomicAdd(h + 3, g.w);
-    }
+  int32_t b, e;
+  edge_range(ev, v, b, e);
+  if (e <= b) return;
+  const int32_t inv = __float_as_int(1.f / static_cast<float>(e - b));
+  for (int32_t k = b; k < e; ++k) {
+    const int32_t u = ev.local[k];
+    if (u < 0 || u >= n_src) continue;
+    const int32_t slot = atomicAdd(&pos[u], 1);
+    if (slot < off[u + 1] && slot < ev.cap_nnz) csc[slot] = make_int2(static_cast<int32_t>(v), inv);
   }
 }
 
-// dH[i] := dH[i] if out[i] > 0 else 0, for the n_dst rows of the block that
-// produced `out` (row stride d)
-__global__ __launch_bounds__(256) void k_relu_mask(const int32_t* __restrict__ sizes, const float* __restrict__ out,
-                                                   int d, float* __restrict__ dH) {
-  const int64_t n = static_cast<int64_t>(load_size(&sizes[kNDst])) * d;
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-    dH[i] = out[i] > 0.f ? dH[i] : 0.f;
+// G lanes per source row u, lane c covers columns 4c, 4c + G, ... (d % 4 ==
+// 0): dH[u] = (out[u] > 0) * ((u < n_dst ? dH[u] : 0) + sum over u's
+// transpose entries (v, w) of w * dM[v]).  out is the layer below's output.
+template <int G>
+__global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ sizes,
+                                                   const int32_t* __restrict__ off, const int2* __restrict__ csc,
+                                                   int64_t cap_nnz, const float* __restrict__ dM,
+                                                   const float* __restrict__ out, int d, float* __restrict__ dH) {
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  const int32_t n_src = load_size(&sizes[kNSrc]);
+  const int64_t u = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
+  const int lane = threadIdx.x & (G - 1);
+  if (u >= n_src) return;
+  int32_t s0 = off[u], s1 = off[u + 1];
+  s0 = s0 < 0 ? 0 : s0;
+  s1 = s1 > cap_nnz ? static_cast<int32_t>(cap_nnz) : s1;
+  const bool self = u < n_dst;
+  const int chunks = d / 4;
+  for (int c = lane; c < chunks; c += G) {
+    const int64_t at = u * d + 4 * c;
+    float4 acc = self ? *reinterpret_cast<const float4*>(dH + at) : make_float4(0.f, 0.f, 0.f, 0.f);
+    int32_t s = s0;
+    for (; s + 1 < s1; s += 2) {
+      const int2 e0 = csc[s], e1 = csc[s + 1];
+      const bool ok0 = e0.x >= 0 && e0.x < n_dst, ok1 = e1.x >= 0 && e1.x < n_dst;
+      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
+      const float4 g1 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok1 ? e1.x : 0) * d + 4 * c);
+      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f, w1 = ok1 ? __int_as_float(e1.y) : 0.f;
+      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
+      acc.x += w1 * g1.x; acc.y += w1 * g1.y; acc.z += w1 * g1.z; acc.w += w1 * g1.w;
+    }
+    if (s < s1) {
+      const int2 e0 = csc[s];
+      const bool ok0 = e0.x >= 0 && e0.x < n_dst;
+      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
+      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f;
+      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
+    }
+    const float4 o = *reinterpret_cast<const float4*>(out + at);
+    acc.x = o.x > 0.f ? acc.x : 0.f;
+    acc.y = o.y > 0.f ? acc.y : 0.f;
+    acc.z = o.z > 0.f ? acc.z : 0.f;
+    acc.w = o.w > 0.f ? acc.w : 0.f;
+    *reinterpret_cast<float4*>(dH + at) = acc;
+  }
 }
+
+// ---- SGD ------------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void k_sgd(SgdArgs a, float lr) {
   for (int t = 0; t < a.count; ++t) {
@@ -368,47 +574,58 @@ inline unsigned grid_of(int64_t threads, int64_t cap = 65535) {
 }  // namespace
 
 hipError_t launch_xent(const float* logits, const int32_t* labels, int n, int C, int ldz, float* dz,
-                       float* loss_rows, float* loss, hipStream_t s) {
-  if (n > 0)
-    hipLaunchKernelGGL(k_xent, dim3((n + 3) / 4), dim3(256), 0, s, logits, labels, n, C, ldz, dz, loss_rows);
+                       float* loss_rows, float* loss, int32_t* clear, int64_t clear_n, hipStream_t s) {
+  const unsigned g = static_cast<unsigned>(std::max(1, (n + 3) / 4));
+  hipLaunchKernelGGL(k_xent, dim3(g), dim3(256), 0, s, logits, labels, n, C, ldz, dz, loss_rows, clear, clear_n);
   if (loss) hipLaunchKernelGGL(k_loss_sum, dim3(1), dim3(256), 0, s, loss_rows, n, loss);
   return hipGetLastError();
 }
 
+int wgrad_ldp(int d_out) { return (d_out + 3) / 4 * 4; }
+
+// Row ranges of the weight gradient: about 512 workgroups over all tiles
+// (two per CU at the kernel's register use),
+// at least 64 rows each, a multiple of 8 when above 8 so that the tiles of
+// one row range (workgroup ids p + k * parts) share an XCD and its L2.
 int wgrad_parts(int64_t cap_rows, int d_in, int d_out) {
-  const int col_tiles = (d_out + 63) / 64;
-  const int zg = (2 * d_in + 255) / 256;
-  int parts = static_cast<int>((1024 + col_tiles * zg - 1) / (col_tiles * zg));
-  const int64_t by_rows = (cap_rows + 15) / 16;
+  const int tiles = ((wgrad_ldp(d_out) + 63) / 64) * (2 * ((d_in + 63) / 64));
+  int parts = (512 + tiles - 1) / tiles;
+  const int64_t by_rows = (cap_rows + 63) / 64;
   if (parts > by_rows) parts = static_cast<int>(by_rows);
+  if (parts > 8) parts = parts / 8 * 8;
   return parts < 1 ? 1 : parts;
 }
 
-int wgrad_rows_per_part(int64_t cap_rows, int parts) {
+static int wgrad_rows_per_part(int64_t cap_rows, int parts) {
   int64_t r = (cap_rows + parts - 1) / parts;
-  r = (r + 15) / 16 * 16;
-  return static_cast<int>(r < 16 ? 16 : r);
+  r = (r + 63) / 64 * 64;
+  return static_cast<int>(r < 64 ? 64 : r);
 }
 
-int wgrad_k2p(int d_in) { return (2 * d_in + 15) / 16 * 16; }
-
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
-                        int d_out, int64_t cap_rows, float* partial, float* partial_db, float* d_self,
-                        float* d_neigh, float* d_bias, hipStream_t s) {
+                        int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
+                        float* d_bias, hipStream_t s) {
   const int parts = wgrad_parts(cap_rows, d_in, d_out);
   const int rpp = wgrad_rows_per_part(cap_rows, parts);
-  const int k2p = wgrad_k2p(d_in);
-  const dim3 grid(parts, (d_out + 63) / 64, (2 * d_in + 255) / 256);
-  hipLaunchKernelGGL(k_wgrad, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, d_out, rpp, k2p, partial,
-                     partial_db);
-  const int64_t outs = static_cast<int64_t>(2 * d_in) * d_out + d_out;
-  hipLaunchKernelGGL(k_wgrad_reduce, dim3(grid_of(outs, 1 << 30)), dim3(256), 0, s, partial, partial_db, parts,
-                     k2p, d_in, d_out, d_self, d_neigh, d_bias);
+  const int ldp = wgrad_ldp(d_out);
+  const dim3 grid(parts, (ldp + 63) / 64, 2 * ((d_in + 63) / 64));
+  if (static_cast<uint64_t>(std::max<int64_t>(cap_rows, 1)) * std::max(d_in, ldz) * 4 >= (1ull << 32))
+    return hipErrorInvalidValue;
+  const bool vec = d_in % 4 == 0 && reinterpret_cast<uintptr_t>(H) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(M) % 16 == 0;
+  if (vec)
+    hipLaunchKernelGGL(k_wgrad<true>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, rpp, partial);
+  else
+    hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, rpp, partial);
+  const int64_t outs = static_cast<int64_t>(2 * d_in + 1) * (ldp / 4);
+  hipLaunchKernelGGL(k_wgrad_reduce, dim3(static_cast<unsigned>((outs + 63) / 64)), dim3(256), 0, s, partial,
+                     parts, d_in, d_out, ldp, d_self, d_neigh, d_bias);
   return hipGetLastError();
 }
 
 hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_out, const float* ws,
-                        const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows, hipStream_t s) {
+                        const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
+                        const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t* cnt, hipStream_t s) {
   const int nch = (d_out + 15) / 16;
   const int col_tiles = (2 * d_in + 63) / 64;
   int64_t rows = (cap_rows + 63) / 64;
@@ -416,7 +633,18 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
   if (rows > want) rows = want;
   if (rows < 1) rows = 1;
   const dim3 grid(static_cast<unsigned>(rows), col_tiles);
-#define GMB_DGRAD(C) hipLaunchKernelGGL(k_dgrad<C>, grid, dim3(256), 0, s, sizes, dZ, ldz, d_out, ws, wn, d_in, dH, dM)
+  const EdgeView ev{indptr, local, cap_nnz};
+  const bool vec = d_out % 4 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(wn) % 16 == 0;
+#define GMB_DGRAD(C)                                                                                          \
+  do {                                                                                                        \
+    if (vec)                                                                                                  \
+      hipLaunchKernelGGL((k_dgrad<C, true>), grid, dim3(256), 0, s, sizes, dZ, ldz, d_out, ws, wn, d_in, dH, dM, \
+                         ev, cnt);                                                                            \
+    else                                                                                                      \
+      hipLaunchKernelGGL((k_dgrad<C, false>), grid, dim3(256), 0, s, sizes, dZ, ldz, d_out, ws, wn, d_in, dH,    \
+                         dM, ev, cnt);                                                                        \
+  } while (0)
   if (nch <= 4) GMB_DGRAD(4);
   else if (nch <= 8) GMB_DGRAD(8);
   else if (nch <= 16) GMB_DGRAD(16);
@@ -427,28 +655,28 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
   return hipGetLastError();
 }
 
-hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local, const float* dM,
-                                int d, float* dH, int64_t cap_dst, int64_t cap_src, hipStream_t s) {
-  hipLaunchKernelGGL(k_zero_tail, dim3(grid_of((cap_src - 0) * d / 4 + 1, 8192)), dim3(256), 0, s, sizes, dH, d);
+hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
+                                int64_t cap_nnz, const float* dM, const float* out, int d, float* dH,
+                                int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
+                                int2* csc, hipStream_t s) {
+  const EdgeView ev{indptr, local, cap_nnz};
+  hipLaunchKernelGGL(k_csc_scan, dim3(1), dim3(1024), 0, s, sizes, cnt, off, pos);
+  hipLaunchKernelGGL(k_csc_fill, dim3(grid_of(std::max<int64_t>(cap_dst, 1), 1 << 30)), dim3(256), 0, s, sizes,
+                     ev, pos, off, csc);
   const int chunks = d / 4;
   int G = 64;
-  if (chunks <= 8) G = 8;
+  if (chunks <= 4) G = 4;
+  else if (chunks <= 8) G = 8;
   else if (chunks <= 16) G = 16;
   else if (chunks <= 32) G = 32;
-  const dim3 grid(grid_of(std::max<int64_t>(cap_dst, 1) * G, 1 << 30));
+  const dim3 grid(grid_of(std::max<int64_t>(cap_src, 1) * G, 1 << 30));
   switch (G) {
-    case 8: hipLaunchKernelGGL(k_scatter_mean<8>, grid, dim3(256), 0, s, sizes, indptr, local, dM, d, dH); break;
-    case 16: hipLaunchKernelGGL(k_scatter_mean<16>, grid, dim3(256), 0, s, sizes, indptr, local, dM, d, dH); break;
-    case 32: hipLaunchKernelGGL(k_scatter_mean<32>, grid, dim3(256), 0, s, sizes, indptr, local, dM, d, dH); break;
-    default: hipLaunchKernelGGL(k_scatter_mean<64>, grid, dim3(256), 0, s, sizes, indptr, local, dM, d, dH); break;
+    case 4: hipLaunchKernelGGL(k_pull_mean<4>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
+    case 8: hipLaunchKernelGGL(k_pull_mean<8>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
+    case 16: hipLaunchKernelGGL(k_pull_mean<16>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
+    case 32: hipLaunchKernelGGL(k_pull_mean<32>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
+    default: hipLaunchKernelGGL(k_pull_mean<64>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_relu_mask(const int32_t* sizes, const float* out, int d, float* dH, int64_t cap_rows,
-                            hipStream_t s) {
-  hipLaunchKernelGGL(k_relu_mask, dim3(grid_of(std::max<int64_t>(cap_rows, 1) * d / 4 + 1, 8192)), dim3(256), 0,
-                     s, sizes, out, d, dH);
   return hipGetLastError();
 }
 
