@@ -437,6 +437,8 @@ struct BackwardPlan {
   size_t off_a, off_b, off_dm, off_part, off_lossrows;
   size_t off_cnt, off_off, off_pos, off_csc;   // the transpose of a block
   int64_t cnt_len;                             // ints of the edge counters
+  int64_t scan_len;                            // ints of one layer's scan state
+  int64_t clear_len;                           // ints cleared at the start (counters + scan states)
   size_t total;
 };
 
@@ -477,9 +479,11 @@ int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* 
   off = align_up(off + 4 * part);
   p.off_lossrows = off;
   off = align_up(off + 4 * static_cast<size_t>(std::max(b->num_seeds, 1)));
-  p.cnt_len = static_cast<int64_t>(src);
+  p.cnt_len = static_cast<int64_t>((src + 1) / 2 * 2);
+  p.scan_len = 2 + 2 * gmb::csc_scan_tiles(static_cast<int64_t>(src));
+  p.clear_len = p.cnt_len + static_cast<int64_t>(std::max(L - 1, 0)) * p.scan_len;
   p.off_cnt = off;
-  off = align_up(off + 4 * src);
+  off = align_up(off + 4 * static_cast<size_t>(p.clear_len));
   p.off_off = off;
   off = align_up(off + 4 * (src + 1));
   p.off_pos = off;
@@ -539,7 +543,7 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
   int32_t* pos = reinterpret_cast<int32_t*>(base + p.off_pos);
   int2* csc = reinterpret_cast<int2*>(base + p.off_csc);
   hipError_t e = gmb::launch_xent(logits, labels, blocks->num_seeds, weights->dims[L], p.ldz[L - 1], cur,
-                                  reinterpret_cast<float*>(base + p.off_lossrows), loss, cnt, p.cnt_len, s);
+                                  reinterpret_cast<float*>(base + p.off_lossrows), loss, cnt, p.clear_len, s);
   if (e != hipSuccess) return hip_fail(e, "loss launch");
   for (int l = L - 1; l >= 0; --l) {
     const gmb_block& bk = blocks->blk[l];
@@ -555,12 +559,13 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
     // in-edge counts per source on the way
     e = gmb::launch_dgrad(bk.sizes, cur, p.ldz[l], d_out, static_cast<const float*>(weights->w_self[l]),
                           static_cast<const float*>(weights->w_neigh[l]), d_in, other, dM, bk.cap_dst, bk.indptr,
-                          bk.indices, bk.cap_nnz, cnt, s);
+                          bk.indices, bk.cap_nnz, bk.fanout, cnt, s);
     if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
     // the mean's backward through the block's transpose, the ReLU of the
     // layer below on the way out: `other` becomes that layer's dZ
-    e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, bk.cap_nnz, dM, h_in, d_in, other, bk.cap_dst,
-                                  bk.cap_src, cnt, offs, pos, csc, s);
+    uint32_t* scan_state = reinterpret_cast<uint32_t*>(cnt + p.cnt_len + (l - 1) * p.scan_len);
+    e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, bk.cap_nnz, bk.fanout, dM, h_in, d_in, other,
+                                  bk.cap_dst, bk.cap_src, cnt, offs, pos, scan_state, csc, s);
     if (e != hipSuccess) return hip_fail(e, "mean-backward launch");
     std::swap(cur, other);
   }

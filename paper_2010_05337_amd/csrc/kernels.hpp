@@ -134,11 +134,15 @@ hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, in
                         float* d_bias, hipStream_t s);
 hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_out, const float* ws,
                         const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
-                        const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t* cnt, hipStream_t s);
+                        const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t fanout, int32_t* cnt,
+                        hipStream_t s);
+// look-back tiles of the transpose scan over cap_src sources; its state
+// (one ticket word pair, then 2 words per tile) must start zeroed
+int64_t csc_scan_tiles(int64_t cap_src);
 hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
-                                int64_t cap_nnz, const float* dM, const float* out, int d, float* dH,
+                                int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
-                                int2* csc, hipStream_t s);
+                                uint32_t* scan_state, int2* csc, hipStream_t s);
 hipError_t launch_sgd(const SgdArgs& a, float lr, hipStream_t s);
 
 }  // namespace gmb

@@ -94,7 +94,8 @@ __global__ __launch_bounds__(256) void k_loss_sum(const float* __restrict__ rows
 // Workgroup (p, y, z) owns 64 rows of [dW_self; dW_neigh] -- columns
 // [64 z', 64 z' + 64) of H (z < TI = ceil(d_in / 64), z' = z) or of M
 // (z' = z - TI), the output rows d_in + those -- and output columns
-// [64 y, 64 y + 64), over the block rows [p R, (p + 1) R); wave w takes the
+// [64 y, 64 y + 64), over the block rows [p R, (p + 1) R) (R: the n_dst rows
+// split over the gridDim.x ranges); wave w takes the
 // 16-row steps w, w + 4, ... of that range.  Lane (q, c) = (l / 16, l % 16)
 // owns the four columns 64 z' + 4c + t of its array and o = 64 y + 4c + j of
 // dZ, and reads each as one 16-byte load (VEC; else four scalar loads).
@@ -112,10 +113,10 @@ __global__ __launch_bounds__(256) void k_loss_sum(const float* __restrict__ rows
 constexpr int kWgradRed = 2 * 64 * 64;   // LDS floats of the cross-wave sum
 
 template <bool VEC>
-__global__ __launch_bounds__(256) void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
                                                const float* __restrict__ M, int d_in,
                                                const float* __restrict__ dZ, int ldz, int ldp,
-                                               int rows_per_part, float* __restrict__ partial) {
+                                               float* __restrict__ partial) {
   __shared__ float red[kWgradRed];
   __shared__ float red_db[4][64];
   const int32_t n = load_size(&sizes[kNDst]);
@@ -135,7 +136,10 @@ __global__ __launch_bounds__(256) void k_wgrad(const int32_t* __restrict__ sizes
   uint32_t xcol[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) xcol[t] = static_cast<uint32_t>(VEC ? (cb < d_in ? cb : 0) : (cb + t < d_in ? cb + t : 0)) * 4u;
-  const int r0 = p * rows_per_part;
+  // the block's actual rows split evenly over the gridDim.x ranges (16-row
+  // granules); every range writes its partial, empty or not
+  const int rows_per_part = ((n + gridDim.x - 1) / gridDim.x + 15) / 16 * 16;
+  const int r0 = min(p * rows_per_part, n);
   const int r1 = min(r0 + rows_per_part, n);
   floatx4 acc[4][4];
 #pragma unroll
@@ -175,27 +179,29 @@ __global__ __launch_bounds__(256) void k_wgrad(const int32_t* __restrict__ sizes
     }
   };
 
+  // loads run two steps ahead of the products.  The body is unrolled three
+  // times so that every buffer keeps its registers (a copy between buffers
+  // would wait for the load); the step count is rounded up to a multiple of
+  // three, the extra steps read the range's last row and add zero, and no
+  // branch surrounds a product, so the accumulators stay in place
   int k0 = r0 + 16 * wave;
-  if (k0 < r1) {
-    float4 xa[4], zb[4];
-    load(k0, xa, zb);
-    for (;;) {
-      const int kn = k0 + 64;
-      if (kn < r1) {
-        float4 xn[4], zn[4];
-        load(kn, xn, zn);
-        compute(k0, xa, zb);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          xa[s] = xn[s];
-          zb[s] = zn[s];
-        }
-        k0 = kn;
-      } else {
-        compute(k0, xa, zb);
-        break;
-      }
-    }
+  const int nsteps = __builtin_amdgcn_readfirstlane(k0 < r1 ? (r1 - k0 + 63) / 64 : 0);
+  float4 xa[4], za[4], xb[4], zb[4], xc[4], zc4[4];
+  if (nsteps > 0) {
+    load(k0, xa, za);
+    load(k0 + 64, xb, zb);
+  }
+  for (int it = 0; it < nsteps; it += 3) {
+    load(k0 + 128, xc, zc4);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(k0, xa, za);
+    load(k0 + 192, xa, za);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(k0 + 64, xb, zb);
+    load(k0 + 256, xb, zb);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(k0 + 128, xc, zc4);
+    k0 += 192;
   }
   // column sums of dZ: over the lane's rows, then over q
 #pragma unroll
@@ -302,14 +308,16 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ 
 
 // ---- input gradient -------------------------------------------------------
 
-// The block's edges visited by destination row, e in [indptr[v],
-// indptr[v+1]) clamped to [0, cap_nnz), sources outside [0, n_src) skipped
-// (only after a data error): the count and the fill below see the same
-// edges, so every source's slots are filled exactly once.
+// The block's edges as slots (v, j), j < fanout (a sampled row holds at
+// most fanout edges): slot (v, j) is edge indptr[v] + j if that is below
+// indptr[v+1] and cap_nnz; sources outside [0, n_src) are skipped (only
+// after a data error).  The count and the fill below enumerate the same
+// slots, so every source's places in the transpose are filled exactly once.
 struct EdgeView {
   const int32_t* indptr;
   const int32_t* local;
   int64_t cap_nnz;
+  int32_t fanout;
 };
 
 __device__ __forceinline__ void edge_range(const EdgeView& ev, int64_t v, int32_t& b, int32_t& e) {
@@ -319,6 +327,25 @@ __device__ __forceinline__ void edge_range(const EdgeView& ev, int64_t v, int32_
   e = e < b ? b : (e > ev.cap_nnz ? static_cast<int32_t>(ev.cap_nnz) : e);
 }
 
+// Calls f(v, u, k_v) for every slot of the block that holds an edge, slot
+// t = v * fanout + j over a grid-stride loop starting at t0.
+template <typename F>
+__device__ __forceinline__ void for_each_edge_slot(const EdgeView& ev, int32_t n_dst, int32_t n_src, int64_t t0,
+                                                   int64_t stride, F&& f) {
+  if (ev.fanout < 1) return;
+  const int64_t total = static_cast<int64_t>(n_dst) * ev.fanout;
+  for (int64_t t = t0; t < total; t += stride) {
+    const int64_t v = t / ev.fanout;
+    const int32_t j = static_cast<int32_t>(t - v * ev.fanout);
+    int32_t b, e;
+    edge_range(ev, v, b, e);
+    if (b + j >= e) continue;
+    const int32_t u = ev.local[b + j];
+    if (u < 0 || u >= n_src) continue;
+    f(v, u, e - b);
+  }
+}
+
 // out = dZ [W_self; W_neigh]^T over the block's n_dst rows: K = d_out (in
 // NCH chunks of 16), output column nn < d_in goes to dH, d_in <= nn < 2 d_in
 // to dM (both with row stride d_in).  The slab holds B[k][nn] = W[nn][k]
@@ -326,9 +353,9 @@ __device__ __forceinline__ void edge_range(const EdgeView& ev, int64_t v, int32_
 // kernel), filled with 16-byte loads and stores when d_out % 4 == 0 (VEC);
 // lane l (q = l/16) of a wave reads B[16c + 4q .. +3][nn] with one 16-byte
 // LDS read and A = dZ[row][16c + 4q .. +3] (ldz % 4 == 0, zero past d_out)
-// with one 16-byte global read.  Before that, every thread of the grid
+// with one 16-byte global read.  Afterwards every thread of the grid
 // counts in-edges of the block's sources into cnt (grid-stride over the
-// destination rows).
+// edge slots).
 template <int NCH, bool VEC>
 __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes, const float* __restrict__ dZ,
                                                int ldz, int d_out, const float* __restrict__ Ws,
@@ -336,173 +363,210 @@ __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes
                                                float* __restrict__ dH, float* __restrict__ dM, EdgeView ev,
                                                int32_t* __restrict__ cnt) {
   constexpr int BN = 64;
-  __shared__ __attribute__((aligned(16))) float Bp[NCH * 16 * BN];
+  // float4 stride of the slab rows (c, q): one float4 of padding where it
+  // fits, so that the fill's stores (consecutive lanes in consecutive rows)
+  // spread over all banks
+  constexpr int RS = NCH <= 32 ? BN + 1 : BN;
+  __shared__ __attribute__((aligned(16))) float Bp[NCH * 4 * RS * 4];
   const int32_t M = load_size(&sizes[kNDst]);
-  {
-    const int32_t n_src = load_size(&sizes[kNSrc]);
-    const int64_t nthreads = static_cast<int64_t>(gridDim.x) * gridDim.y * blockDim.x;
-    for (int64_t v = (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x;
-         v < M; v += nthreads) {
-      int32_t b, e;
-      edge_range(ev, v, b, e);
-      for (int32_t k = b; k < e; ++k) {
-        const int32_t u = ev.local[k];
-        if (u >= 0 && u < n_src) atomicAdd(&cnt[u], 1);
-      }
-    }
-  }
   const int row_tiles = (M + 63) / 64;
-  if (static_cast<int>(blockIdx.x) >= row_tiles) return;
-  const int n0 = blockIdx.y * BN;
-  const int K2 = 2 * d_in;
-  if (VEC) {
-    // item (nn, k4): W[n0 + nn][4 k4 .. 4 k4 + 3], k4 fastest
-    constexpr int kPer = BN * NCH * 4 / 256;   // float4 items per thread
-    constexpr int kBatch = kPer < 8 ? kPer : 8;  // kPer is a multiple of it
-    for (int u0 = 0; u0 < kPer; u0 += kBatch) {
-      float4 v[kBatch];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int idx = (u0 + u) * 256 + threadIdx.x;
-        const int nn = idx / (NCH * 4), k4 = idx % (NCH * 4);
-        const int gn = n0 + nn;
-        const bool in = gn < K2 && 4 * k4 < d_out;
-        const float* w = gn < d_in ? Ws + static_cast<int64_t>(gn) * d_out
-                                   : Wn + static_cast<int64_t>(in ? gn - d_in : 0) * d_out;
-        float4 x = *reinterpret_cast<const float4*>(w + (in ? 4 * k4 : 0));
-        asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
-        v[u] = in ? x : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int idx = (u0 + u) * 256 + threadIdx.x;
-        const int nn = idx / (NCH * 4), k4 = idx % (NCH * 4);
-        *reinterpret_cast<float4*>(&Bp[(((k4 >> 2) * 4 + (k4 & 3)) * BN + nn) * 4]) = v[u];
-      }
-    }
-  } else {
-    // item (nn, k) with k fastest, so a weight row is read contiguously
-    constexpr int kItems = BN * NCH * 16;
-    for (int base = 0; base < kItems; base += 256 * 8) {
-      float v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int idx = base + u * 256 + threadIdx.x;
-        const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
-        const int gn = n0 + nn;
-        const bool in = idx < kItems && gn < K2 && k < d_out;
-        const float* w = gn < d_in ? Ws + static_cast<int64_t>(gn) * d_out
-                                   : Wn + static_cast<int64_t>(in ? gn - d_in : 0) * d_out;
-        float x = w[in ? k : 0];
-        asm volatile("" : "+v"(x));
-        v[u] = in ? x : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int idx = base + u * 256 + threadIdx.x;
-        if (idx >= kItems) continue;
-        const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
-        Bp[(((k >> 4) * 4 + ((k >> 2) & 3)) * BN + nn) * 4 + (k & 3)] = v[u];
-      }
-    }
-  }
-  __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, r16 = lane & 15;
-  for (int rt = blockIdx.x; rt < row_tiles; rt += gridDim.x) {
-    const int row = rt * 64 + wave * 16 + r16;
-    const float* zr = dZ + static_cast<int64_t>(row < M ? row : M - 1) * ldz;
+  const int n0 = blockIdx.y * BN;
+  const int K2 = 2 * d_in;
+  if (static_cast<int>(blockIdx.x) < row_tiles) {
+    // A of the first row tile: dZ[row][16c + 4q .. +3], issued before the
+    // slab fill so that the two latencies overlap
+    // (all loads issued first, then one opaque step over the values so that
+    // the selects cannot become branched loads, then the selects: one wait)
+    auto issue_a = [&](int rt, float4 (&a)[NCH]) {
+      const int row = rt * 64 + wave * 16 + r16;
+      const float* zr = dZ + static_cast<int64_t>(row < M ? row : M - 1) * ldz;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const int k = 16 * c + 4 * q;
+        a[c] = *reinterpret_cast<const float4*>(zr + (k < ldz ? k : 0));
+      }
+    };
+    auto finish_a = [&](float4 (&a)[NCH]) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) asm volatile("" : "+v"(a[c].x), "+v"(a[c].y), "+v"(a[c].z), "+v"(a[c].w));
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+        if (16 * c + 4 * q >= ldz) a[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    };
     float4 a[NCH];
+    issue_a(blockIdx.x, a);
+    if (VEC) {
+      // item (nn, k4): W[n0 + nn][4 k4 .. 4 k4 + 3], k4 fastest; all of a
+      // thread's loads in flight at once
+      constexpr int kPer = BN * NCH * 4 / 256;
+      constexpr int kBatch = kPer % 16 == 0 ? 16 : (kPer % 8 == 0 ? 8 : kPer);
+      static_assert(kPer % kBatch == 0, "the fill batches must tile the slab exactly");
+      for (int u0 = 0; u0 < kPer; u0 += kBatch) {
+        float4 v[kBatch];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int k = 16 * c + 4 * q;
-      float4 x = *reinterpret_cast<const float4*>(zr + (k < ldz ? k : 0));
-      asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
-      a[c] = k < ldz ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int u = 0; u < kBatch; ++u) {
+          const int idx = (u0 + u) * 256 + threadIdx.x;
+          const int nn = idx / (NCH * 4), k4 = idx % (NCH * 4);
+          const int gn = n0 + nn;
+          const bool in = gn < K2 && 4 * k4 < d_out;
+          const float* w = gn < d_in ? Ws + static_cast<int64_t>(gn) * d_out
+                                     : Wn + static_cast<int64_t>(in ? gn - d_in : 0) * d_out;
+          v[u] = *reinterpret_cast<const float4*>(w + (in ? 4 * k4 : 0));
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) asm volatile("" : "+v"(v[u].x), "+v"(v[u].y), "+v"(v[u].z), "+v"(v[u].w));
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          const int idx = (u0 + u) * 256 + threadIdx.x;
+          const int nn = idx / (NCH * 4), k4 = idx % (NCH * 4);
+          const bool in = n0 + nn < K2 && 4 * k4 < d_out;
+          *reinterpret_cast<float4*>(&Bp[(k4 * RS + nn) * 4]) = in ? v[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+    } else {
+      // item (nn, k) with k fastest, so a weight row is read contiguously
+      constexpr int kItems = BN * NCH * 16;
+      for (int base = 0; base < kItems; base += 256 * 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int idx = base + u * 256 + threadIdx.x;
+          const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
+          const int gn = n0 + nn;
+          const bool in = idx < kItems && gn < K2 && k < d_out;
+          const float* w = gn < d_in ? Ws + static_cast<int64_t>(gn) * d_out
+                                     : Wn + static_cast<int64_t>(in ? gn - d_in : 0) * d_out;
+          v[u] = w[in ? k : 0];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) asm volatile("" : "+v"(v[u]));
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int idx = base + u * 256 + threadIdx.x;
+          if (idx >= kItems) continue;
+          const int nn = idx / (NCH * 16), k = idx % (NCH * 16);
+          const bool in = n0 + nn < K2 && k < d_out;
+          Bp[((k >> 2) * RS + nn) * 4 + (k & 3)] = in ? v[u] : 0.f;
+        }
+      }
     }
-    floatx4 acc[4];
+    finish_a(a);
+    __syncthreads();
+    for (int rt = blockIdx.x;;) {
+      floatx4 acc[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < 4; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      float4 b[4];
+      for (int c = 0; c < NCH; ++c) {
+        float4 b[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const float4*>(&Bp[(((c * 4 + q) * BN) + j * 16 + r16) * 4]);
+        for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const float4*>(&Bp[((c * 4 + q) * RS + j * 16 + r16) * 4]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].x, b[j].x, acc[j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].x, b[j].x, acc[j], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].y, b[j].y, acc[j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].y, b[j].y, acc[j], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].z, b[j].z, acc[j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].z, b[j].z, acc[j], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].w, b[j].w, acc[j], 0, 0, 0);
-    }
-    const int orow0 = rt * 64 + wave * 16 + 4 * q;
+        for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c].w, b[j].w, acc[j], 0, 0, 0);
+      }
+      const int orow0 = rt * 64 + wave * 16 + 4 * q;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int nn = n0 + j * 16 + r16;
-      if (nn >= K2) continue;
-      float* dst = nn < d_in ? dH + nn : dM + (nn - d_in);
+      for (int j = 0; j < 4; ++j) {
+        const int nn = n0 + j * 16 + r16;
+        if (nn >= K2) continue;
+        float* dst = nn < d_in ? dH + nn : dM + (nn - d_in);
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (orow0 + r < M) dst[static_cast<int64_t>(orow0 + r) * d_in] = acc[j][r];
+        for (int r = 0; r < 4; ++r)
+          if (orow0 + r < M) dst[static_cast<int64_t>(orow0 + r) * d_in] = acc[j][r];
+      }
+      rt += gridDim.x;
+      if (rt >= row_tiles) break;
+      issue_a(rt, a);
+      finish_a(a);
     }
   }
+  // the block's in-edge count per source, for the transpose (the next
+  // kernel on the stream reads it)
+  for_each_edge_slot(ev, M, load_size(&sizes[kNSrc]),
+                     (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x,
+                     static_cast<int64_t>(gridDim.x) * gridDim.y * blockDim.x,
+                     [&](int64_t, int32_t u, int32_t) { atomicAdd(&cnt[u], 1); });
 }
 
 // ---- mean backward: the block's transpose -----------------------------------
 
-// One workgroup: off[u] = sum of cnt[0 .. u), off[n_src] = the total,
-// pos[u] = off[u] (the fill's cursors), and cnt cleared for the next layer.
-__global__ __launch_bounds__(1024) void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt,
-                                                   int32_t* __restrict__ off, int32_t* __restrict__ pos) {
-  __shared__ int32_t smem[16];
+// off[u] = sum of cnt[0 .. u), off[n_src] = the total, pos[u] = off[u]
+// (the fill's cursors), and cnt cleared for the next layer.  Tiles of 1024
+// counts (four per thread), numbered by an atomic ticket, joined by the
+// decoupled look-back (both the ticket and the look-back words start at 0).
+// If the look-back's bounded wait runs out (it does not when every tile
+// runs), the offsets come out wrong but the fill and the pull stay in
+// bounds.
+constexpr int kScanTile = 1024;
+
+__global__ __launch_bounds__(256) void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt,
+                                                  int32_t* __restrict__ off, int32_t* __restrict__ pos,
+                                                  uint32_t* __restrict__ ticket, uint64_t* __restrict__ words) {
+  __shared__ int s_tile;
+  __shared__ int32_t s_excl;
+  __shared__ int32_t smem[4];
   const int32_t n = load_size(&sizes[kNSrc]);
-  int32_t carry = 0;
-  for (int32_t base = 0; base < n; base += 4096) {
-    const int32_t i0 = base + 4 * static_cast<int32_t>(threadIdx.x);
-    int32_t c[4];
+  const int tile = claim_tile(ticket, &s_tile);
+  const int ntiles = (n + kScanTile - 1) / kScanTile;
+  if (tile >= ntiles) {
+    if (tile == 0 && threadIdx.x == 0) off[0] = 0;
+    return;
+  }
+  const int32_t i0 = tile * kScanTile + 4 * static_cast<int32_t>(threadIdx.x);
+  int32_t c[4];
+  if (i0 + 3 < n) {
+    const int4 x = *reinterpret_cast<const int4*>(cnt + i0);
+    c[0] = x.x; c[1] = x.y; c[2] = x.z; c[3] = x.w;
+    *reinterpret_cast<int4*>(cnt + i0) = make_int4(0, 0, 0, 0);
+  } else {
 #pragma unroll
     for (int j = 0; j < 4; ++j) c[j] = i0 + j < n ? cnt[i0 + j] : 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       if (i0 + j < n) cnt[i0 + j] = 0;
-    const int32_t x[1] = {c[0] + c[1] + c[2] + c[3]};
-    int32_t excl[1], total[1];
-    block_exclusive_scan_multi<1024, 1>(x, excl, total, smem);
-    int32_t o = carry + excl[0];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (i0 + j < n) {
-        off[i0 + j] = o;
-        pos[i0 + j] = o;
-      }
-      o += c[j];
-    }
-    carry += total[0];
   }
-  if (threadIdx.x == 0) off[n] = carry;
+  const int32_t x[1] = {c[0] + c[1] + c[2] + c[3]};
+  int32_t excl[1], total[1];
+  block_exclusive_scan_multi<256, 1>(x, excl, total, smem);
+  if (threadIdx.x < 64) {
+    const int32_t agg[1] = {total[0]};
+    int32_t ex[1];
+    tile_lookback_multi<1>(words, 0, tile, agg, ex);
+    if (threadIdx.x == 0) s_excl = ex[0];
+  }
+  __syncthreads();
+  int32_t o = s_excl + excl[0];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (i0 + j < n) {
+      off[i0 + j] = o;
+      pos[i0 + j] = o;
+    }
+    o += c[j];
+  }
+  if (tile == ntiles - 1 && threadIdx.x == 0) off[n] = s_excl + total[0];
 }
 
-// Thread per destination row v: every edge (v <- u) takes the next slot of
-// u and stores (v, 1/k_v) there.
+// Thread per edge slot: the edge (v <- u) takes the next place of u and
+// stores (v, 1/k_v) there.
 __global__ __launch_bounds__(256) void k_csc_fill(const int32_t* __restrict__ sizes, EdgeView ev,
                                                   int32_t* __restrict__ pos, const int32_t* __restrict__ off,
                                                   int2* __restrict__ csc) {
-  const int32_t n_dst = load_size(&sizes[kNDst]);
-  const int32_t n_src = load_size(&sizes[kNSrc]);
-  const int64_t v = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (v >= n_dst) return;
-  int32_t b, e;
-  edge_range(ev, v, b, e);
-  if (e <= b) return;
-  const int32_t inv = __float_as_int(1.f / static_cast<float>(e - b));
-  for (int32_t k = b; k < e; ++k) {
-    const int32_t u = ev.local[k];
-    if (u < 0 || u >= n_src) continue;
-    const int32_t slot = atomicAdd(&pos[u], 1);
-    if (slot < off[u + 1] && slot < ev.cap_nnz) csc[slot] = make_int2(static_cast<int32_t>(v), inv);
-  }
+  for_each_edge_slot(ev, load_size(&sizes[kNDst]), load_size(&sizes[kNSrc]),
+                     static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x,
+                     static_cast<int64_t>(gridDim.x) * blockDim.x, [&](int64_t v, int32_t u, int32_t k) {
+                       const int32_t slot = atomicAdd(&pos[u], 1);
+                       if (slot < off[u + 1] && slot < ev.cap_nnz)
+                         csc[slot] = make_int2(static_cast<int32_t>(v), __float_as_int(1.f / static_cast<float>(k)));
+                     });
 }
 
 // G lanes per source row u, lane c covers columns 4c, 4c + G, ... (d % 4 ==
@@ -596,17 +660,10 @@ int wgrad_parts(int64_t cap_rows, int d_in, int d_out) {
   return parts < 1 ? 1 : parts;
 }
 
-static int wgrad_rows_per_part(int64_t cap_rows, int parts) {
-  int64_t r = (cap_rows + parts - 1) / parts;
-  r = (r + 63) / 64 * 64;
-  return static_cast<int>(r < 64 ? 64 : r);
-}
-
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
                         int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
                         float* d_bias, hipStream_t s) {
   const int parts = wgrad_parts(cap_rows, d_in, d_out);
-  const int rpp = wgrad_rows_per_part(cap_rows, parts);
   const int ldp = wgrad_ldp(d_out);
   const dim3 grid(parts, (ldp + 63) / 64, 2 * ((d_in + 63) / 64));
   if (static_cast<uint64_t>(std::max<int64_t>(cap_rows, 1)) * std::max(d_in, ldz) * 4 >= (1ull << 32))
@@ -614,9 +671,9 @@ hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, in
   const bool vec = d_in % 4 == 0 && reinterpret_cast<uintptr_t>(H) % 16 == 0 &&
                    reinterpret_cast<uintptr_t>(M) % 16 == 0;
   if (vec)
-    hipLaunchKernelGGL(k_wgrad<true>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, rpp, partial);
+    hipLaunchKernelGGL(k_wgrad<true>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
   else
-    hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, rpp, partial);
+    hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
   const int64_t outs = static_cast<int64_t>(2 * d_in + 1) * (ldp / 4);
   hipLaunchKernelGGL(k_wgrad_reduce, dim3(static_cast<unsigned>((outs + 63) / 64)), dim3(256), 0, s, partial,
                      parts, d_in, d_out, ldp, d_self, d_neigh, d_bias);
@@ -625,7 +682,8 @@ hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, in
 
 hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_out, const float* ws,
                         const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
-                        const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t* cnt, hipStream_t s) {
+                        const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t fanout, int32_t* cnt,
+                        hipStream_t s) {
   const int nch = (d_out + 15) / 16;
   const int col_tiles = (2 * d_in + 63) / 64;
   int64_t rows = (cap_rows + 63) / 64;
@@ -633,7 +691,7 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
   if (rows > want) rows = want;
   if (rows < 1) rows = 1;
   const dim3 grid(static_cast<unsigned>(rows), col_tiles);
-  const EdgeView ev{indptr, local, cap_nnz};
+  const EdgeView ev{indptr, local, cap_nnz, fanout};
   const bool vec = d_out % 4 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0 &&
                    reinterpret_cast<uintptr_t>(wn) % 16 == 0;
 #define GMB_DGRAD(C)                                                                                          \
@@ -655,14 +713,17 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
   return hipGetLastError();
 }
 
+int64_t csc_scan_tiles(int64_t cap_src) { return std::max<int64_t>(1, (cap_src + kScanTile - 1) / kScanTile); }
+
 hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
-                                int64_t cap_nnz, const float* dM, const float* out, int d, float* dH,
+                                int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
-                                int2* csc, hipStream_t s) {
-  const EdgeView ev{indptr, local, cap_nnz};
-  hipLaunchKernelGGL(k_csc_scan, dim3(1), dim3(1024), 0, s, sizes, cnt, off, pos);
-  hipLaunchKernelGGL(k_csc_fill, dim3(grid_of(std::max<int64_t>(cap_dst, 1), 1 << 30)), dim3(256), 0, s, sizes,
-                     ev, pos, off, csc);
+                                uint32_t* scan_state, int2* csc, hipStream_t s) {
+  const EdgeView ev{indptr, local, cap_nnz, fanout};
+  hipLaunchKernelGGL(k_csc_scan, dim3(static_cast<unsigned>(csc_scan_tiles(cap_src))), dim3(256), 0, s, sizes, cnt,
+                     off, pos, scan_state, reinterpret_cast<uint64_t*>(scan_state + 2));
+  const int64_t slots = std::max<int64_t>(cap_dst, 1) * std::max(fanout, 1);
+  hipLaunchKernelGGL(k_csc_fill, dim3(grid_of(slots, 1 << 16)), dim3(256), 0, s, sizes, ev, pos, off, csc);
   const int chunks = d / 4;
   int G = 64;
   if (chunks <= 4) G = 4;
