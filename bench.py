@@ -62,6 +62,9 @@ def parse():
                     help="infer: sample + gather + forward (the default); train: the whole "
                          "training iteration, + loss, backward and SGD (fp32 workloads)")
     ap.add_argument("--lr", type=float, default=0.01, help="SGD step size of --mode train")
+    ap.add_argument("--fused", action="store_true",
+                    help="--mode train: the forward with the feature pull folded into layer 0 "
+                         "(only the destination rows gathered)")
     return ap.parse_args()
 
 
@@ -354,6 +357,7 @@ def main():
         lanes.append(dict(
             csr=c, ws_sample=ws_s,
             x=torch.empty((probe.input_capacity, cfg.feat_dim), dtype=feats.dtype, device=dev),
+            x_dst=torch.empty((gmb.dst_capacity(probe), cfg.feat_dim), dtype=feats.dtype, device=dev),
             ws_fwd=gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1],
             logits=torch.empty((cfg.batch, cfg.dims[-1]), dtype=torch.float32, device=dev)))
     torch.cuda.synchronize()
@@ -435,6 +439,31 @@ def main():
     for ln in lanes:
         ln["csr"].check_status()
 
+    # pass D: the fused path (sampling, then the forward that reads layer
+    # 0's neighbour rows from the feature table and gathers only the
+    # destination rows), S streams in flight, median of PASS_A_RUNS
+    def step_fused(i, nstreams):
+        b = i % nb
+        ln = lanes[i % nstreams]
+        with torch.cuda.stream(streams[i % nstreams]):
+            blocks = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b),
+                                       workspace=ln["ws_sample"])
+            gmb.sage_forward_fused(blocks, feats, weights, x_dst=ln["x_dst"], workspace=ln["ws_fwd"],
+                                   logits=ln["logits"][:batches[b].numel()])
+    for i in range(args.warmup):
+        step_fused(i, S)
+    runs_d = []
+    for _ in range(PASS_A_RUNS):
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        for i in range(K):
+            step_fused(i, S)
+        torch.cuda.synchronize()
+        runs_d.append(time.perf_counter() - t3)
+    T3 = sorted(runs_d)[len(runs_d) // 2]
+    for ln in lanes:
+        ln["csr"].check_status()
+
     # a plain device copy of known size: the bandwidth a streaming kernel
     # reaches on this GPU, and the calibration of the HBM byte counters
     src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
@@ -509,6 +538,10 @@ def main():
     res["forward"] = {"alg_bytes": b_fwd, "linear_flops": flops,
                       "linear_TFLOPs_lower_bound": flops / tf / 1e12, "mfma_peak_TFLOPs": peak}
     res["gemm_check"] = gemm_check(torch, dev)
+    res["fused_forward"] = {"seeds_per_s": seeds_total / T3, "ms_per_step": 1e3 * T3 / K,
+                            "runs_seeds_per_s": [seeds_total / t for t in runs_d], "streams": S,
+                            "what": "sample_blocks + sage_forward_fused (layer-0 mean from the feature "
+                                    "table, only block 0's destination rows gathered)"}
     # dominant kernel of the path: the feature gather, one launch per step,
     # timed in the isolated pass (the K launches after warm-up and pass A)
     res["roofline"] = {"kernel": "k_gather", "bound": "hbm",
@@ -559,8 +592,9 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         c = csr if k == 0 else gmb.CSRGraph(ip, ix)
         ws_s = gmb._aligned_bytes(gmb.sample_workspace_bytes(cfg.batch, fanouts, g.num_nodes), dev)[1]
         probe = gmb.sample_blocks(c, batches[0], fanouts, wl.batch_key(0), workspace=ws_s)
+        rows = gmb.dst_capacity(probe) if args.fused else probe.input_capacity
         lanes.append(dict(csr=c, ws_sample=ws_s, stream=torch.cuda.Stream(),
-                          x=torch.empty((probe.input_capacity, cfg.feat_dim), dtype=feats.dtype, device=dev),
+                          x=torch.empty((rows, cfg.feat_dim), dtype=feats.dtype, device=dev),
                           ready=torch.cuda.Event(), done=torch.cuda.Event()))
     ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1]
     ws_bwd = gmb._aligned_bytes(gmb.backward_workspace_bytes(probe, weights), dev)[1]
@@ -570,8 +604,14 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
     losses = torch.zeros(W + 2 * K, dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
 
+    def forward(blocks, x, b):
+        if args.fused:   # x: the destination rows, gathered by the forward itself
+            return gmb.sage_forward_fused(blocks, feats, weights, x_dst=x, workspace=ws_fwd,
+                                          logits=logits[:batches[b].numel()])[0]
+        return gmb.sage_forward(blocks, x, weights, workspace=ws_fwd, logits=logits[:batches[b].numel()])
+
     def model(blocks, x, b, i):
-        lg = gmb.sage_forward(blocks, x, weights, workspace=ws_fwd, logits=logits[:batches[b].numel()])
+        lg = forward(blocks, x, b)
         gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
                           workspace=ws_bwd)
         gmb.sgd_update(weights, grads, args.lr)
@@ -583,7 +623,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         with torch.cuda.stream(st):
             st.wait_event(ln["done"])
             blocks = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b), workspace=ln["ws_sample"])
-            x = gmb.gather_features(blocks, feats, out=ln["x"])
+            x = ln["x"] if args.fused else gmb.gather_features(blocks, feats, out=ln["x"])
             ln["ready"].record(st)
         comp.wait_event(ln["ready"])
         model(blocks, x, b, i)
@@ -619,9 +659,9 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         e[0].record(comp)
         blocks = gmb.sample_blocks(ln0["csr"], batches[b], fanouts, wl.batch_key(b), workspace=ln0["ws_sample"])
         e[1].record(comp)
-        x = gmb.gather_features(blocks, feats, out=ln0["x"])
+        x = ln0["x"] if args.fused else gmb.gather_features(blocks, feats, out=ln0["x"])
         e[2].record(comp)
-        lg = gmb.sage_forward(blocks, x, weights, workspace=ws_fwd, logits=logits[:batches[b].numel()])
+        lg = forward(blocks, x, b)
         e[3].record(comp)
         gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
                           workspace=ws_bwd)
@@ -649,7 +689,8 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         bwd_flops += backward_flops(sizes, cfg.dims)
     tf, tb = stage["forward"] / 1e3, stage["backward"] / 1e3
     res = {
-        "metric": "seeds/s of the training iteration (sample+gather+SAGE fwd+loss+bwd+SGD)",
+        "metric": "seeds/s of the training iteration (sample+gather+SAGE fwd+loss+bwd+SGD)"
+                  + (", gather folded into the forward" if args.fused else ""),
         "value": seeds_total / T,
         "unit": "seeds/s",
         "n_gpus": 1, "steps": K, "warmup": W,
@@ -660,7 +701,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
                                f"x{cfg.feat_dim}, SAGE {'-'.join(map(str, cfg.dims))}, fanouts {fanouts}, batch "
                                f"{cfg.batch}, {nb} batches per epoch, SGD lr {args.lr}",
                    "batch": cfg.batch, "fanouts": fanouts, "dims": list(cfg.dims), "batches_per_epoch": nb,
-                   "mode": "train"},
+                   "mode": "train", "fused": bool(args.fused)},
         "epoch_s": nb * T / K,
         "pass_a_runs_seeds_per_s": [seeds_total / t for t in runs],
         "sampled_edges_per_s": edges_total / T,
@@ -671,16 +712,20 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         "backward_products_TFLOPs_lower_bound": bwd_flops / tb / 1e12,
         "mfma_peak_TFLOPs": FP32_MFMA_PEAK_TFLOPS,
         "gemm_check": gemm_check(torch, dev),
-        "gather_GBps": b_gather / (stage["gather"] / 1e3) / 1e9,
+        "gather_GBps": None if args.fused else b_gather / (stage["gather"] / 1e3) / 1e9,
         "loss": {"first": float(loss_h[0]), "last_of_pass_A": float(loss_h[W + K - 1]),
                  "last": float(loss_h[-1])},
         "datagen_s": t_gen,
     }
     # the gather is the one kernel of the iteration bracketed alone by events
-    res["roofline"] = {"kernel": "k_gather", "bound": "hbm", "achieved": res["gather_GBps"],
-                       "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": res["gather_GBps"] / HBM_PEAK_GBPS,
-                       "traffic": None, "alg_bytes_per_launch": b_gather / K,
-                       "avg_launch_ms": stage["gather"] / K}
+    # (in the fused form it runs inside the forward stage: no line)
+    if not args.fused:
+        res["roofline"] = {"kernel": "k_gather", "bound": "hbm", "achieved": res["gather_GBps"],
+                           "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": res["gather_GBps"] / HBM_PEAK_GBPS,
+                           "traffic": None, "alg_bytes_per_launch": b_gather / K,
+                           "avg_launch_ms": stage["gather"] / K}
+    else:
+        del res["gather_GBps"]   # no gather stage of its own
     if args.cpu_batches > 0:
         res["cpu_baseline"] = cpu_baseline_train(args, wl, fanouts)
     print(json.dumps(res), flush=True)

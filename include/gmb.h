@@ -227,6 +227,28 @@ int64_t gmb_forward_hidden_offset(const gmb_blocks* blocks, const gmb_sage_weigh
 int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
                      float* logits, void* ws, size_t ws_bytes, void* stream);
 
+/* The forward of gmb_sage_forward with the feature pull of Section III-C
+ * folded into layer 0: instead of a gathered copy of every input row, the
+ * layer-0 mean reads the sampled neighbours' rows straight from the feature
+ * table by their global ids (block 0's nbr array), and only block 0's
+ * destination rows, which its linear term h_v W_self needs, are gathered
+ * into x_dst.  The results are bit for bit those of gmb_sage_forward on
+ * the same blocks and weights (the same rows are summed in the same order).
+ *   feats      device [num_nodes, dims[0]] in weights->dtype, read-only.
+ *   num_nodes  rows of feats (1 .. 2^31 - 1).
+ *   x_dst      device [blocks->blk[0].cap_dst, dims[0]] in weights->dtype,
+ *              caller-owned, written with the destination rows; it stands
+ *              for `x` in a later gmb_sage_backward (which reads layer 0's
+ *              destination rows only).
+ *   status     NULL or the sampler state's status word
+ *              (gmb_state_status_word): an id outside [0, num_nodes) in
+ *              the gather sets GMB_STATUS_ERANGE there and gives a zero row;
+ *              in the mean it is read as row 0.
+ *   others     as for gmb_sage_forward (same workspace size). */
+int gmb_sage_forward_fused(const gmb_blocks* blocks, const void* feats, int64_t num_nodes, void* x_dst,
+                           const gmb_sage_weights* weights, float* logits, void* ws, size_t ws_bytes,
+                           uint32_t* status, void* stream);
+
 /* ---- training step (the trainer's iteration of Section III-E) ---------- */
 
 /* Gradient arrays of an L-layer model, one per weight array, fp32 and laid

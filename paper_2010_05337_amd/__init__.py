@@ -31,7 +31,7 @@ EXPORTS = (
     "gmb_abi_version", "gmb_last_error", "gmb_sampler_state_bytes", "gmb_sampler_state_init",
     "gmb_state_status_word", "gmb_read_status", "gmb_sample_workspace_bytes", "gmb_sample_blocks",
     "gmb_read_sizes", "gmb_gather_features", "gmb_forward_workspace_bytes",
-    "gmb_forward_hidden_offset", "gmb_sage_forward", "gmb_backward_workspace_bytes",
+    "gmb_forward_hidden_offset", "gmb_sage_forward", "gmb_sage_forward_fused", "gmb_backward_workspace_bytes",
     "gmb_sage_backward", "gmb_sgd_update",
 )
 
@@ -116,6 +116,9 @@ def lib() -> ctypes.CDLL:
         L.gmb_sage_forward.restype = ctypes.c_int
         L.gmb_sage_forward.argtypes = [ctypes.POINTER(BlocksStruct), vp, ctypes.POINTER(WeightsStruct),
                                        vp, vp, sz, vp]
+        L.gmb_sage_forward_fused.restype = ctypes.c_int
+        L.gmb_sage_forward_fused.argtypes = [ctypes.POINTER(BlocksStruct), vp, ctypes.c_int64, vp,
+                                             ctypes.POINTER(WeightsStruct), vp, vp, sz, vp, vp]
         L.gmb_backward_workspace_bytes.restype = sz
         L.gmb_backward_workspace_bytes.argtypes = [ctypes.POINTER(BlocksStruct),
                                                    ctypes.POINTER(WeightsStruct)]
@@ -384,6 +387,10 @@ def sage_forward(blocks: Blocks, feats: torch.Tensor, weights: SageWeights,
                                   _stream_handle()))
     if not return_hidden:
         return logits
+    return logits, _hidden_views(blocks, weights, workspace)
+
+
+def _hidden_views(blocks: Blocks, weights: SageWeights, workspace: torch.Tensor):
     hidden = []
     sizes = blocks.sizes()
     es = 2 if weights.dtype == GMB_BF16 else 4
@@ -393,7 +400,48 @@ def sage_forward(blocks: Blocks, feats: torch.Tensor, weights: SageWeights,
         d = weights.dims[l + 1]
         h = workspace[off:off + n * d * es].view(weights.torch_dtype).view(n, d)
         hidden.append(h)
-    return logits, hidden
+    return hidden
+
+
+def dst_capacity(blocks: Blocks) -> int:
+    """Rows of block 0's destinations (the x_dst buffer of the fused forward)."""
+    return int(blocks.struct.blk[0].cap_dst)
+
+
+def sage_forward_fused(blocks: Blocks, feats: torch.Tensor, weights: SageWeights,
+                       x_dst: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                       logits: torch.Tensor | None = None, return_hidden: bool = False):
+    """The forward with the feature pull folded into layer 0: `feats` is the
+    whole feature table [num_nodes, dims[0]]; block 0's destination rows are
+    gathered into x_dst ([dst capacity, dims[0]]), the layer-0 mean reads
+    the table directly.  Returns (logits, x_dst) (and the hidden
+    activations with return_hidden); x_dst serves as `x` of sage_backward."""
+    _require_cuda(feats, "feats")
+    if feats.dtype != weights.torch_dtype:
+        raise TypeError("feats and weights must have the same dtype")
+    if feats.dim() != 2 or feats.shape[1] != weights.dims[0]:
+        raise ValueError("feats must be [num_nodes, dims[0]]")
+    need = lib().gmb_forward_workspace_bytes(ctypes.byref(blocks.struct), ctypes.byref(weights.struct))
+    if need == 0:
+        _check(-1)
+    if workspace is None or workspace.numel() < need or workspace.data_ptr() % 256:
+        _, workspace = _aligned_bytes(need, feats.device)
+    if x_dst is None:
+        x_dst = torch.empty((dst_capacity(blocks), weights.dims[0]), dtype=feats.dtype, device=feats.device)
+    if x_dst.dtype != feats.dtype or x_dst.dim() != 2 or x_dst.shape[1] != weights.dims[0] or \
+            x_dst.shape[0] < dst_capacity(blocks) or not x_dst.is_contiguous():
+        raise ValueError("x_dst must be a contiguous [dst capacity, dims[0]] tensor of the features' dtype")
+    B, C = blocks.num_seeds, weights.dims[-1]
+    if logits is None:
+        logits = torch.empty((max(B, 0), C), dtype=torch.float32, device=feats.device)
+    _check(lib().gmb_sage_forward_fused(ctypes.byref(blocks.struct), ctypes.c_void_p(feats.data_ptr()),
+                                        feats.shape[0], ctypes.c_void_p(x_dst.data_ptr()),
+                                        ctypes.byref(weights.struct), ctypes.c_void_p(logits.data_ptr()),
+                                        ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                        ctypes.c_void_p(blocks.csr.status_word), _stream_handle()))
+    if not return_hidden:
+        return logits, x_dst
+    return logits, x_dst, _hidden_views(blocks, weights, workspace)
 
 
 # ---------------------------------------------------------------- training

@@ -181,6 +181,48 @@ int plan_forward(const gmb_blocks* b, const gmb_sage_weights* w, ForwardPlan* pl
   return GMB_OK;
 }
 
+int check_forward(const gmb_blocks* blocks, const gmb_sage_weights* weights, const float* logits, const void* ws,
+                  size_t ws_bytes, ForwardPlan* p) {
+  int st = plan_forward(blocks, weights, p);
+  if (st != GMB_OK) return st;
+  if (!logits) return fail(GMB_EINVAL, "logits is NULL");
+  if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(GMB_EINVAL, "workspace is not 256-byte aligned");
+  if (ws_bytes < p->total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p->total);
+  return GMB_OK;
+}
+
+// The layers in order.  Layer 0's linear reads its destination rows from
+// x_self; its mean reads the rows mean_rows[mean_ids[e]] (the gathered
+// input and the local ids, or the feature table and the global ids).
+int run_forward(const gmb_blocks* blocks, const void* x_self, const int32_t* mean_ids, const void* mean_rows,
+                int64_t mean_max_id, const gmb_sage_weights* weights, float* logits, const ForwardPlan& p,
+                void* ws, hipStream_t s) {
+  const int L = weights->num_layers;
+  const int bf16 = weights->dtype == GMB_BF16;
+  char* base = static_cast<char*>(ws);
+  const void* h_in = x_self;
+  for (int l = 0; l < L; ++l) {
+    const gmb_block& bk = blocks->blk[l];
+    void* agg = base + p.off_agg[l];
+    const int d_in = weights->dims[l], d_out = weights->dims[l + 1];
+    const bool last = (l == L - 1);
+    void* h_out = last ? static_cast<void*>(logits) : static_cast<void*>(base + p.off_hidden[l]);
+    const int32_t* ids = l == 0 ? mean_ids : bk.indices;
+    const void* rows = l == 0 ? mean_rows : h_in;
+    const int64_t max_id = l == 0 ? mean_max_id : std::max<int64_t>(bk.cap_src, 1);
+    hipError_t e = gmb::launch_mean_aggregate(bk.sizes, bk.indptr, ids, rows, d_in, bf16, agg, bk.cap_dst,
+                                              bk.fanout, max_id, s);
+    if (e != hipSuccess) return hip_fail(e, "mean-aggregation launch");
+    e = gmb::launch_sage_linear(bk.sizes, h_in, agg, weights->w_self[l], weights->w_neigh[l],
+                                weights->bias[l], d_in, d_out, bf16, last ? 0 : 1,
+                                (last || !bf16) ? 1 : 0, h_out, bk.cap_dst, s);
+    if (e != hipSuccess) return hip_fail(e, "linear launch");
+    h_in = h_out;
+  }
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -397,33 +439,31 @@ int64_t gmb_forward_hidden_offset(const gmb_blocks* blocks, const gmb_sage_weigh
 int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
                      float* logits, void* ws, size_t ws_bytes, void* stream) {
   ForwardPlan p;
-  int st = plan_forward(blocks, weights, &p);
+  int st = check_forward(blocks, weights, logits, ws, ws_bytes, &p);
   if (st != GMB_OK) return st;
-  if (!x || !logits) return fail(GMB_EINVAL, "x or logits is NULL");
-  if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(GMB_EINVAL, "workspace is not 256-byte aligned");
-  if (ws_bytes < p.total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p.total);
+  if (!x) return fail(GMB_EINVAL, "x is NULL");
+  const gmb_block& b0 = blocks->blk[0];
+  return run_forward(blocks, x, b0.indices, x, std::max<int64_t>(b0.cap_src, 1), weights, logits, p, ws,
+                     as_stream(stream));
+}
+
+int gmb_sage_forward_fused(const gmb_blocks* blocks, const void* feats, int64_t num_nodes, void* x_dst,
+                           const gmb_sage_weights* weights, float* logits, void* ws, size_t ws_bytes,
+                           uint32_t* status, void* stream) {
+  ForwardPlan p;
+  int st = check_forward(blocks, weights, logits, ws, ws_bytes, &p);
+  if (st != GMB_OK) return st;
+  if (!feats || !x_dst) return fail(GMB_EINVAL, "feats or x_dst is NULL");
+  if (num_nodes < 1 || num_nodes > kMaxInt32)
+    return fail(GMB_EINVAL, "num_nodes=%lld outside 1..2^31-1", static_cast<long long>(num_nodes));
   const hipStream_t s = as_stream(stream);
-  const int L = weights->num_layers;
-  const int bf16 = weights->dtype == GMB_BF16;
-  char* base = static_cast<char*>(ws);
-  const void* h_in = x;
-  for (int l = 0; l < L; ++l) {
-    const gmb_block& bk = blocks->blk[l];
-    void* agg = base + p.off_agg[l];
-    const int d_in = weights->dims[l], d_out = weights->dims[l + 1];
-    const bool last = (l == L - 1);
-    void* h_out = last ? static_cast<void*>(logits) : static_cast<void*>(base + p.off_hidden[l]);
-    hipError_t e = gmb::launch_mean_aggregate(bk.sizes, bk.indptr, bk.indices, h_in, d_in, bf16, agg,
-                                              bk.cap_dst, bk.fanout, s);
-    if (e != hipSuccess) return hip_fail(e, "mean-aggregation launch");
-    e = gmb::launch_sage_linear(bk.sizes, h_in, agg, weights->w_self[l], weights->w_neigh[l],
-                                weights->bias[l], d_in, d_out, bf16, last ? 0 : 1,
-                                (last || !bf16) ? 1 : 0, h_out, bk.cap_dst, s);
-    if (e != hipSuccess) return hip_fail(e, "linear launch");
-    h_in = h_out;
-  }
-  return ok();
+  const gmb_block& b0 = blocks->blk[0];
+  const int64_t row_bytes = static_cast<int64_t>(weights->dims[0]) * (weights->dtype == GMB_BF16 ? 2 : 4);
+  // block 0's destinations are the first n_dst source ids
+  hipError_t e = gmb::launch_gather(b0.src_ids, b0.sizes + gmb::kNDst, b0.cap_dst, feats, num_nodes, row_bytes,
+                                    x_dst, status, s);
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return run_forward(blocks, x_dst, b0.nbr, feats, num_nodes, weights, logits, p, ws, s);
 }
 
 }  // extern "C"

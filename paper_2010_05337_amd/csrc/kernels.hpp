@@ -109,10 +109,11 @@ hipError_t launch_gather(const int32_t* ids, const int32_t* n_dev, int64_t n_cap
                          int64_t num_nodes, int64_t row_bytes, void* out, uint32_t* status,
                          hipStream_t s);
 
-// sage.hip
+// sage.hip.  The mean reads rows H[ids[e]] with ids in [0, max_id)
+// (others are read as row 0).
 hipError_t launch_mean_aggregate(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                  const void* h, int d, int bf16, void* agg, int64_t cap_dst,
-                                 int fanout, hipStream_t s);
+                                 int fanout, int64_t max_id, hipStream_t s);
 hipError_t launch_sage_linear(const int32_t* sizes, const void* h_self, const void* agg,
                               const void* w_self, const void* w_neigh, const float* bias, int d_in,
                               int d_out, int bf16, int relu, int out_f32, void* out,

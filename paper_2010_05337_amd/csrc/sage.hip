@@ -2,7 +2,9 @@
 // message f = h_u, the aggregator = mean over the sampled in-neighbours and
 // the update g = act(h_v W_self + m_v W_neigh + b); Section IV model).
 //
-//   k_mean    m_v = (1/k_v) sum_e H[local[e]], fp32 accumulation; a group of
+//   k_mean    m_v = (1/k_v) sum_e H[ids[e]] (ids: the block's local ids into the
+//             layer input, or for a layer 0 that reads the feature table,
+//             the edges' global ids), fp32 accumulation; a group of
 //             G lanes per destination row, 16-byte chunks of the feature
 //             row per lane; the group reads the row's local ids in one
 //             access and then up to U neighbour rows in one batch.
@@ -99,7 +101,7 @@ template <typename T, int VEC, int G, int U>
 __global__ __launch_bounds__(256) void k_mean(const int32_t* sizes, const int32_t* __restrict__ indptr,
                                               const int32_t* __restrict__ local,
                                               const T* __restrict__ H, int d, T* __restrict__ M,
-                                              int64_t cap_rows) {
+                                              int64_t cap_rows, int64_t max_id) {
   const int64_t row = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
   const int lane = threadIdx.x & (G - 1);
   // independent first reads, the row offsets first (the compiler keeps
@@ -118,14 +120,15 @@ __global__ __launch_bounds__(256) void k_mean(const int32_t* sizes, const int32_
     float acc[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
-    // the group reads G local ids at once (lane i: edge base + i), then
+    // the group reads G row ids at once (lane i: edge base + i), then
     // its rows U at a time (U >= the fan-out where possible, so one batch
     // per row) with every read unconditional; past the row's end a slot
-    // re-reads the first id and is dropped.  A negative local id only
-    // exists after a data error; it is read as row 0.
+    // re-reads the first id and is dropped.  An id outside [0, max_id)
+    // only exists after a data error; it is read as row 0.
     for (int32_t base = 0; base < k; base += G) {
       const int32_t n_here = k - base < G ? k - base : G;
-      const int32_t mine = max(local[beg + base + (lane < n_here ? lane : 0)], 0);
+      int32_t mine = local[beg + base + (lane < n_here ? lane : 0)];
+      mine = (mine < 0 || mine >= max_id) ? 0 : mine;
       for (int u0 = 0; u0 < n_here; u0 += U) {
         int32_t id[U];
 #pragma unroll
@@ -157,7 +160,7 @@ __global__ __launch_bounds__(256) void k_mean(const int32_t* sizes, const int32_
 
 template <typename T, int VEC>
 hipError_t mean_dispatch(const int32_t* sizes, const int32_t* indptr, const int32_t* local, const void* h,
-                         int d, void* m, int64_t cap_dst, int fanout, hipStream_t s) {
+                         int d, void* m, int64_t cap_dst, int fanout, int64_t max_id, hipStream_t s) {
   const int chunks = d / VEC;
   int G = 64;
   if (chunks <= 4) G = 4;
@@ -174,7 +177,7 @@ hipError_t mean_dispatch(const int32_t* sizes, const int32_t* indptr, const int3
   T* M = static_cast<T*>(m);
   const int64_t cap = cap_dst < 1 ? 1 : cap_dst;   // indptr holds cap_dst + 1 >= 1 entries
 #define GMB_MEAN(GG, UU) \
-  hipLaunchKernelGGL((k_mean<T, VEC, GG, UU>), grid, block, 0, s, sizes, indptr, local, H, d, M, cap)
+  hipLaunchKernelGGL((k_mean<T, VEC, GG, UU>), grid, block, 0, s, sizes, indptr, local, H, d, M, cap, max_id)
 #define GMB_MEAN_G(UU)                \
   switch (G) {                        \
     case 4: GMB_MEAN(4, UU); break;   \
@@ -825,16 +828,16 @@ void launch_bf16_slab(const int32_t* sizes, const uint16_t* hs, const uint16_t* 
 
 hipError_t launch_mean_aggregate(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                  const void* h, int d, int bf16, void* agg, int64_t cap_dst,
-                                 int fanout, hipStream_t s) {
+                                 int fanout, int64_t max_id, hipStream_t s) {
   const uintptr_t align = reinterpret_cast<uintptr_t>(h) | reinterpret_cast<uintptr_t>(agg);
   if (bf16) {
     if (d % 8 == 0 && align % 16 == 0)
-      return mean_dispatch<uint16_t, 8>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
-    return mean_dispatch<uint16_t, 1>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
+      return mean_dispatch<uint16_t, 8>(sizes, indptr, local, h, d, agg, cap_dst, fanout, max_id, s);
+    return mean_dispatch<uint16_t, 1>(sizes, indptr, local, h, d, agg, cap_dst, fanout, max_id, s);
   }
   if (d % 4 == 0 && align % 16 == 0)
-    return mean_dispatch<float, 4>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
-  return mean_dispatch<float, 1>(sizes, indptr, local, h, d, agg, cap_dst, fanout, s);
+    return mean_dispatch<float, 4>(sizes, indptr, local, h, d, agg, cap_dst, fanout, max_id, s);
+  return mean_dispatch<float, 1>(sizes, indptr, local, h, d, agg, cap_dst, fanout, max_id, s);
 }
 
 hipError_t launch_sage_linear(const int32_t* sizes, const void* h_self, const void* agg,

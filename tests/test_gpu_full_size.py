@@ -209,3 +209,27 @@ def test_full_size_training_step(orc, dg, setup):
     out = dict(hidden=hidden, grads=grads, loss=float(loss.item()), before=before)
     compare_train_step(orc, out, ref, X, w, labels, lr, wt, exact_hidden=False)
     csr.check_status()
+
+
+def test_full_size_fused_forward(setup):
+    """The fused forward (layer-0 mean straight from the feature table, only
+    the destination rows gathered) against the three-call path, bit for
+    bit, on the first and last batch, in bench.py's buffers."""
+    wl, csr, feats, weights, _, _ = setup
+    lane = Lane(csr, wl, feats, weights)
+    nb = len(wl.batches)
+    for b in sorted({0, nb - 1}):
+        blocks, x, logits, hidden = lane.run(wl, feats, weights, b)
+        lg = logits.clone()
+        hid = [h.clone() for h in hidden]
+        n_dst0 = blocks.sizes()[0][0]
+        x_dst = torch.empty((gmb.dst_capacity(blocks), wl.cfg.feat_dim), dtype=feats.dtype, device="cuda")
+        logits2, x_dst, hidden2 = gmb.sage_forward_fused(blocks, feats, weights, x_dst=x_dst,
+                                                         workspace=lane.ws_fwd, return_hidden=True)
+        bits = (lambda t: t.view(torch.int16)) if feats.dtype == torch.bfloat16 else (lambda t: t.view(torch.int32))
+        assert torch.equal(bits(x_dst[:n_dst0]), bits(x[:n_dst0])), f"batch {b} x_dst"
+        assert torch.equal(logits2, lg), f"batch {b} logits"
+        for l, (h1, h2) in enumerate(zip(hid, hidden2)):
+            assert torch.equal(bits(h1), bits(h2)), f"batch {b} hidden {l}"
+        print(f"{wl.cfg.name}: batch {b}: fused forward equal to the three-call path", flush=True)
+    csr.check_status()

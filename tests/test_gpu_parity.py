@@ -233,3 +233,56 @@ def test_forward_more_shapes_f32(orc, dg, tiny, dims, fanouts):
     w = dg.sage_weights(dims, 32)
     seeds = dg.permutation(10000, 33)[:150]
     _forward_case(orc, dg, tiny, feats, w, seeds, fanouts, 34, TOL_F32)
+
+
+# ---- the forward with the feature pull folded into layer 0 -----------------
+
+def _fused_case(orc, dg, g, feats, w, seeds, fanouts, key, tol):
+    """The fused forward against the three-call path on the same blocks: the
+    logits and every hidden layer bit for bit, x_dst = the gathered rows of
+    block 0's destinations bit for bit; and the logits against the oracle."""
+    csr = csr_on_device(g)
+    ft = to_torch_feats(feats)
+    wt = to_torch_weights(w)
+    blocks, host = gpu_blocks(csr, seeds, fanouts, key)
+    x = gmb.gather_features(blocks, ft)
+    logits, hidden = gmb.sage_forward(blocks, x, wt, return_hidden=True)
+    logits2, x_dst, hidden2 = gmb.sage_forward_fused(blocks, ft, wt, return_hidden=True)
+    csr.check_status()
+    n_dst0 = host[0]["n_dst"]
+    assert torch.equal(tensor_bits_t(x_dst[:n_dst0]), tensor_bits_t(x[:n_dst0])), "x_dst"
+    assert torch.equal(logits, logits2), "logits"
+    for l, (h1, h2) in enumerate(zip(hidden, hidden2)):
+        assert torch.equal(tensor_bits_t(h1), tensor_bits_t(h2)), f"hidden layer {l}"
+    ref_blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, key)
+    X = orc.widen(orc.gather(feats, ref_blocks[0].src), w.dtype)
+    ws, wn, bs = w.as_f64()
+    ref_logits, _ = orc.sage_forward(ref_blocks, X, ws, wn, bs)
+    err = rowwise_rel_err(tensor_f64(logits2), ref_logits)
+    print(f"fused forward: equal to the three-call path; logits rel. error {err:.2e}", flush=True)
+    assert err <= tol
+
+
+def tensor_bits_t(t):
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+@pytest.mark.parametrize("dims,fanouts,dtype", [([16, 16, 8], [5, 5], "f32"), ([10, 12, 7], [8, 4], "f32"),
+                                                ([64, 256, 47], [10, 4], "bf16"), ([12, 40, 5], [3, 6], "bf16"),
+                                                ([128, 64, 40, 3], [3, 2, 5], "f32")])
+def test_forward_fused_equals_three_calls(orc, dg, tiny, dims, fanouts, dtype):
+    feats = dg.features(10000, dims[0], 51, dtype)
+    w = dg.sage_weights(dims, 52, dtype)
+    seeds = dg.permutation(10000, 53)[:200]
+    _fused_case(orc, dg, tiny, feats, w, seeds, fanouts, 54, TOL_F32 if dtype == "f32" else TOL_BF16)
+
+
+def test_forward_fused_hubs(orc, dg):
+    """The 100k-degree hub graph shape on the fused path (bf16 x128, fan-outs
+    25/10): hubs as seeds among ordinary vertices."""
+    g = dg.inject_hubs(dg.er_directed(20000, 8.0, 61), 5, 3000, 62)
+    feats = dg.features(20000, 128, 63, "bf16")
+    w = dg.sage_weights([128, 256, 47], 64, "bf16")
+    seeds = np.concatenate([np.asarray(g.hubs, np.int32),
+                            dg.permutation(20000, 65)[:300][~np.isin(dg.permutation(20000, 65)[:300], g.hubs)]])
+    _fused_case(orc, dg, g, feats, w, seeds.astype(np.int32), [25, 10], 66, TOL_BF16)

@@ -184,3 +184,31 @@ def test_backward_rejects_unsupported_models(dg):
         assert gmb.backward_workspace_bytes(blocks, wt) == 0
         with pytest.raises(gmb.GmbError):
             gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd)
+
+
+def test_train_step_on_fused_forward(orc, dg):
+    """The training step fed by the fused forward: x_dst (block 0's
+    destination rows) stands for the gathered input in the backward."""
+    n, dims, fanouts, n_seeds = 3000, [24, 32, 32, 6], [4, 2, 8], 90
+    g = exact_graph(n, 71)
+    feats, w = exact_model(dg, n, dims, 72)
+    seeds = dg.permutation(n, 73)[:n_seeds]
+    labels = dg.labels(n, dims[-1], 74)[seeds]
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    ft = torch.from_numpy(feats).cuda()
+    blocks, host = gpu_blocks(csr, seeds, fanouts, 75)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+    logits, x_dst, hidden = gmb.sage_forward_fused(blocks, ft, wt, workspace=ws_fwd, return_hidden=True)
+    y = torch.from_numpy(labels).cuda()
+    grads, loss = gmb.sage_backward(blocks, x_dst, wt, logits, y, ws_fwd)
+    before = [[t.clone() for t in arrs] for arrs in (wt.w_self, wt.w_neigh, wt.bias)]
+    gmb.sgd_update(wt, grads, 0.25)
+    torch.cuda.synchronize()
+    ref_blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, 75)
+    assert_blocks_equal(host, ref_blocks)
+    X = orc.gather(feats, ref_blocks[0].src).astype(np.float64)
+    assert_hidden_exact(orc, ref_blocks, X, w)
+    out = dict(hidden=hidden, grads=grads, loss=float(loss.item()), before=before)
+    compare_train_step(orc, out, ref_blocks, X, w, labels, 0.25, wt, exact_hidden=True)
+    csr.check_status()
