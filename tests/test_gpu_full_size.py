@@ -233,3 +233,50 @@ def test_full_size_fused_forward(setup):
             assert torch.equal(bits(h1), bits(h2)), f"batch {b} hidden {l}"
         print(f"{wl.cfg.name}: batch {b}: fused forward equal to the three-call path", flush=True)
     csr.check_status()
+
+
+def test_every_batch_of_the_epoch(orc, setup):
+    """Sampling, relabel and gather of every batch of the epoch bit for bit,
+    and the forward of the first 16 batches within the tolerance, against
+    the oracle run on host threads (its C calls release the interpreter
+    lock; at most 32 batches in flight)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+
+    wl, csr, feats, weights, _, _ = setup
+    cfg, g = wl.cfg, wl.graph
+    lane = Lane(csr, wl, feats, weights)
+    nb = len(wl.batches)
+    n_fwd = min(16, nb)
+    ws, wn, bs = wl.weights.as_f64()
+    orc.lib()
+
+    def oracle_batch(b):
+        ref = orc.sample_blocks(g.indptr, g.indices, wl.batches[b], list(cfg.fanouts), wl.batch_key(b))
+        X = orc.gather(wl.feats, ref[0].src)
+        logits = orc.sage_forward(ref, orc.widen(X, cfg.feat_dtype), ws, wn, bs)[0] if b < n_fwd else None
+        return ref, X, logits
+
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    worst = 0.0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        futs = {}
+        for b in range(min(32, nb)):
+            futs[b] = ex.submit(oracle_batch, b)
+        for b in range(nb):
+            blocks, x, logits, _ = lane.run(wl, feats, weights, b)
+            host = host_blocks(blocks)
+            ref, X, ref_logits = futs.pop(b).result()
+            if b + 32 < nb:
+                futs[b + 32] = ex.submit(oracle_batch, b + 32)
+            assert_blocks_equal(host, ref, f"{cfg.name} batch {b}")
+            got = tensor_bits(x)[:ref[0].n_src]
+            assert got.view(np.uint8).tobytes() == X.view(np.uint8).tobytes(), f"batch {b}: gathered rows differ"
+            if ref_logits is not None:
+                e = rowwise_rel_err(tensor_f64(logits), ref_logits)
+                worst = max(worst, e)
+                assert e <= TOL[cfg.feat_dtype], (b, e)
+            del ref, X
+    csr.check_status()
+    print(f"{cfg.name}: {nb} batches bit-exact (sampling, relabel, gather); forward of the first {n_fwd}: "
+          f"max rel. error {worst:.2e}", flush=True)
