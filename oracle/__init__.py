@@ -24,7 +24,12 @@ Parity status per function:
   softmax_xent,     pinned: central finite differences of the loss in every
   sage_backward     parameter (fp64), and the full-neighbourhood special
                     case == torch autograd (fp64, CPU) of the dense
-                    full-graph model
+                    full-graph model; its input-row gradient likewise
+                    (finite differences in every input entry, autograd of
+                    the dense model in the feature matrix)
+  embedding_sgd     pinned: rows outside the batch unchanged bit for bit,
+                    the touched rows against the formula, repeated rows
+                    refused; a small step lowers the loss
 """
 from __future__ import annotations
 
@@ -269,11 +274,12 @@ def sage_forward_train(blocks, X: np.ndarray, w_self, w_neigh, bias):
     return H, outs, means
 
 
-def sage_backward(blocks, X: np.ndarray, w_self, w_neigh, hidden, means, dlogits):
+def sage_backward(blocks, X: np.ndarray, w_self, w_neigh, hidden, means, dlogits, input_grad: bool = False):
     """Gradients of the loss in every parameter, from dL/dlogits back to
-    layer 0 (the input features are not trained).  hidden and means come
-    from sage_forward_train.  Returns (dW_self, dW_neigh, db), lists by
-    layer."""
+    layer 0.  hidden and means come from sage_forward_train.  Returns
+    (dW_self, dW_neigh, db), lists by layer; with input_grad also dX, the
+    gradient in the layer-0 input rows X [n_src(0), D] (the input has no
+    activation, so nothing masks it)."""
     L = len(blocks)
     dWs, dWn, dbs = [None] * L, [None] * L, [None] * L
     dOut = np.ascontiguousarray(dlogits, dtype=np.float64)
@@ -296,7 +302,7 @@ def sage_backward(blocks, X: np.ndarray, w_self, w_neigh, hidden, means, dlogits
         dbs[l] = np.zeros(d_out)
         Hd = np.ascontiguousarray(Hin[:n])
         m = np.ascontiguousarray(means[l], dtype=np.float64)
-        if l > 0:
+        if l > 0 or input_grad:
             dH = np.zeros((blk.n_src, d_in))
             dM = np.zeros((n, d_in))
             dHd = np.zeros((n, d_in))
@@ -308,6 +314,8 @@ def sage_backward(blocks, X: np.ndarray, w_self, w_neigh, hidden, means, dlogits
         else:
             lib().orc_sage_linear_backward(n, d_in, d_out, _p(Hd), _p(m), _p(ws), _p(wn), _p(dZ),
                                            _p(dWs[l]), _p(dWn[l]), _p(dbs[l]), None, None)
+    if input_grad:
+        return dWs, dWn, dbs, dOut
     return dWs, dWn, dbs
 
 
@@ -315,6 +323,32 @@ def sgd(params, grads, lr: float):
     """p - lr * g for every array."""
     return [np.asarray(p, dtype=np.float64) - lr * np.asarray(g, dtype=np.float64)
             for p, g in zip(params, grads)]
+
+
+def embedding_sgd(table: np.ndarray, rows, dX: np.ndarray, lr: float) -> np.ndarray:
+    """The sparse update of learnable vertex embeddings (Section III-E: SGD
+    on the rows a mini-batch touched): table[rows[u]] -= lr * dX[u].  The
+    rows of one mini-batch are distinct (its input vertices).  Returns the
+    updated copy."""
+    out = np.array(table, dtype=np.float64, copy=True)
+    rows = np.asarray(rows, dtype=np.int64)
+    if len(np.unique(rows)) != len(rows):
+        raise ValueError("the rows of one mini-batch must be distinct")
+    out[rows] -= lr * np.asarray(dX, dtype=np.float64)
+    return out
+
+
+def sage_train_step_embed(blocks, table: np.ndarray, w_self, w_neigh, bias, labels, lr: float, emb_lr: float):
+    """A training step whose layer-0 inputs are learnable vertex embeddings:
+    X = table[src(0)], forward, loss, backward down to X, SGD on the dense
+    weights and on the embedding rows.  Returns (loss, (dW_self, dW_neigh,
+    db), dX, (new W_self, new W_neigh, new b), new table)."""
+    X = np.asarray(table, dtype=np.float64)[np.asarray(blocks[0].src, dtype=np.int64)]
+    logits, hidden, means = sage_forward_train(blocks, X, w_self, w_neigh, bias)
+    loss, dz = softmax_xent(logits, labels)
+    dWs, dWn, dbs, dX = sage_backward(blocks, X, w_self, w_neigh, hidden, means, dz, input_grad=True)
+    return (loss, (dWs, dWn, dbs), dX, (sgd(w_self, dWs, lr), sgd(w_neigh, dWn, lr), sgd(bias, dbs, lr)),
+            embedding_sgd(table, blocks[0].src, dX, emb_lr))
 
 
 def sage_train_step(blocks, X: np.ndarray, w_self, w_neigh, bias, labels, lr: float):

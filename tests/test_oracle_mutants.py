@@ -126,6 +126,8 @@ def test_pins_catch_mutant(name, tmp_path, dg):
         "xent": lambda: tt.test_softmax_xent_value_and_gradient(mut),
         "train_fd": lambda: tt.test_backward_matches_finite_differences(mut, dg),
         "train_dense": lambda: tt.test_full_neighbourhood_gradients_equal_dense_autograd(mut, dg, 2),
+        "input_fd": lambda: tt.test_input_gradient_matches_finite_differences(mut, dg),
+        "input_dense": lambda: tt.test_input_gradient_equals_dense_autograd(mut, dg, 2),
     }
     caught = next((k for k, fn in checks.items() if _fails(fn)), None)
     assert caught is not None, f"mutant {name} passed every pin"

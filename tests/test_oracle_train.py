@@ -130,3 +130,82 @@ def test_sgd_step(orc, dg):
     # a small step along the negative gradient lowers the loss
     _, _, _, (sws, swn, sbs) = orc.sage_train_step(blocks, X0, ws, wn, bs, y, 1e-3)
     assert _loss(orc, blocks, X0, sws, swn, sbs, y) < loss
+
+
+# ---- learnable vertex embeddings: the input-row gradient and its update ----
+
+def test_input_gradient_matches_finite_differences(orc, dg):
+    """Every entry of the layer-0 input rows of a three-layer model."""
+    dims, fanouts = [5, 4, 4, 3], [2, 3, 2]
+    g, blocks, X0, ws, wn, bs, y, _, _ = _setup(orc, dg, dims, fanouts)
+    logits, hidden, means = orc.sage_forward_train(blocks, X0, ws, wn, bs)
+    _, dz = orc.softmax_xent(logits, y)
+    _, _, _, dX = orc.sage_backward(blocks, X0, ws, wn, hidden, means, dz, input_grad=True)
+    assert dX.shape == X0.shape
+    h = 1e-6
+    scale = max(1.0, np.abs(dX).max())
+    for idx in np.ndindex(*X0.shape):
+        keep = X0[idx]
+        X0[idx] = keep + h
+        up = _loss(orc, blocks, X0, ws, wn, bs, y)
+        X0[idx] = keep - h
+        dn = _loss(orc, blocks, X0, ws, wn, bs, y)
+        X0[idx] = keep
+        fd = (up - dn) / (2 * h)
+        assert abs(fd - dX[idx]) < 1e-6 * scale, (idx, fd, dX[idx])
+
+
+@pytest.mark.parametrize("L", [1, 2, 3])
+def test_input_gradient_equals_dense_autograd(orc, dg, L):
+    """Full neighbourhoods: the gradient in the input rows equals torch
+    autograd of the dense full-graph model in the feature matrix, at the
+    rows of the sampled input vertices (every other row's gradient is 0)."""
+    g = dg.er_directed(300, 4.0, 11)
+    fo = [int(g.degrees().max()) + 1] * L
+    dims = [6] + [7] * (L - 1) + [4]
+    w = dg.sage_weights(dims, 5)
+    ws, wn, bs = w.as_f64()
+    X = np.random.default_rng(1).standard_normal((300, 6))
+    seeds = dg.permutation(300, 2)[:40]
+    y = dg.labels(300, dims[-1], 9)[seeds]
+    blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fo, 77)
+    _, _, dX, _, _ = orc.sage_train_step_embed(blocks, X, ws, wn, bs, y, 0.1, 0.1)
+    n = g.num_nodes
+    A = torch.zeros((n, n), dtype=torch.float64)
+    for v in range(n):
+        row = g.indices[g.indptr[v]:g.indptr[v + 1]]
+        if len(row):
+            A[v, torch.from_numpy(row.astype(np.int64))] = 1.0 / len(row)
+    Xt = torch.tensor(X, requires_grad=True)
+    H = Xt
+    for l in range(L):
+        Z = H @ torch.from_numpy(ws[l]) + (A @ H) @ torch.from_numpy(wn[l]) + torch.from_numpy(bs[l])
+        H = torch.relu(Z) if l < L - 1 else Z
+    loss = torch.nn.functional.cross_entropy(H[torch.from_numpy(seeds.astype(np.int64))],
+                                             torch.from_numpy(y.astype(np.int64)))
+    (gX,) = torch.autograd.grad(loss, [Xt])
+    gX = gX.numpy()
+    src = np.asarray(blocks[0].src, dtype=np.int64)
+    assert np.allclose(dX, gX[src], rtol=1e-10, atol=1e-12), np.abs(dX - gX[src]).max()
+    rest = np.setdiff1d(np.arange(n), src)
+    assert np.abs(gX[rest]).max(initial=0.0) == 0.0
+
+
+def test_embedding_sgd(orc, dg):
+    rng = np.random.default_rng(5)
+    table = rng.standard_normal((50, 6))
+    rows = np.array([7, 3, 41, 0])
+    dX = rng.standard_normal((4, 6))
+    new = orc.embedding_sgd(table, rows, dX, 0.5)
+    untouched = np.setdiff1d(np.arange(50), rows)
+    assert np.array_equal(new[untouched], table[untouched])
+    for i, r in enumerate(rows):
+        assert np.array_equal(new[r], table[r] - 0.5 * dX[i])
+    with pytest.raises(ValueError):
+        orc.embedding_sgd(table, np.array([1, 1]), dX[:2], 0.5)
+    # a small step on the embeddings (weights held) lowers the loss
+    dims, fanouts = [5, 4, 3], [2, 3]
+    g, blocks, X0, ws, wn, bs, y, seeds, Xall = _setup(orc, dg, dims, fanouts)
+    loss0, _, _, _, tab = orc.sage_train_step_embed(blocks, Xall, ws, wn, bs, y, 0.0, 1e-2)
+    X1 = tab[np.asarray(blocks[0].src, dtype=np.int64)]
+    assert _loss(orc, blocks, X1, ws, wn, bs, y) < loss0
