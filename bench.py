@@ -62,6 +62,9 @@ def parse():
                     help="infer: sample + gather + forward (the default); train: the whole "
                          "training iteration, + loss, backward and SGD (fp32 workloads)")
     ap.add_argument("--lr", type=float, default=0.01, help="SGD step size of --mode train")
+    ap.add_argument("--embed", action="store_true",
+                    help="--mode train: the layer-0 inputs are learnable vertex embeddings (a table "
+                         "initialised from the features), updated by sparse SGD every iteration")
     ap.add_argument("--fused", action="store_true",
                     help="--mode train: the forward with the feature pull folded into layer 0 "
                          "(only the destination rows gathered)")
@@ -585,6 +588,10 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
     C = cfg.dims[-1]
     lab_all = vertex_labels(g.num_nodes, C, cfg.seeds[2] + 1)
     labels = [torch.from_numpy(lab_all[b]).to(dev) for b in wl.batches]
+    if args.embed:
+        # the table the layer-0 inputs come from, trained in place (loaders
+        # gather from it while the compute stream updates it: Hogwild)
+        feats = feats.clone()
     S = max(1, args.streams)
     comp = torch.cuda.current_stream()
     lanes = []
@@ -597,7 +604,9 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
                           x=torch.empty((rows, cfg.feat_dim), dtype=feats.dtype, device=dev),
                           ready=torch.cuda.Event(), done=torch.cuda.Event()))
     ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(probe, weights), dev)[1]
-    ws_bwd = gmb._aligned_bytes(gmb.backward_workspace_bytes(probe, weights), dev)[1]
+    ws_bwd = gmb._aligned_bytes((gmb.backward_embedding_workspace_bytes if args.embed
+                                 else gmb.backward_workspace_bytes)(probe, weights), dev)[1]
+    emb = dict(embedding=feats, emb_lr=args.lr) if args.embed else {}
     logits = torch.empty((cfg.batch, C), dtype=torch.float32, device=dev)
     grads = gmb.SageGrads(weights)
     K, W = args.steps, args.warmup
@@ -613,7 +622,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
     def model(blocks, x, b, i):
         lg = forward(blocks, x, b)
         gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
-                          workspace=ws_bwd)
+                          workspace=ws_bwd, **emb)
         gmb.sgd_update(weights, grads, args.lr)
 
     def step(i):
@@ -664,7 +673,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         lg = forward(blocks, x, b)
         e[3].record(comp)
         gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
-                          workspace=ws_bwd)
+                          workspace=ws_bwd, **emb)
         e[4].record(comp)
         gmb.sgd_update(weights, grads, args.lr)
         e[5].record(comp)
@@ -690,7 +699,8 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
     tf, tb = stage["forward"] / 1e3, stage["backward"] / 1e3
     res = {
         "metric": "seeds/s of the training iteration (sample+gather+SAGE fwd+loss+bwd+SGD)"
-                  + (", gather folded into the forward" if args.fused else ""),
+                  + (", gather folded into the forward" if args.fused else "")
+                  + (", learnable vertex embeddings" if args.embed else ""),
         "value": seeds_total / T,
         "unit": "seeds/s",
         "n_gpus": 1, "steps": K, "warmup": W,
@@ -701,7 +711,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
                                f"x{cfg.feat_dim}, SAGE {'-'.join(map(str, cfg.dims))}, fanouts {fanouts}, batch "
                                f"{cfg.batch}, {nb} batches per epoch, SGD lr {args.lr}",
                    "batch": cfg.batch, "fanouts": fanouts, "dims": list(cfg.dims), "batches_per_epoch": nb,
-                   "mode": "train", "fused": bool(args.fused)},
+                   "mode": "train", "fused": bool(args.fused), "embed": bool(args.embed)},
         "epoch_s": nb * T / K,
         "pass_a_runs_seeds_per_s": [seeds_total / t for t in runs],
         "sampled_edges_per_s": edges_total / T,

@@ -298,6 +298,37 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
                       const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
                       const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- learnable vertex embeddings (Section III-C, Section III-E) -------- */
+
+/* Bytes of workspace gmb_sage_backward_embedding needs (0 for bad arguments,
+ * including a model it does not support: those of gmb_sage_backward, and
+ * dims[0] or dims[1] breaking the same limits as the hidden widths). */
+size_t gmb_backward_embedding_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights);
+
+/* gmb_sage_backward for a model whose layer-0 inputs are learnable vertex
+ * embeddings (the transductive case of Section III-C): besides the weight
+ * gradients it takes the gradient in layer 0's input rows,
+ * dX = dZ_0 W_self^T on the destination rows plus, over every block-0 edge
+ * (v <- u), (dZ_0 W_neigh^T)[v] / k_v on row u (no activation acts on the
+ * input), and applies it at once as the sparse SGD step of the paper's
+ * embeddings (Section III-E): table[src_ids[u]] -= emb_lr * dX[u] for every
+ * input vertex u of block 0.  dX is never stored.
+ *   x          as for gmb_sage_backward: the gathered input rows (those
+ *              of table), or x_dst of gmb_sage_forward_fused run on table.
+ *   table      device fp32 [num_nodes, dims[0]], 16-byte aligned, updated
+ *              in place (rows of vertices outside the mini-batch are not
+ *              touched).
+ *   emb_lr     the embeddings' step size.
+ *   ws         >= gmb_backward_embedding_workspace_bytes() bytes.
+ * The rows of one mini-batch are distinct, so the update needs no atomics;
+ * calls in flight together on several streams update the shared table
+ * without locks (asynchronous SGD as in Hogwild, as the paper updates its
+ * embeddings), and a gather running meanwhile may see old or new rows. */
+int gmb_sage_backward_embedding(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
+                                const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
+                                const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, float* table,
+                                int64_t num_nodes, float emb_lr, void* stream);
+
 /* One SGD step: every weight array W -= lr * dW, every bias b -= lr * db,
  * in place on the device arrays that `weights` points to (fp32). */
 int gmb_sgd_update(const gmb_sage_weights* weights, const gmb_sage_grads* grads, float lr, void* stream);

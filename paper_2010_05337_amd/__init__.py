@@ -32,7 +32,8 @@ EXPORTS = (
     "gmb_state_status_word", "gmb_read_status", "gmb_sample_workspace_bytes", "gmb_sample_blocks",
     "gmb_read_sizes", "gmb_gather_features", "gmb_forward_workspace_bytes",
     "gmb_forward_hidden_offset", "gmb_sage_forward", "gmb_sage_forward_fused", "gmb_backward_workspace_bytes",
-    "gmb_sage_backward", "gmb_sgd_update",
+    "gmb_sage_backward", "gmb_sgd_update", "gmb_backward_embedding_workspace_bytes",
+    "gmb_sage_backward_embedding",
 )
 
 
@@ -125,6 +126,13 @@ def lib() -> ctypes.CDLL:
         L.gmb_sage_backward.restype = ctypes.c_int
         L.gmb_sage_backward.argtypes = [ctypes.POINTER(BlocksStruct), vp, ctypes.POINTER(WeightsStruct), vp, vp,
                                         vp, sz, ctypes.POINTER(GradsStruct), vp, vp, sz, vp]
+        L.gmb_backward_embedding_workspace_bytes.restype = sz
+        L.gmb_backward_embedding_workspace_bytes.argtypes = [ctypes.POINTER(BlocksStruct),
+                                                             ctypes.POINTER(WeightsStruct)]
+        L.gmb_sage_backward_embedding.restype = ctypes.c_int
+        L.gmb_sage_backward_embedding.argtypes = [ctypes.POINTER(BlocksStruct), vp, ctypes.POINTER(WeightsStruct),
+                                                  vp, vp, vp, sz, ctypes.POINTER(GradsStruct), vp, vp, sz, vp,
+                                                  ctypes.c_int64, ctypes.c_float, vp]
         L.gmb_sgd_update.restype = ctypes.c_int
         L.gmb_sgd_update.argtypes = [ctypes.POINTER(WeightsStruct), ctypes.POINTER(GradsStruct),
                                      ctypes.c_float, vp]
@@ -467,17 +475,31 @@ def backward_workspace_bytes(blocks: Blocks, weights: SageWeights) -> int:
     return lib().gmb_backward_workspace_bytes(ctypes.byref(blocks.struct), ctypes.byref(weights.struct))
 
 
+def backward_embedding_workspace_bytes(blocks: Blocks, weights: SageWeights) -> int:
+    return lib().gmb_backward_embedding_workspace_bytes(ctypes.byref(blocks.struct), ctypes.byref(weights.struct))
+
+
 def sage_backward(blocks: Blocks, feats: torch.Tensor, weights: SageWeights, logits: torch.Tensor,
                   labels: torch.Tensor, fwd_workspace: torch.Tensor, grads: SageGrads | None = None,
-                  loss: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+                  loss: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                  embedding: torch.Tensor | None = None, emb_lr: float = 0.0):
     """Gradients of the mean softmax cross-entropy of `logits` (from the
     sage_forward call that used `fwd_workspace`) against `labels` (device
     int32, one per seed).  Returns (grads, loss) with loss a 1-element
-    float32 device tensor."""
+    float32 device tensor.  With `embedding` (the fp32 [num_nodes, dims[0]]
+    table the layer-0 inputs were taken from) the gradient in the input
+    rows is applied to the table as an SGD step of size emb_lr."""
     _require_cuda(labels, "labels")
     if labels.dtype != torch.int32 or labels.numel() < blocks.num_seeds:
         raise TypeError("labels must be int32 with one entry per seed")
-    need = backward_workspace_bytes(blocks, weights)
+    if embedding is not None:
+        _require_cuda(embedding, "embedding")
+        if embedding.dtype != torch.float32 or embedding.dim() != 2 or embedding.shape[1] != weights.dims[0] \
+                or not embedding.is_contiguous():
+            raise ValueError("embedding must be a contiguous float32 [num_nodes, dims[0]] tensor")
+        need = backward_embedding_workspace_bytes(blocks, weights)
+    else:
+        need = backward_workspace_bytes(blocks, weights)
     if need == 0:
         _check(-1)
     if workspace is None or workspace.numel() < need or workspace.data_ptr() % 256:
@@ -486,12 +508,15 @@ def sage_backward(blocks: Blocks, feats: torch.Tensor, weights: SageWeights, log
         grads = SageGrads(weights)
     if loss is None:
         loss = torch.empty(1, dtype=torch.float32, device=feats.device)
-    _check(lib().gmb_sage_backward(ctypes.byref(blocks.struct), ctypes.c_void_p(feats.data_ptr()),
-                                   ctypes.byref(weights.struct), ctypes.c_void_p(logits.data_ptr()),
-                                   ctypes.c_void_p(labels.data_ptr()),
-                                   ctypes.c_void_p(fwd_workspace.data_ptr()), fwd_workspace.numel(),
-                                   ctypes.byref(grads.struct), ctypes.c_void_p(loss.data_ptr()),
-                                   ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream_handle()))
+    common = (ctypes.byref(blocks.struct), ctypes.c_void_p(feats.data_ptr()), ctypes.byref(weights.struct),
+              ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(labels.data_ptr()),
+              ctypes.c_void_p(fwd_workspace.data_ptr()), fwd_workspace.numel(), ctypes.byref(grads.struct),
+              ctypes.c_void_p(loss.data_ptr()), ctypes.c_void_p(workspace.data_ptr()), workspace.numel())
+    if embedding is None:
+        _check(lib().gmb_sage_backward(*common, _stream_handle()))
+    else:
+        _check(lib().gmb_sage_backward_embedding(*common, ctypes.c_void_p(embedding.data_ptr()),
+                                                 embedding.shape[0], float(emb_lr), _stream_handle()))
     return grads, loss
 
 

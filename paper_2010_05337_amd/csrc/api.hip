@@ -475,22 +475,26 @@ namespace {
 struct BackwardPlan {
   int ldz[GMB_MAX_LAYERS];   // row stride of dZ of layer l (floats, multiple of 4)
   size_t off_a, off_b, off_dm, off_part, off_lossrows;
-  size_t off_cnt, off_off, off_pos, off_csc;   // the transpose of a block
+  size_t off_cnt, off_off, off_pos, off_csc, off_long;   // the transpose of a block
   int64_t cnt_len;                             // ints of the edge counters
   int64_t scan_len;                            // ints of one layer's scan state
   int64_t clear_len;                           // ints cleared at the start (counters + scan states)
   size_t total;
 };
 
-int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* plan) {
+// embed: layer 0's inputs are learnable vertex embeddings, so the backward
+// also runs layer 0's input gradient and its transpose (the rows it needs:
+// layer 0's destinations for the self part and the mean's gradient).
+int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* plan, bool embed) {
   ForwardPlan fp;
   int st = plan_forward(b, w, &fp);
   if (st != GMB_OK) return st;
   if (w->dtype != GMB_F32) return fail(GMB_EINVAL, "the training step is fp32 only");
   const int L = w->num_layers;
-  for (int l = 1; l < L; ++l)
-    if (w->dims[l] % 4) return fail(GMB_EINVAL, "hidden dims[%d]=%d is not a multiple of 4", l, w->dims[l]);
-  for (int l = 1; l < L; ++l)
+  const int first = embed ? 0 : 1;   // the lowest layer whose input gradient runs
+  for (int l = first; l < L; ++l)
+    if (w->dims[l] % 4) return fail(GMB_EINVAL, "dims[%d]=%d is not a multiple of 4", l, w->dims[l]);
+  for (int l = first; l < L; ++l)
     if (w->dims[l + 1] > 640) return fail(GMB_EINVAL, "dims[%d]=%d above 640 (input-gradient kernel)", l + 1, w->dims[l + 1]);
   BackwardPlan p{};
   size_t buf = 0, dm = 0, part = 0, src = 1, nnz = 1;
@@ -499,8 +503,9 @@ int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* 
     const gmb_block& k = b->blk[l];
     p.ldz[l] = (l == L - 1) ? (d_out + 3) / 4 * 4 : d_out;
     buf = std::max(buf, static_cast<size_t>(std::max<int64_t>(k.cap_dst, 1)) * p.ldz[l]);
-    if (l > 0) {
-      buf = std::max(buf, static_cast<size_t>(std::max<int64_t>(k.cap_src, 1)) * d_in);
+    if (l > 0) buf = std::max(buf, static_cast<size_t>(std::max<int64_t>(k.cap_src, 1)) * d_in);
+    if (l == 0 && embed) buf = std::max(buf, static_cast<size_t>(std::max<int64_t>(k.cap_dst, 1)) * d_in);
+    if (l >= first) {
       dm = std::max(dm, static_cast<size_t>(std::max<int64_t>(k.cap_dst, 1)) * d_in);
       src = std::max(src, static_cast<size_t>(k.cap_src));
       nnz = std::max(nnz, static_cast<size_t>(k.cap_nnz));
@@ -521,7 +526,7 @@ int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* 
   off = align_up(off + 4 * static_cast<size_t>(std::max(b->num_seeds, 1)));
   p.cnt_len = static_cast<int64_t>((src + 1) / 2 * 2);
   p.scan_len = 2 + 2 * gmb::csc_scan_tiles(static_cast<int64_t>(src));
-  p.clear_len = p.cnt_len + static_cast<int64_t>(std::max(L - 1, 0)) * p.scan_len;
+  p.clear_len = p.cnt_len + static_cast<int64_t>(std::max(L - first, 0)) * p.scan_len;
   p.off_cnt = off;
   off = align_up(off + 4 * static_cast<size_t>(p.clear_len));
   p.off_off = off;
@@ -530,6 +535,8 @@ int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* 
   off = align_up(off + 4 * src);
   p.off_csc = off;
   off = align_up(off + 8 * nnz);
+  p.off_long = off;
+  off = align_up(off + 4 * src);
   p.total = off;
   *plan = p;
   return GMB_OK;
@@ -544,21 +551,15 @@ int check_grads(const gmb_sage_grads* g, const gmb_sage_weights* w) {
   return GMB_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights) {
+// The backward from the loss down; with table != NULL layer 0's input
+// gradient is applied to the embedding rows of block 0's sources.
+int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights, const float* logits,
+                 const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes, const gmb_sage_grads* grads,
+                 float* loss, void* ws, size_t ws_bytes, float* table, int64_t num_nodes, float emb_lr,
+                 void* stream) {
+  const bool embed = table != nullptr;
   BackwardPlan p;
-  if (plan_backward(blocks, weights, &p) != GMB_OK) return 0;
-  return p.total;
-}
-
-int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
-                      const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
-                      const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, void* stream) {
-  BackwardPlan p;
-  int st = plan_backward(blocks, weights, &p);
+  int st = plan_backward(blocks, weights, &p, embed);
   if (st != GMB_OK) return st;
   ForwardPlan fp;
   plan_forward(blocks, weights, &fp);
@@ -582,6 +583,7 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
   int32_t* offs = reinterpret_cast<int32_t*>(base + p.off_off);
   int32_t* pos = reinterpret_cast<int32_t*>(base + p.off_pos);
   int2* csc = reinterpret_cast<int2*>(base + p.off_csc);
+  int32_t* long_rows = reinterpret_cast<int32_t*>(base + p.off_long);
   hipError_t e = gmb::launch_xent(logits, labels, blocks->num_seeds, weights->dims[L], p.ldz[L - 1], cur,
                                   reinterpret_cast<float*>(base + p.off_lossrows), loss, cnt, p.clear_len, s);
   if (e != hipSuccess) return hip_fail(e, "loss launch");
@@ -594,7 +596,7 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
     e = gmb::launch_wgrad(bk.sizes, h_in, m, d_in, cur, p.ldz[l], d_out, std::max<int64_t>(bk.cap_dst, 1), part,
                           grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], s);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
-    if (l == 0) break;
+    if (l == 0 && !embed) break;
     // dZ [W_self; W_neigh]^T: dH_self into `other`, dM; the block's
     // in-edge counts per source on the way
     e = gmb::launch_dgrad(bk.sizes, cur, p.ldz[l], d_out, static_cast<const float*>(weights->w_self[l]),
@@ -602,14 +604,52 @@ int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_we
                           bk.indices, bk.cap_nnz, bk.fanout, cnt, s);
     if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
     // the mean's backward through the block's transpose, the ReLU of the
-    // layer below on the way out: `other` becomes that layer's dZ
-    uint32_t* scan_state = reinterpret_cast<uint32_t*>(cnt + p.cnt_len + (l - 1) * p.scan_len);
-    e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, bk.cap_nnz, bk.fanout, dM, h_in, d_in, other,
-                                  bk.cap_dst, bk.cap_src, cnt, offs, pos, scan_state, csc, s);
+    // layer below on the way out: `other` becomes that layer's dZ; on layer
+    // 0 (learnable embeddings) the input gradient goes into the table rows
+    uint32_t* scan_state = reinterpret_cast<uint32_t*>(cnt + p.cnt_len + (embed ? l : l - 1) * p.scan_len);
+    e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, bk.cap_nnz, bk.fanout, dM,
+                                  l == 0 ? nullptr : h_in, d_in, other, bk.cap_dst, bk.cap_src, cnt, offs, pos,
+                                  scan_state, csc, long_rows, l == 0 ? table : nullptr, bk.src_ids, num_nodes,
+                                  emb_lr, s);
     if (e != hipSuccess) return hip_fail(e, "mean-backward launch");
     std::swap(cur, other);
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights) {
+  BackwardPlan p;
+  if (plan_backward(blocks, weights, &p, false) != GMB_OK) return 0;
+  return p.total;
+}
+
+size_t gmb_backward_embedding_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights) {
+  BackwardPlan p;
+  if (plan_backward(blocks, weights, &p, true) != GMB_OK) return 0;
+  return p.total;
+}
+
+int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
+                      const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
+                      const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, void* stream) {
+  return run_backward(blocks, x, weights, logits, labels, fwd_ws, fwd_ws_bytes, grads, loss, ws, ws_bytes, nullptr,
+                      0, 0.f, stream);
+}
+
+int gmb_sage_backward_embedding(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
+                                const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
+                                const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, float* table,
+                                int64_t num_nodes, float emb_lr, void* stream) {
+  if (!table) return fail(GMB_EINVAL, "table is NULL");
+  if (num_nodes < 1 || num_nodes > kMaxInt32)
+    return fail(GMB_EINVAL, "num_nodes=%lld outside 1..2^31-1", static_cast<long long>(num_nodes));
+  if (reinterpret_cast<uintptr_t>(table) % 16) return fail(GMB_EINVAL, "table must be 16-byte aligned");
+  return run_backward(blocks, x, weights, logits, labels, fwd_ws, fwd_ws_bytes, grads, loss, ws, ws_bytes, table,
+                      num_nodes, emb_lr, stream);
 }
 
 int gmb_sgd_update(const gmb_sage_weights* weights, const gmb_sage_grads* grads, float lr, void* stream) {

@@ -138,12 +138,16 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
                         const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t fanout, int32_t* cnt,
                         hipStream_t s);
 // look-back tiles of the transpose scan over cap_src sources; its state
-// (one ticket word pair, then 2 words per tile) must start zeroed
+// (the tile ticket, the long-row count, then 2 words per tile) must start
+// zeroed; long_rows holds cap_src ints
 int64_t csc_scan_tiles(int64_t cap_src);
+// With table != NULL the pull applies table[ids[u]] -= lr * g instead of
+// writing the masked gradient into dH (out unused).
 hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                 int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
-                                uint32_t* scan_state, int2* csc, hipStream_t s);
+                                uint32_t* scan_state, int2* csc, int32_t* long_rows, float* table, const int32_t* ids,
+                                int64_t num_nodes, float lr, hipStream_t s);
 hipError_t launch_sgd(const SgdArgs& a, float lr, hipStream_t s);
 
 }  // namespace gmb

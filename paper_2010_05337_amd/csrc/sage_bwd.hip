@@ -24,6 +24,8 @@
 //                  edges (v <- u) of dM[v] / k_v), one pass per source row:
 //                  the mean's backward as a gather over the transpose, with
 //                  the ReLU of the layer below applied on the way out
+//   k_pull_update  on layer 0 with learnable vertex embeddings: the same
+//                  sum applied at once as the sparse SGD step of the rows
 //   k_sgd          W -= lr dW over every parameter array
 #include <algorithm>
 
@@ -499,17 +501,20 @@ __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes
 // ---- mean backward: the block's transpose -----------------------------------
 
 // off[u] = sum of cnt[0 .. u), off[n_src] = the total, pos[u] = off[u]
-// (the fill's cursors), and cnt cleared for the next layer.  Tiles of 1024
+// (the fill's cursors), cnt cleared for the next layer, and the sources
+// with more than kLongList entries listed in long_rows[0 .. *n_long).  Tiles of 1024
 // counts (four per thread), numbered by an atomic ticket, joined by the
 // decoupled look-back (both the ticket and the look-back words start at 0).
 // If the look-back's bounded wait runs out (it does not when every tile
 // runs), the offsets come out wrong but the fill and the pull stay in
 // bounds.
 constexpr int kScanTile = 1024;
+constexpr int kLongList = 16;   // transpose lists longer than this take a workgroup each
 
 __global__ __launch_bounds__(256) void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ off, int32_t* __restrict__ pos,
-                                                  uint32_t* __restrict__ ticket, uint64_t* __restrict__ words) {
+                                                  uint32_t* __restrict__ ticket, uint64_t* __restrict__ words,
+                                                  uint32_t* __restrict__ n_long, int32_t* __restrict__ long_rows) {
   __shared__ int s_tile;
   __shared__ int32_t s_excl;
   __shared__ int32_t smem[4];
@@ -553,6 +558,21 @@ __global__ __launch_bounds__(256) void k_csc_scan(const int32_t* __restrict__ si
     o += c[j];
   }
   if (tile == ntiles - 1 && threadIdx.x == 0) off[n] = s_excl + total[0];
+  // sources with long lists (hubs) go to the list the workgroup-per-row
+  // kernel takes (the per-row kernels skip them); after the look-back, so
+  // that the successors' waits do not include it; one atomic per wave and
+  // item, the lanes' places from the ballot
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint64_t mask = __ballot(c[j] > kLongList);
+    if (!mask) continue;   // uniform
+    const int leader = __ffsll(static_cast<long long>(mask)) - 1;
+    uint32_t base = 0;
+    if (lane == leader) base = atomicAdd(n_long, static_cast<uint32_t>(__popcll(mask)));
+    base = __shfl(base, leader, 64);
+    if (c[j] > kLongList) long_rows[base + __popcll(mask & ((1ull << lane) - 1ull))] = i0 + j;
+  }
 }
 
 // Thread per edge slot: the edge (v <- u) takes the next place of u and
@@ -570,8 +590,13 @@ __global__ __launch_bounds__(256) void k_csc_fill(const int32_t* __restrict__ si
 }
 
 // G lanes per source row u, lane c covers columns 4c, 4c + G, ... (d % 4 ==
-// 0): dH[u] = (out[u] > 0) * ((u < n_dst ? dH[u] : 0) + sum over u's
-// transpose entries (v, w) of w * dM[v]).  out is the layer below's output.
+// 0): g = (u < n_dst ? dH[u] : 0) + sum over u's transpose entries (v, w) of
+// w * dM[v].  UPDATE = false: dH[u] = (out[u] > 0) * g (out: the layer
+// below's output).  UPDATE = true (layer 0 with learnable vertex
+// embeddings): table[ids[u]] -= lr * g, a plain read-modify-write (the rows
+// of one mini-batch are distinct; mini-batches in flight together update
+// without locks, as Hogwild does); an id outside [0, num_nodes) skips the
+// row (only after a data error).
 template <int G>
 __global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ sizes,
                                                    const int32_t* __restrict__ off, const int2* __restrict__ csc,
@@ -583,12 +608,15 @@ __global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ s
   const int lane = threadIdx.x & (G - 1);
   if (u >= n_src) return;
   int32_t s0 = off[u], s1 = off[u + 1];
+  if (s1 - s0 > kLongList) return;   // k_pull_long's row
   s0 = s0 < 0 ? 0 : s0;
   s1 = s1 > cap_nnz ? static_cast<int32_t>(cap_nnz) : s1;
   const bool self = u < n_dst;
   const int chunks = d / 4;
   for (int c = lane; c < chunks; c += G) {
     const int64_t at = u * d + 4 * c;
+    // the layer below's output does not depend on the gradient: read first
+    const float4 o = *reinterpret_cast<const float4*>(out + at);
     float4 acc = self ? *reinterpret_cast<const float4*>(dH + at) : make_float4(0.f, 0.f, 0.f, 0.f);
     int32_t s = s0;
     for (; s + 1 < s1; s += 2) {
@@ -607,12 +635,211 @@ __global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ s
       const float w0 = ok0 ? __int_as_float(e0.y) : 0.f;
       acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
     }
-    const float4 o = *reinterpret_cast<const float4*>(out + at);
     acc.x = o.x > 0.f ? acc.x : 0.f;
     acc.y = o.y > 0.f ? acc.y : 0.f;
     acc.z = o.z > 0.f ? acc.z : 0.f;
     acc.w = o.w > 0.f ? acc.w : 0.f;
     *reinterpret_cast<float4*>(dH + at) = acc;
+  }
+}
+
+// Layer 0 with learnable vertex embeddings: table[ids[u]] -= lr * g_u with
+// g_u = (u < n_dst ? dH[u] : 0) + sum over u's transpose entries (v, w) of
+// w * dM[v], as a plain read-modify-write (the rows of one mini-batch are
+// distinct; mini-batches in flight together update without locks, as
+// Hogwild does; an id outside [0, num_nodes) skips its row).  The update is
+// bound by the latency of three dependent rounds of reads per row (offsets
+// and ids; table row, self part and the first entries; the entries' dM
+// rows), so each G-lane group takes R rows and issues every round for all
+// of them at once; entries past the first E of a row (few rows have them)
+// follow one by one.  Lane c covers the float4 columns c, c + G, ...
+template <int G, int R, int E>
+__global__ __launch_bounds__(256) void k_pull_update(const int32_t* __restrict__ sizes,
+                                                     const int32_t* __restrict__ off,
+                                                     const int2* __restrict__ csc, int64_t cap_nnz,
+                                                     const float* __restrict__ dM, const float* __restrict__ dH,
+                                                     int d, float* __restrict__ table,
+                                                     const int32_t* __restrict__ ids, int64_t num_nodes, float lr) {
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  const int32_t n_src = load_size(&sizes[kNSrc]);
+  const int64_t group = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
+  const int lane = threadIdx.x & (G - 1);
+  const int64_t u0 = group * R;
+  if (u0 >= n_src) return;
+  // round 1: the rows' offsets and table ids
+  int32_t s0[R], cnt[R], trow[R];
+  bool live[R], self[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t u = u0 + r;
+    const int64_t uc = u < n_src ? u : u0;
+    int32_t a = off[uc], b = off[uc + 1];
+    const int32_t id = ids[uc];
+    const bool long_list = b - a > kLongList;   // k_pull_long's row
+    a = a < 0 ? 0 : a;
+    b = b > cap_nnz ? static_cast<int32_t>(cap_nnz) : b;
+    s0[r] = a;
+    cnt[r] = b > a && !long_list ? b - a : 0;
+    live[r] = u < n_src && id >= 0 && id < num_nodes && !long_list;
+    trow[r] = live[r] ? id : 0;
+    self[r] = u < n_dst;
+  }
+  const int chunks = d / 4;
+  for (int c0 = lane; c0 < chunks + G - 1 - (chunks - 1) % G; c0 += G) {   // whole passes of the group
+    const int c = c0 < chunks ? c0 : chunks - 1;
+    // round 2: table rows, self parts, the first E entries of every row
+    float4 keep[R], acc[R];
+    int2 e[R][E];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      keep[r] = *reinterpret_cast<const float4*>(table + static_cast<int64_t>(trow[r]) * d + 4 * c);
+      acc[r] = *reinterpret_cast<const float4*>(dH + (self[r] ? u0 + r : 0) * d + 4 * c);
+#pragma unroll
+      for (int j = 0; j < E; ++j) e[r][j] = csc[j < cnt[r] ? s0[r] + j : 0];
+    }
+    // round 3: the entries' dM rows
+    float4 g[R][E];
+    float w[R][E];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const bool ok = j < cnt[r] && e[r][j].x >= 0 && e[r][j].x < n_dst;
+        w[r][j] = ok ? __int_as_float(e[r][j].y) : 0.f;
+        g[r][j] = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? e[r][j].x : 0) * d + 4 * c);
+      }
+    // (the table rows and self parts are used unconditionally from here, so
+    // the compiler cannot turn their reads into branched ones; the step
+    // comes after the dM reads are issued so that all of them overlap)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      asm volatile("" : "+v"(keep[r].x), "+v"(keep[r].y), "+v"(keep[r].z), "+v"(keep[r].w));
+      asm volatile("" : "+v"(acc[r].x), "+v"(acc[r].y), "+v"(acc[r].z), "+v"(acc[r].w));
+      if (!self[r]) acc[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        acc[r].x += w[r][j] * g[r][j].x;
+        acc[r].y += w[r][j] * g[r][j].y;
+        acc[r].z += w[r][j] * g[r][j].z;
+        acc[r].w += w[r][j] * g[r][j].w;
+      }
+    // the rest of the longer lists
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      for (int32_t j = E; j < cnt[r]; ++j) {
+        const int2 x = csc[s0[r] + j];
+        const bool ok = x.x >= 0 && x.x < n_dst;
+        const float4 gx = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? x.x : 0) * d + 4 * c);
+        const float wx = ok ? __int_as_float(x.y) : 0.f;
+        acc[r].x += wx * gx.x; acc[r].y += wx * gx.y; acc[r].z += wx * gx.z; acc[r].w += wx * gx.w;
+      }
+    if (c0 >= chunks) continue;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (!live[r]) continue;
+      float4 v = keep[r];
+      v.x -= lr * acc[r].x; v.y -= lr * acc[r].y; v.z -= lr * acc[r].z; v.w -= lr * acc[r].w;
+      *reinterpret_cast<float4*>(table + static_cast<int64_t>(trow[r]) * d + 4 * c) = v;
+    }
+  }
+}
+
+// The sources with long transpose lists, one workgroup per row (grid-
+// stride over the list): the eight 32-lane groups take the entries
+// j = g, g + 8, ... four at a time (one round of entry reads, then one of
+// dM rows), lane c covers the float4 columns c, c + 32, ...; the groups'
+// sums meet in LDS in a fixed order, then the row is finished as in
+// k_pull_mean (UPDATE = false: masked by the layer below's output, written
+// to dH) or k_pull_update (UPDATE = true: applied to the table row).
+template <bool UPDATE>
+__global__ __launch_bounds__(256) void k_pull_long(const int32_t* __restrict__ sizes,
+                                                   const uint32_t* __restrict__ n_long,
+                                                   const int32_t* __restrict__ long_rows,
+                                                   const int32_t* __restrict__ off, const int2* __restrict__ csc,
+                                                   int64_t cap_nnz, const float* __restrict__ dM,
+                                                   const float* __restrict__ out, int d, float* __restrict__ dH,
+                                                   float* __restrict__ table, const int32_t* __restrict__ ids,
+                                                   int64_t num_nodes, float lr) {
+  constexpr int kGroups = 8, E = 4;
+  __shared__ float4 part[kGroups - 1][32];
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  const int32_t n_src = load_size(&sizes[kNSrc]);
+  const int32_t nl = static_cast<int32_t>(__hip_atomic_load(n_long, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  const int grp = threadIdx.x >> 5, lane = threadIdx.x & 31;
+  const int chunks = d / 4;
+  for (int32_t li = blockIdx.x; li < nl; li += gridDim.x) {
+    const int32_t u = long_rows[li];
+    if (u < 0 || u >= n_src) continue;   // uniform over the workgroup
+    int32_t s0 = off[u], s1 = off[u + 1];
+    s0 = s0 < 0 ? 0 : s0;
+    s1 = s1 > cap_nnz ? static_cast<int32_t>(cap_nnz) : s1;
+    const int32_t cnt = s1 > s0 ? s1 - s0 : 0;
+    int64_t trow = 0;
+    bool live = true;
+    if (UPDATE) {
+      const int32_t id = ids[u];
+      live = id >= 0 && id < num_nodes;
+      trow = live ? id : 0;
+    }
+    for (int c0 = lane; c0 < chunks + 31 - (chunks - 1) % 32; c0 += 32) {   // whole passes
+      const int c = c0 < chunks ? c0 : chunks - 1;
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int32_t base = grp; base < cnt; base += kGroups * E) {
+        int2 e[E];
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+          const int32_t k = base + j * kGroups;
+          e[j] = csc[k < cnt ? s0 + k : s0];
+        }
+        float4 g[E];
+        float w[E];
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+          const bool ok = base + j * kGroups < cnt && e[j].x >= 0 && e[j].x < n_dst;
+          w[j] = ok ? __int_as_float(e[j].y) : 0.f;
+          g[j] = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? e[j].x : 0) * d + 4 * c);
+        }
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+          acc.x += w[j] * g[j].x; acc.y += w[j] * g[j].y; acc.z += w[j] * g[j].z; acc.w += w[j] * g[j].w;
+        }
+      }
+      if (grp > 0) part[grp - 1][lane] = acc;
+      __syncthreads();
+      if (grp == 0) {
+#pragma unroll
+        for (int k = 0; k < kGroups - 1; ++k) {
+          const float4 x = part[k][lane];
+          acc.x += x.x; acc.y += x.y; acc.z += x.z; acc.w += x.w;
+        }
+        const int64_t at = static_cast<int64_t>(u) * d + 4 * c;
+        if (u < n_dst) {
+          const float4 x = *reinterpret_cast<const float4*>(dH + at);
+          acc.x += x.x; acc.y += x.y; acc.z += x.z; acc.w += x.w;
+        }
+        if (c0 < chunks) {
+          if (UPDATE) {
+            if (live) {
+              float4* t = reinterpret_cast<float4*>(table + trow * d + 4 * c);
+              float4 v = *t;
+              v.x -= lr * acc.x; v.y -= lr * acc.y; v.z -= lr * acc.z; v.w -= lr * acc.w;
+              *t = v;
+            }
+          } else {
+            const float4 o = *reinterpret_cast<const float4*>(out + at);
+            acc.x = o.x > 0.f ? acc.x : 0.f;
+            acc.y = o.y > 0.f ? acc.y : 0.f;
+            acc.z = o.z > 0.f ? acc.z : 0.f;
+            acc.w = o.w > 0.f ? acc.w : 0.f;
+            *reinterpret_cast<float4*>(dH + at) = acc;
+          }
+        }
+      }
+      __syncthreads();
+    }
   }
 }
 
@@ -715,29 +942,48 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
 
 int64_t csc_scan_tiles(int64_t cap_src) { return std::max<int64_t>(1, (cap_src + kScanTile - 1) / kScanTile); }
 
+constexpr int kLongGrid = 512;   // workgroups of the long-row kernel (grid-stride over the rows)
+
 hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                 int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
-                                uint32_t* scan_state, int2* csc, hipStream_t s) {
+                                uint32_t* scan_state, int2* csc, int32_t* long_rows, float* table, const int32_t* ids,
+                                int64_t num_nodes, float lr, hipStream_t s) {
   const EdgeView ev{indptr, local, cap_nnz, fanout};
+  // scan_state: [0] the tile ticket, [1] the long-row count, then the
+  // look-back words
   hipLaunchKernelGGL(k_csc_scan, dim3(static_cast<unsigned>(csc_scan_tiles(cap_src))), dim3(256), 0, s, sizes, cnt,
-                     off, pos, scan_state, reinterpret_cast<uint64_t*>(scan_state + 2));
+                     off, pos, scan_state, reinterpret_cast<uint64_t*>(scan_state + 2), scan_state + 1, long_rows);
   const int64_t slots = std::max<int64_t>(cap_dst, 1) * std::max(fanout, 1);
   hipLaunchKernelGGL(k_csc_fill, dim3(grid_of(slots, 1 << 16)), dim3(256), 0, s, sizes, ev, pos, off, csc);
   const int chunks = d / 4;
+  if (table) {
+    constexpr int kG = 32, kR = 4, kE = 2;
+    const dim3 grid(grid_of((std::max<int64_t>(cap_src, 1) + kR - 1) / kR * kG, 1 << 30));
+    hipLaunchKernelGGL((k_pull_update<kG, kR, kE>), grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, dH, d,
+                       table, ids, num_nodes, lr);
+    hipLaunchKernelGGL(k_pull_long<true>, dim3(kLongGrid), dim3(256), 0, s, sizes, scan_state + 1, long_rows, off,
+                       csc, cap_nnz, dM, out, d, const_cast<float*>(dH), table, ids, num_nodes, lr);
+    return hipGetLastError();
+  }
   int G = 64;
   if (chunks <= 4) G = 4;
   else if (chunks <= 8) G = 8;
   else if (chunks <= 16) G = 16;
   else if (chunks <= 32) G = 32;
   const dim3 grid(grid_of(std::max<int64_t>(cap_src, 1) * G, 1 << 30));
+#define GMB_PULL(GG) \
+  hipLaunchKernelGGL((k_pull_mean<GG>), grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH)
   switch (G) {
-    case 4: hipLaunchKernelGGL(k_pull_mean<4>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
-    case 8: hipLaunchKernelGGL(k_pull_mean<8>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
-    case 16: hipLaunchKernelGGL(k_pull_mean<16>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
-    case 32: hipLaunchKernelGGL(k_pull_mean<32>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
-    default: hipLaunchKernelGGL(k_pull_mean<64>, grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH); break;
+    case 4: GMB_PULL(4); break;
+    case 8: GMB_PULL(8); break;
+    case 16: GMB_PULL(16); break;
+    case 32: GMB_PULL(32); break;
+    default: GMB_PULL(64); break;
   }
+  hipLaunchKernelGGL(k_pull_long<false>, dim3(kLongGrid), dim3(256), 0, s, sizes, scan_state + 1, long_rows, off, csc,
+                     cap_nnz, dM, out, d, dH, nullptr, nullptr, num_nodes, lr);
+#undef GMB_PULL
   return hipGetLastError();
 }
 

@@ -280,3 +280,44 @@ def test_every_batch_of_the_epoch(orc, setup):
     csr.check_status()
     print(f"{cfg.name}: {nb} batches bit-exact (sampling, relabel, gather); forward of the first {n_fwd}: "
           f"max rel. error {worst:.2e}", flush=True)
+
+
+def test_full_size_embedding_step(orc, dg, setup):
+    """Batch 0 with the features as learnable vertex embeddings (fp32
+    workloads): the sparse update of the table against the oracle, every
+    row outside the batch untouched (margin biases as in the training-step
+    test)."""
+    wl, csr, feats, _, _, _ = setup
+    cfg, g = wl.cfg, wl.graph
+    if cfg.feat_dtype != "f32":
+        pytest.skip("the training step is fp32 only")
+    seeds = wl.batches[0]
+    ref = orc.sample_blocks(g.indptr, g.indices, seeds, list(cfg.fanouts), wl.batch_key(0))
+    X = orc.gather(wl.feats, ref[0].src).astype(np.float64)
+    w = types.SimpleNamespace(**vars(wl.weights))
+    w.bias = margin_biases(orc, ref, X, wl.weights)
+    w.as_f64 = lambda: ([a.astype(np.float64) for a in w.w_self], [a.astype(np.float64) for a in w.w_neigh],
+                        [b.astype(np.float64) for b in w.bias])
+    wt = to_torch_weights(w)
+    table = feats.clone()
+    lane = Lane(csr, wl, table, wt)
+    blocks, x, logits, _ = lane.run(wl, table, wt, 0)
+    labels = dg.labels(g.num_nodes, cfg.dims[-1], 7)[seeds]
+    emb_lr = 0.5
+    _, loss = gmb.sage_backward(blocks, x, wt, logits, torch.from_numpy(labels).cuda(), lane.ws_fwd,
+                                embedding=table, emb_lr=emb_lr)
+    torch.cuda.synchronize()
+    ws, wn, bs = w.as_f64()
+    ref_loss, _, dX, _, _ = orc.sage_train_step_embed(ref, wl.feats, ws, wn, bs, labels, 0.0, 0.0)
+    assert abs(loss.item() - ref_loss) <= 1e-5 * max(1.0, abs(ref_loss))
+    src = np.asarray(ref[0].src, dtype=np.int64)
+    got = table.cpu().numpy()
+    rest = np.ones(g.num_nodes, dtype=bool)
+    rest[src] = False
+    assert np.array_equal(got[rest], wl.feats[rest]), "rows outside the mini-batch changed"
+    want = wl.feats[src].astype(np.float64) - emb_lr * dX
+    bound = emb_lr * 1e-4 * np.abs(dX).max() + 2.0 ** -23 * np.abs(want).max()
+    err = np.abs(got[src].astype(np.float64) - want).max()
+    print(f"{cfg.name}: {len(src)} embedding rows updated, max error {err:.2e} (bound {bound:.2e})", flush=True)
+    assert err <= bound
+    csr.check_status()

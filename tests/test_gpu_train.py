@@ -35,9 +35,11 @@ from gpu_util import (assert_blocks_equal, compare_train_step, csr_on_device, gp
 from gpu_util import TOL_GRAD  # noqa: E402
 
 
-def exact_graph(n, seed, min_deg=8, spread=9):
+def exact_graph(n, seed, min_deg=8, spread=9, broadcaster=None):
     """In-degree 0 for every 7th vertex, else min_deg .. min_deg+spread-1
-    distinct sources (no self-loops)."""
+    distinct sources (no self-loops).  With a broadcaster vertex b, b is
+    one of the sources of every other non-empty row, so it is sampled by
+    many destinations and its transpose list is long on every layer."""
     rng = np.random.default_rng(seed)
     deg = np.where(np.arange(n) % 7 == 0, 0, min_deg + rng.integers(0, spread, n))
     indptr = np.zeros(n + 1, dtype=np.int64)
@@ -46,6 +48,8 @@ def exact_graph(n, seed, min_deg=8, spread=9):
     for v, d in enumerate(deg):
         u = rng.choice(n - 1, int(d), replace=False)
         u[u >= v] += 1
+        if broadcaster is not None and d and v != broadcaster and broadcaster not in u:
+            u[0] = broadcaster
         rows.append(np.sort(u))
     indices = np.concatenate(rows).astype(np.int32) if rows else np.zeros(0, np.int32)
     return types.SimpleNamespace(num_nodes=n, indptr=indptr, indices=indices)
@@ -211,4 +215,131 @@ def test_train_step_on_fused_forward(orc, dg):
     assert_hidden_exact(orc, ref_blocks, X, w)
     out = dict(hidden=hidden, grads=grads, loss=float(loss.item()), before=before)
     compare_train_step(orc, out, ref_blocks, X, w, labels, 0.25, wt, exact_hidden=True)
+    csr.check_status()
+
+
+# ---- learnable vertex embeddings ---------------------------------------------
+
+def check_embedding_update(orc, table_before, table_after, ref_blocks, ref_table, dX, emb_lr):
+    """Rows of the batch's input vertices against the oracle's update; every
+    other row untouched, bit for bit."""
+    got = table_after.cpu().numpy()
+    before = table_before.cpu().numpy()
+    src = np.asarray(ref_blocks[0].src, dtype=np.int64)
+    rest = np.ones(len(before), dtype=bool)
+    rest[src] = False
+    assert np.array_equal(got[rest], before[rest]), "rows outside the mini-batch changed"
+    want = ref_table[src]
+    bound = emb_lr * TOL_GRAD * max(np.abs(dX).max(), 1e-30) + 2.0 ** -23 * np.abs(want).max()
+    err = np.abs(got[src].astype(np.float64) - want).max()
+    print(f"embedding rows: {len(src)} updated, max error {err:.2e} (bound {bound:.2e})", flush=True)
+    assert err <= bound, (err, bound)
+    assert np.abs(dX).max() == 0.0 or not np.array_equal(got[src], before[src])
+
+
+@pytest.mark.parametrize("dims,fanouts,n_seeds,fused", [([16, 32, 8], [4, 2], 64, False),
+                                                         ([24, 64, 640, 10], [2, 4, 8], 50, True),
+                                                         ([100, 256, 256, 47], [8, 4, 2], 200, False),
+                                                         ([100, 256, 256, 47], [8, 4, 2], 200, True),
+                                                         ([12, 5], [4], 33, True)])
+def test_embedding_train_step_matches_the_oracle(orc, dg, dims, fanouts, n_seeds, fused):
+    """Inputs are learnable vertex embeddings: the weight gradients, the loss
+    and the sparse update of the table rows against the oracle, through the
+    gathered or the fused forward."""
+    n = 3000
+    g = exact_graph(n, 81 + len(dims))
+    table_np, w = exact_model(dg, n, dims, 82 + dims[1])
+    seeds = dg.permutation(n, 83)[:n_seeds]
+    labels = dg.labels(n, dims[-1], 84)[seeds]
+    key, lr, emb_lr = 85, 0.25, 0.5
+    print(f"dims {dims} fan-outs {fanouts} seeds {n_seeds} fused {fused}", flush=True)
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    table = torch.from_numpy(table_np.copy()).cuda()
+    blocks, host = gpu_blocks(csr, seeds, fanouts, key)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), table.device)[1]
+    if fused:
+        logits, x, hidden = gmb.sage_forward_fused(blocks, table, wt, workspace=ws_fwd, return_hidden=True)
+    else:
+        x = gmb.gather_features(blocks, table)
+        logits, hidden = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd, return_hidden=True)
+    table_before = table.clone()
+    y = torch.from_numpy(labels).cuda()
+    grads, loss = gmb.sage_backward(blocks, x, wt, logits, y, ws_fwd, embedding=table, emb_lr=emb_lr)
+    before = [[t.clone() for t in arrs] for arrs in (wt.w_self, wt.w_neigh, wt.bias)]
+    gmb.sgd_update(wt, grads, lr)
+    torch.cuda.synchronize()
+    ref_blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, key)
+    assert_blocks_equal(host, ref_blocks)
+    X = table_np[np.asarray(ref_blocks[0].src, dtype=np.int64)].astype(np.float64)
+    assert_hidden_exact(orc, ref_blocks, X, w)
+    out = dict(hidden=hidden, grads=grads, loss=float(loss.item()), before=before)
+    compare_train_step(orc, out, ref_blocks, X, w, labels, lr, wt, exact_hidden=True)
+    ws, wn, bs = w.as_f64()
+    _, _, dX, _, ref_table = orc.sage_train_step_embed(ref_blocks, table_np.astype(np.float64), ws, wn, bs, labels,
+                                                        lr, emb_lr)
+    check_embedding_update(orc, table_before, table, ref_blocks, ref_table, dX, emb_lr)
+    csr.check_status()
+
+
+def test_embedding_backward_rejects_unsupported(dg):
+    """An input width that is not a multiple of 4 is refused before any
+    launch."""
+    n = 2000
+    g = dg.er_directed(n, 8.0, 91)
+    csr = csr_on_device(g)
+    seeds = dg.permutation(n, 92)[:16]
+    blocks, _ = gpu_blocks(csr, seeds, [3, 3], 93)
+    w = dg.sage_weights([10, 8, 4], 94)
+    wt = to_torch_weights(w)
+    table = torch.from_numpy(dg.features(n, 10, 95, "f32")).cuda()
+    x = gmb.gather_features(blocks, table)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), table.device)[1]
+    logits = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd)
+    labels = torch.zeros(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(gmb.GmbError):
+        gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd, embedding=table, emb_lr=0.1)
+
+
+@pytest.mark.parametrize("embed", [False, True])
+def test_long_transpose_lists(orc, dg, embed):
+    """A broadcaster vertex sampled by hundreds of destinations on every
+    layer: its transpose lists take the workgroup-per-row kernel (the masked
+    pull on the hidden layers, the table update on layer 0)."""
+    n, dims, fanouts, n_seeds = 3000, [16, 32, 32, 6], [4, 8, 4], 400
+    g = exact_graph(n, 101, broadcaster=5)
+    table_np, w = exact_model(dg, n, dims, 102)
+    seeds = dg.permutation(n, 103)[:n_seeds]
+    seeds = seeds[seeds != 5]
+    labels = dg.labels(n, dims[-1], 104)[seeds]
+    lr, emb_lr = 0.25, 0.5
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    table = torch.from_numpy(table_np.copy()).cuda()
+    blocks, host = gpu_blocks(csr, seeds, fanouts, 105)
+    for l, h in enumerate(host):
+        k = int((h["nbr"] == 5).sum())
+        print(f"layer {l}: the broadcaster is sampled {k} times", flush=True)
+        assert k > 16
+    x = gmb.gather_features(blocks, table)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), table.device)[1]
+    logits, hidden = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd, return_hidden=True)
+    table_before = table.clone()
+    y = torch.from_numpy(labels).cuda()
+    kw = dict(embedding=table, emb_lr=emb_lr) if embed else {}
+    grads, loss = gmb.sage_backward(blocks, x, wt, logits, y, ws_fwd, **kw)
+    before = [[t.clone() for t in arrs] for arrs in (wt.w_self, wt.w_neigh, wt.bias)]
+    gmb.sgd_update(wt, grads, lr)
+    torch.cuda.synchronize()
+    ref_blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, 105)
+    assert_blocks_equal(host, ref_blocks)
+    X = table_np[np.asarray(ref_blocks[0].src, dtype=np.int64)].astype(np.float64)
+    assert_hidden_exact(orc, ref_blocks, X, w)
+    out = dict(hidden=hidden, grads=grads, loss=float(loss.item()), before=before)
+    compare_train_step(orc, out, ref_blocks, X, w, labels, lr, wt, exact_hidden=True)
+    if embed:
+        ws, wn, bs = w.as_f64()
+        _, _, dX, _, ref_table = orc.sage_train_step_embed(ref_blocks, table_np.astype(np.float64), ws, wn, bs,
+                                                            labels, lr, emb_lr)
+        check_embedding_update(orc, table_before, table, ref_blocks, ref_table, dX, emb_lr)
     csr.check_status()
