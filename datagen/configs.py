@@ -65,10 +65,12 @@ CONFIGS = {
                      (401, 402, 403, 404, 405), rmat_scale=22, rmat_draws=90_600_000,
                      rmat_abc=(0.45, 0.22, 0.22), hubs=100, hub_deg=100_000,
                      train_fraction=0.08, base_graph="products2m"),
-    # 111M-node R-MAT shaped like Table I's citation graph (int64 indptr).
+    # 111M-node R-MAT shaped like Table I's citation graph (int64 indptr):
+    # scale 27 rejected to N = 111,059,956; 2.41e9 draws give ~3.23e9
+    # symmetrised edges (calibrated once: 2.5e9 draws gave 3,350,569,258).
     "papers111m": Config("papers111m", "rmat", 111_059_956, 128, "bf16", (128, 256, 256, 172),
                          (15, 10, 5), 1000, (501, 502, 503, 504, 505), rmat_scale=27,
-                         rmat_draws=0, rmat_abc=(0.57, 0.19, 0.19), train_fraction=0.01),
+                         rmat_draws=2_410_000_000, rmat_abc=(0.57, 0.19, 0.19), train_fraction=0.01),
 }
 
 

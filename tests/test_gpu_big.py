@@ -1,0 +1,79 @@
+"""GPU parity on the 111M-node workload (3.2e9 edges, int64 row offsets,
+bf16 x128, fan-outs 15/10/5, batch 1000): the first 32 batches of the epoch
+bit for bit for sampling, relabel and gather, the forward of the first 4
+within 2e-2.  Generating the workload takes a few minutes and about 90 GB of
+host memory, so the test runs only when GMB_BIG=1 is set.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU on this machine", allow_module_level=True)
+if os.environ.get("GMB_BIG") != "1":
+    pytest.skip("the 111M-node workload runs with GMB_BIG=1", allow_module_level=True)
+
+import paper_2010_05337_amd as gmb  # noqa: E402
+from datagen.configs import make_workload  # noqa: E402
+from gpu_util import assert_blocks_equal, rowwise_rel_err, tensor_bits, tensor_f64, to_torch_weights  # noqa: E402
+
+
+def test_papers111m_first_batches(orc):
+    from concurrent.futures import ThreadPoolExecutor
+    wl = make_workload("papers111m")
+    cfg, g = wl.cfg, wl.graph
+    deg = g.degrees()
+    print(f"papers111m: N={g.num_nodes} E={g.num_edges} ({g.num_edges / 3_231_371_744:.4f} of 3,231,371,744) "
+          f"max deg={deg.max()} mean={deg.mean():.2f} p50={np.median(deg):.0f} p99={np.percentile(deg, 99):.0f} "
+          f"isolated={(deg == 0).mean():.3f}", flush=True)
+    assert g.num_edges > 2 ** 31, "the workload must need 64-bit row offsets"
+    ip = torch.from_numpy(g.indptr).cuda()
+    ix = torch.from_numpy(g.indices).cuda()
+    csr = gmb.CSRGraph(ip, ix)
+    feats = torch.from_numpy(wl.feats.view(np.int16)).cuda().view(torch.bfloat16)
+    weights = to_torch_weights(wl.weights)
+    ws, wn, bs = wl.weights.as_f64()
+    nb = min(32, len(wl.batches))
+    n_fwd = 4
+    orc.lib()
+
+    def oracle_batch(b):
+        ref = orc.sample_blocks(g.indptr, g.indices, wl.batches[b], list(cfg.fanouts), wl.batch_key(b))
+        X = orc.gather(wl.feats, ref[0].src)
+        logits = orc.sage_forward(ref, orc.widen(X, cfg.feat_dtype), ws, wn, bs)[0] if b < n_fwd else None
+        return ref, X, logits
+
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    worst = 0.0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        futs = [ex.submit(oracle_batch, b) for b in range(nb)]
+        for b in range(nb):
+            s = torch.from_numpy(wl.batches[b]).cuda()
+            blocks = gmb.sample_blocks(csr, s, list(cfg.fanouts), wl.batch_key(b))
+            x = gmb.gather_features(blocks, feats)
+            logits = gmb.sage_forward(blocks, x, weights)
+            host = []
+            for blk in blocks.blocks():
+                host.append(dict(n_dst=blk.n_dst, n_src=blk.n_src, nnz=blk.nnz,
+                                 indptr=blk.indptr.cpu().numpy().astype(np.int64),
+                                 local=blk.indices.cpu().numpy().astype(np.int64),
+                                 nbr=blk.nbr.cpu().numpy().astype(np.int64),
+                                 src=blk.src_ids.cpu().numpy().astype(np.int64)))
+            ref, X, ref_logits = futs[b].result()
+            futs[b] = None
+            assert_blocks_equal(host, ref, f"papers111m batch {b}")
+            got = tensor_bits(x)[:ref[0].n_src]
+            assert got.view(np.uint8).tobytes() == X.view(np.uint8).tobytes(), f"batch {b}: gathered rows differ"
+            if ref_logits is not None:
+                e = rowwise_rel_err(tensor_f64(logits), ref_logits)
+                worst = max(worst, e)
+                assert e <= 2e-2, (b, e)
+            if b == 0:
+                print(f"  batch 0 sizes {[(r.n_dst, r.n_src, r.nnz) for r in ref]}", flush=True)
+    csr.check_status()
+    print(f"papers111m: {nb} batches bit-exact (sampling, relabel, gather); forward of the first {n_fwd}: "
+          f"max rel. error {worst:.2e}", flush=True)
