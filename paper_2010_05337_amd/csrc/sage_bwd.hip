@@ -26,6 +26,8 @@
 //                  the ReLU of the layer below applied on the way out
 //   k_pull_update  on layer 0 with learnable vertex embeddings: the same
 //                  sum applied at once as the sparse SGD step of the rows
+//                  (both end their grids with workgroups that take the
+//                  sources with long transpose lists, hubs, one each)
 //   k_sgd          W -= lr dW over every parameter array
 #include <algorithm>
 
@@ -115,7 +117,8 @@ __global__ __launch_bounds__(256) void k_loss_sum(const float* __restrict__ rows
 constexpr int kWgradRed = 2 * 64 * 64;   // LDS floats of the cross-wave sum
 
 template <bool VEC>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
                                                const float* __restrict__ M, int d_in,
                                                const float* __restrict__ dZ, int ldz, int ldp,
                                                float* __restrict__ partial) {
@@ -589,180 +592,21 @@ __global__ __launch_bounds__(256) void k_csc_fill(const int32_t* __restrict__ si
                      });
 }
 
-// G lanes per source row u, lane c covers columns 4c, 4c + G, ... (d % 4 ==
-// 0): g = (u < n_dst ? dH[u] : 0) + sum over u's transpose entries (v, w) of
-// w * dM[v].  UPDATE = false: dH[u] = (out[u] > 0) * g (out: the layer
-// below's output).  UPDATE = true (layer 0 with learnable vertex
-// embeddings): table[ids[u]] -= lr * g, a plain read-modify-write (the rows
-// of one mini-batch are distinct; mini-batches in flight together update
-// without locks, as Hogwild does); an id outside [0, num_nodes) skips the
-// row (only after a data error).
-template <int G>
-__global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ sizes,
-                                                   const int32_t* __restrict__ off, const int2* __restrict__ csc,
-                                                   int64_t cap_nnz, const float* __restrict__ dM,
-                                                   const float* __restrict__ out, int d, float* __restrict__ dH) {
-  const int32_t n_dst = load_size(&sizes[kNDst]);
-  const int32_t n_src = load_size(&sizes[kNSrc]);
-  const int64_t u = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
-  const int lane = threadIdx.x & (G - 1);
-  if (u >= n_src) return;
-  int32_t s0 = off[u], s1 = off[u + 1];
-  if (s1 - s0 > kLongList) return;   // k_pull_long's row
-  s0 = s0 < 0 ? 0 : s0;
-  s1 = s1 > cap_nnz ? static_cast<int32_t>(cap_nnz) : s1;
-  const bool self = u < n_dst;
-  const int chunks = d / 4;
-  for (int c = lane; c < chunks; c += G) {
-    const int64_t at = u * d + 4 * c;
-    // the layer below's output does not depend on the gradient: read first
-    const float4 o = *reinterpret_cast<const float4*>(out + at);
-    float4 acc = self ? *reinterpret_cast<const float4*>(dH + at) : make_float4(0.f, 0.f, 0.f, 0.f);
-    int32_t s = s0;
-    for (; s + 1 < s1; s += 2) {
-      const int2 e0 = csc[s], e1 = csc[s + 1];
-      const bool ok0 = e0.x >= 0 && e0.x < n_dst, ok1 = e1.x >= 0 && e1.x < n_dst;
-      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
-      const float4 g1 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok1 ? e1.x : 0) * d + 4 * c);
-      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f, w1 = ok1 ? __int_as_float(e1.y) : 0.f;
-      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
-      acc.x += w1 * g1.x; acc.y += w1 * g1.y; acc.z += w1 * g1.z; acc.w += w1 * g1.w;
-    }
-    if (s < s1) {
-      const int2 e0 = csc[s];
-      const bool ok0 = e0.x >= 0 && e0.x < n_dst;
-      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
-      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f;
-      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
-    }
-    acc.x = o.x > 0.f ? acc.x : 0.f;
-    acc.y = o.y > 0.f ? acc.y : 0.f;
-    acc.z = o.z > 0.f ? acc.z : 0.f;
-    acc.w = o.w > 0.f ? acc.w : 0.f;
-    *reinterpret_cast<float4*>(dH + at) = acc;
-  }
-}
-
-// Layer 0 with learnable vertex embeddings: table[ids[u]] -= lr * g_u with
-// g_u = (u < n_dst ? dH[u] : 0) + sum over u's transpose entries (v, w) of
-// w * dM[v], as a plain read-modify-write (the rows of one mini-batch are
-// distinct; mini-batches in flight together update without locks, as
-// Hogwild does; an id outside [0, num_nodes) skips its row).  The update is
-// bound by the latency of three dependent rounds of reads per row (offsets
-// and ids; table row, self part and the first entries; the entries' dM
-// rows), so each G-lane group takes R rows and issues every round for all
-// of them at once; entries past the first E of a row (few rows have them)
-// follow one by one.  Lane c covers the float4 columns c, c + G, ...
-template <int G, int R, int E>
-__global__ __launch_bounds__(256) void k_pull_update(const int32_t* __restrict__ sizes,
-                                                     const int32_t* __restrict__ off,
-                                                     const int2* __restrict__ csc, int64_t cap_nnz,
-                                                     const float* __restrict__ dM, const float* __restrict__ dH,
-                                                     int d, float* __restrict__ table,
-                                                     const int32_t* __restrict__ ids, int64_t num_nodes, float lr) {
-  const int32_t n_dst = load_size(&sizes[kNDst]);
-  const int32_t n_src = load_size(&sizes[kNSrc]);
-  const int64_t group = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
-  const int lane = threadIdx.x & (G - 1);
-  const int64_t u0 = group * R;
-  if (u0 >= n_src) return;
-  // round 1: the rows' offsets and table ids
-  int32_t s0[R], cnt[R], trow[R];
-  bool live[R], self[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int64_t u = u0 + r;
-    const int64_t uc = u < n_src ? u : u0;
-    int32_t a = off[uc], b = off[uc + 1];
-    const int32_t id = ids[uc];
-    const bool long_list = b - a > kLongList;   // k_pull_long's row
-    a = a < 0 ? 0 : a;
-    b = b > cap_nnz ? static_cast<int32_t>(cap_nnz) : b;
-    s0[r] = a;
-    cnt[r] = b > a && !long_list ? b - a : 0;
-    live[r] = u < n_src && id >= 0 && id < num_nodes && !long_list;
-    trow[r] = live[r] ? id : 0;
-    self[r] = u < n_dst;
-  }
-  const int chunks = d / 4;
-  for (int c0 = lane; c0 < chunks + G - 1 - (chunks - 1) % G; c0 += G) {   // whole passes of the group
-    const int c = c0 < chunks ? c0 : chunks - 1;
-    // round 2: table rows, self parts, the first E entries of every row
-    float4 keep[R], acc[R];
-    int2 e[R][E];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      keep[r] = *reinterpret_cast<const float4*>(table + static_cast<int64_t>(trow[r]) * d + 4 * c);
-      acc[r] = *reinterpret_cast<const float4*>(dH + (self[r] ? u0 + r : 0) * d + 4 * c);
-#pragma unroll
-      for (int j = 0; j < E; ++j) e[r][j] = csc[j < cnt[r] ? s0[r] + j : 0];
-    }
-    // round 3: the entries' dM rows
-    float4 g[R][E];
-    float w[R][E];
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int j = 0; j < E; ++j) {
-        const bool ok = j < cnt[r] && e[r][j].x >= 0 && e[r][j].x < n_dst;
-        w[r][j] = ok ? __int_as_float(e[r][j].y) : 0.f;
-        g[r][j] = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? e[r][j].x : 0) * d + 4 * c);
-      }
-    // (the table rows and self parts are used unconditionally from here, so
-    // the compiler cannot turn their reads into branched ones; the step
-    // comes after the dM reads are issued so that all of them overlap)
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      asm volatile("" : "+v"(keep[r].x), "+v"(keep[r].y), "+v"(keep[r].z), "+v"(keep[r].w));
-      asm volatile("" : "+v"(acc[r].x), "+v"(acc[r].y), "+v"(acc[r].z), "+v"(acc[r].w));
-      if (!self[r]) acc[r] = make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int j = 0; j < E; ++j) {
-        acc[r].x += w[r][j] * g[r][j].x;
-        acc[r].y += w[r][j] * g[r][j].y;
-        acc[r].z += w[r][j] * g[r][j].z;
-        acc[r].w += w[r][j] * g[r][j].w;
-      }
-    // the rest of the longer lists
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-      for (int32_t j = E; j < cnt[r]; ++j) {
-        const int2 x = csc[s0[r] + j];
-        const bool ok = x.x >= 0 && x.x < n_dst;
-        const float4 gx = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? x.x : 0) * d + 4 * c);
-        const float wx = ok ? __int_as_float(x.y) : 0.f;
-        acc[r].x += wx * gx.x; acc[r].y += wx * gx.y; acc[r].z += wx * gx.z; acc[r].w += wx * gx.w;
-      }
-    if (c0 >= chunks) continue;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      if (!live[r]) continue;
-      float4 v = keep[r];
-      v.x -= lr * acc[r].x; v.y -= lr * acc[r].y; v.z -= lr * acc[r].z; v.w -= lr * acc[r].w;
-      *reinterpret_cast<float4*>(table + static_cast<int64_t>(trow[r]) * d + 4 * c) = v;
-    }
-  }
-}
-
-// The sources with long transpose lists, one workgroup per row (grid-
-// stride over the list): the eight 32-lane groups take the entries
+// The sources with long transpose lists, one workgroup per row (the n_wg
+// workgroups that the row kernels append to their grids stride over the
+// list; wg is this one's index among them): the eight 32-lane groups take the entries
 // j = g, g + 8, ... four at a time (one round of entry reads, then one of
 // dM rows), lane c covers the float4 columns c, c + 32, ...; the groups'
 // sums meet in LDS in a fixed order, then the row is finished as in
 // k_pull_mean (UPDATE = false: masked by the layer below's output, written
 // to dH) or k_pull_update (UPDATE = true: applied to the table row).
 template <bool UPDATE>
-__global__ __launch_bounds__(256) void k_pull_long(const int32_t* __restrict__ sizes,
-                                                   const uint32_t* __restrict__ n_long,
-                                                   const int32_t* __restrict__ long_rows,
-                                                   const int32_t* __restrict__ off, const int2* __restrict__ csc,
-                                                   int64_t cap_nnz, const float* __restrict__ dM,
-                                                   const float* __restrict__ out, int d, float* __restrict__ dH,
-                                                   float* __restrict__ table, const int32_t* __restrict__ ids,
-                                                   int64_t num_nodes, float lr) {
+__device__ void pull_long_rows(int wg, int n_wg, const int32_t* __restrict__ sizes,
+                               const uint32_t* __restrict__ n_long, const int32_t* __restrict__ long_rows,
+                               const int32_t* __restrict__ off, const int2* __restrict__ csc, int64_t cap_nnz,
+                               const float* __restrict__ dM, const float* __restrict__ out, int d,
+                               float* __restrict__ dH, float* __restrict__ table, const int32_t* __restrict__ ids,
+                               int64_t num_nodes, float lr) {
   constexpr int kGroups = 8, E = 4;
   __shared__ float4 part[kGroups - 1][32];
   const int32_t n_dst = load_size(&sizes[kNDst]);
@@ -770,7 +614,7 @@ __global__ __launch_bounds__(256) void k_pull_long(const int32_t* __restrict__ s
   const int32_t nl = static_cast<int32_t>(__hip_atomic_load(n_long, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
   const int grp = threadIdx.x >> 5, lane = threadIdx.x & 31;
   const int chunks = d / 4;
-  for (int32_t li = blockIdx.x; li < nl; li += gridDim.x) {
+  for (int32_t li = wg; li < nl; li += n_wg) {
     const int32_t u = long_rows[li];
     if (u < 0 || u >= n_src) continue;   // uniform over the workgroup
     int32_t s0 = off[u], s1 = off[u + 1];
@@ -839,6 +683,178 @@ __global__ __launch_bounds__(256) void k_pull_long(const int32_t* __restrict__ s
         }
       }
       __syncthreads();
+    }
+  }
+}
+
+// G lanes per source row u, lane c covers columns 4c, 4c + G, ... (d % 4 ==
+// 0): g = (u < n_dst ? dH[u] : 0) + sum over u's transpose entries (v, w) of
+// w * dM[v].  UPDATE = false: dH[u] = (out[u] > 0) * g (out: the layer
+// below's output).  UPDATE = true (layer 0 with learnable vertex
+// embeddings): table[ids[u]] -= lr * g, a plain read-modify-write (the rows
+// of one mini-batch are distinct; mini-batches in flight together update
+// without locks, as Hogwild does); an id outside [0, num_nodes) skips the
+// row (only after a data error).
+template <int G>
+__global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ sizes,
+                                                   const int32_t* __restrict__ off, const int2* __restrict__ csc,
+                                                   int64_t cap_nnz, const float* __restrict__ dM,
+                                                   const float* __restrict__ out, int d, float* __restrict__ dH,
+                                                   int row_blocks, const uint32_t* __restrict__ n_long,
+                                                   const int32_t* __restrict__ long_rows) {
+  if (static_cast<int>(blockIdx.x) >= row_blocks) {   // the long lists
+    pull_long_rows<false>(blockIdx.x - row_blocks, gridDim.x - row_blocks, sizes, n_long, long_rows, off, csc,
+                          cap_nnz, dM, out, d, dH, nullptr, nullptr, 0, 0.f);
+    return;
+  }
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  const int32_t n_src = load_size(&sizes[kNSrc]);
+  const int64_t u = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
+  const int lane = threadIdx.x & (G - 1);
+  if (u >= n_src) return;
+  int32_t s0 = off[u], s1 = off[u + 1];
+  if (s1 - s0 > kLongList) return;   // a long list: the appended workgroups take it
+  s0 = s0 < 0 ? 0 : s0;
+  s1 = s1 > cap_nnz ? static_cast<int32_t>(cap_nnz) : s1;
+  const bool self = u < n_dst;
+  const int chunks = d / 4;
+  for (int c = lane; c < chunks; c += G) {
+    const int64_t at = u * d + 4 * c;
+    // the layer below's output does not depend on the gradient: read first
+    const float4 o = *reinterpret_cast<const float4*>(out + at);
+    float4 acc = self ? *reinterpret_cast<const float4*>(dH + at) : make_float4(0.f, 0.f, 0.f, 0.f);
+    int32_t s = s0;
+    for (; s + 1 < s1; s += 2) {
+      const int2 e0 = csc[s], e1 = csc[s + 1];
+      const bool ok0 = e0.x >= 0 && e0.x < n_dst, ok1 = e1.x >= 0 && e1.x < n_dst;
+      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
+      const float4 g1 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok1 ? e1.x : 0) * d + 4 * c);
+      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f, w1 = ok1 ? __int_as_float(e1.y) : 0.f;
+      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
+      acc.x += w1 * g1.x; acc.y += w1 * g1.y; acc.z += w1 * g1.z; acc.w += w1 * g1.w;
+    }
+    if (s < s1) {
+      const int2 e0 = csc[s];
+      const bool ok0 = e0.x >= 0 && e0.x < n_dst;
+      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
+      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f;
+      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
+    }
+    acc.x = o.x > 0.f ? acc.x : 0.f;
+    acc.y = o.y > 0.f ? acc.y : 0.f;
+    acc.z = o.z > 0.f ? acc.z : 0.f;
+    acc.w = o.w > 0.f ? acc.w : 0.f;
+    *reinterpret_cast<float4*>(dH + at) = acc;
+  }
+}
+
+// Layer 0 with learnable vertex embeddings: table[ids[u]] -= lr * g_u with
+// g_u = (u < n_dst ? dH[u] : 0) + sum over u's transpose entries (v, w) of
+// w * dM[v], as a plain read-modify-write (the rows of one mini-batch are
+// distinct; mini-batches in flight together update without locks, as
+// Hogwild does; an id outside [0, num_nodes) skips its row).  The update is
+// bound by the latency of three dependent rounds of reads per row (offsets
+// and ids; table row, self part and the first entries; the entries' dM
+// rows), so each G-lane group takes R rows and issues every round for all
+// of them at once; entries past the first E of a row (few rows have them)
+// follow one by one.  Lane c covers the float4 columns c, c + G, ...
+template <int G, int R, int E>
+__global__ __launch_bounds__(256) void k_pull_update(const int32_t* __restrict__ sizes,
+                                                     const int32_t* __restrict__ off,
+                                                     const int2* __restrict__ csc, int64_t cap_nnz,
+                                                     const float* __restrict__ dM, float* __restrict__ dH,
+                                                     int d, float* __restrict__ table,
+                                                     const int32_t* __restrict__ ids, int64_t num_nodes, float lr,
+                                                     int row_blocks, const uint32_t* __restrict__ n_long,
+                                                     const int32_t* __restrict__ long_rows) {
+  if (static_cast<int>(blockIdx.x) >= row_blocks) {   // the long lists
+    pull_long_rows<true>(blockIdx.x - row_blocks, gridDim.x - row_blocks, sizes, n_long, long_rows, off, csc,
+                         cap_nnz, dM, nullptr, d, dH, table, ids, num_nodes, lr);
+    return;
+  }
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  const int32_t n_src = load_size(&sizes[kNSrc]);
+  const int64_t group = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / G;
+  const int lane = threadIdx.x & (G - 1);
+  const int64_t u0 = group * R;
+  if (u0 >= n_src) return;
+  // first reads: the rows' offsets and table ids
+  int32_t s0[R], cnt[R], trow[R];
+  bool live[R], self[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t u = u0 + r;
+    const int64_t uc = u < n_src ? u : u0;
+    int32_t a = off[uc], b = off[uc + 1];
+    const int32_t id = ids[uc];
+    const bool long_list = b - a > kLongList;   // the appended workgroups take it
+    a = a < 0 ? 0 : a;
+    b = b > cap_nnz ? static_cast<int32_t>(cap_nnz) : b;
+    s0[r] = a;
+    cnt[r] = b > a && !long_list ? b - a : 0;
+    live[r] = u < n_src && id >= 0 && id < num_nodes && !long_list;
+    trow[r] = live[r] ? id : 0;
+    self[r] = u < n_dst;
+  }
+  const int chunks = d / 4;
+  for (int c0 = lane; c0 < chunks + G - 1 - (chunks - 1) % G; c0 += G) {   // whole passes of the group
+    const int c = c0 < chunks ? c0 : chunks - 1;
+    // second reads: table rows, self parts, the first E entries of every row
+    float4 keep[R], acc[R];
+    int2 e[R][E];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      keep[r] = *reinterpret_cast<const float4*>(table + static_cast<int64_t>(trow[r]) * d + 4 * c);
+      acc[r] = *reinterpret_cast<const float4*>(dH + (self[r] ? u0 + r : 0) * d + 4 * c);
+#pragma unroll
+      for (int j = 0; j < E; ++j) e[r][j] = csc[j < cnt[r] ? s0[r] + j : 0];
+    }
+    // third reads: the entries' dM rows
+    float4 g[R][E];
+    float w[R][E];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const bool ok = j < cnt[r] && e[r][j].x >= 0 && e[r][j].x < n_dst;
+        w[r][j] = ok ? __int_as_float(e[r][j].y) : 0.f;
+        g[r][j] = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? e[r][j].x : 0) * d + 4 * c);
+      }
+    // (the table rows and self parts are used unconditionally from here, so
+    // the compiler cannot turn their reads into branched ones; the step
+    // comes after the dM reads are issued so that all of them overlap)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      asm volatile("" : "+v"(keep[r].x), "+v"(keep[r].y), "+v"(keep[r].z), "+v"(keep[r].w));
+      asm volatile("" : "+v"(acc[r].x), "+v"(acc[r].y), "+v"(acc[r].z), "+v"(acc[r].w));
+      if (!self[r]) acc[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        acc[r].x += w[r][j] * g[r][j].x;
+        acc[r].y += w[r][j] * g[r][j].y;
+        acc[r].z += w[r][j] * g[r][j].z;
+        acc[r].w += w[r][j] * g[r][j].w;
+      }
+    // the rest of the longer lists
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      for (int32_t j = E; j < cnt[r]; ++j) {
+        const int2 x = csc[s0[r] + j];
+        const bool ok = x.x >= 0 && x.x < n_dst;
+        const float4 gx = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? x.x : 0) * d + 4 * c);
+        const float wx = ok ? __int_as_float(x.y) : 0.f;
+        acc[r].x += wx * gx.x; acc[r].y += wx * gx.y; acc[r].z += wx * gx.z; acc[r].w += wx * gx.w;
+      }
+    if (c0 >= chunks) continue;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (!live[r]) continue;
+      float4 v = keep[r];
+      v.x -= lr * acc[r].x; v.y -= lr * acc[r].y; v.z -= lr * acc[r].z; v.w -= lr * acc[r].w;
+      *reinterpret_cast<float4*>(table + static_cast<int64_t>(trow[r]) * d + 4 * c) = v;
     }
   }
 }
@@ -942,7 +958,7 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
 
 int64_t csc_scan_tiles(int64_t cap_src) { return std::max<int64_t>(1, (cap_src + kScanTile - 1) / kScanTile); }
 
-constexpr int kLongGrid = 512;   // workgroups of the long-row kernel (grid-stride over the rows)
+constexpr int kLongGrid = 512;   // workgroups appended for the long lists (grid-stride over them)
 
 hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                 int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
@@ -957,13 +973,13 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
   const int64_t slots = std::max<int64_t>(cap_dst, 1) * std::max(fanout, 1);
   hipLaunchKernelGGL(k_csc_fill, dim3(grid_of(slots, 1 << 16)), dim3(256), 0, s, sizes, ev, pos, off, csc);
   const int chunks = d / 4;
+  // each grid ends with kLongGrid workgroups for the long lists
   if (table) {
     constexpr int kG = 32, kR = 4, kE = 2;
-    const dim3 grid(grid_of((std::max<int64_t>(cap_src, 1) + kR - 1) / kR * kG, 1 << 30));
-    hipLaunchKernelGGL((k_pull_update<kG, kR, kE>), grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, dH, d,
-                       table, ids, num_nodes, lr);
-    hipLaunchKernelGGL(k_pull_long<true>, dim3(kLongGrid), dim3(256), 0, s, sizes, scan_state + 1, long_rows, off,
-                       csc, cap_nnz, dM, out, d, const_cast<float*>(dH), table, ids, num_nodes, lr);
+    const unsigned rows = grid_of((std::max<int64_t>(cap_src, 1) + kR - 1) / kR * kG, 1 << 30);
+    hipLaunchKernelGGL((k_pull_update<kG, kR, kE>), dim3(rows + kLongGrid), dim3(256), 0, s, sizes, off, csc,
+                       cap_nnz, dM, dH, d, table, ids, num_nodes, lr, static_cast<int>(rows), scan_state + 1,
+                       long_rows);
     return hipGetLastError();
   }
   int G = 64;
@@ -971,9 +987,10 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
   else if (chunks <= 8) G = 8;
   else if (chunks <= 16) G = 16;
   else if (chunks <= 32) G = 32;
-  const dim3 grid(grid_of(std::max<int64_t>(cap_src, 1) * G, 1 << 30));
-#define GMB_PULL(GG) \
-  hipLaunchKernelGGL((k_pull_mean<GG>), grid, dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, out, d, dH)
+  const unsigned rows = grid_of(std::max<int64_t>(cap_src, 1) * G, 1 << 30);
+#define GMB_PULL(GG)                                                                                     \
+  hipLaunchKernelGGL((k_pull_mean<GG>), dim3(rows + kLongGrid), dim3(256), 0, s, sizes, off, csc, cap_nnz, dM, \
+                     out, d, dH, static_cast<int>(rows), scan_state + 1, long_rows)
   switch (G) {
     case 4: GMB_PULL(4); break;
     case 8: GMB_PULL(8); break;
@@ -981,8 +998,6 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
     case 32: GMB_PULL(32); break;
     default: GMB_PULL(64); break;
   }
-  hipLaunchKernelGGL(k_pull_long<false>, dim3(kLongGrid), dim3(256), 0, s, sizes, scan_state + 1, long_rows, off, csc,
-                     cap_nnz, dM, out, d, dH, nullptr, nullptr, num_nodes, lr);
 #undef GMB_PULL
   return hipGetLastError();
 }
