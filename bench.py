@@ -55,6 +55,10 @@ def parse():
                     help="print the HBM traffic of the gather and copy kernels from two rocprofv3 "
                          "--pmc runs of this script (FETCH_SIZE, then WRITE_SIZE; CSV output "
                          "under each directory) as JSON and exit")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="DIR",
+                    help="print a markdown table of per-kernel hardware counters from rocprofv3 --pmc "
+                         "runs of this script (CSV output under each directory; one counter set per run) "
+                         "and exit")
     ap.add_argument("--streams", type=int, default=4,
                     help="mini-batches in flight: batch i runs on stream i %% streams, each stream "
                          "with its own sampler state and workspaces")
@@ -235,6 +239,104 @@ def _pmc_per_dispatch(d: str, counter: str):
     return {k: list(v.values()) for k, v in acc.items()}
 
 
+SIMDS = 256 * 4          # MI355X: 256 CUs of 4 SIMDs
+CLOCK_HZ = 2.4e9
+
+
+def summarize_counters(args):
+    """Per kernel, the median over its dispatches of each counter found in
+    the rocprofv3 --pmc runs under the given directories, and derived
+    figures: MFMA busy share of all SIMD cycles over the dispatch
+    (SQ_VALU_MFMA_BUSY_CYCLES summed over the SIMDs), VALU and vector-read
+    instructions per wave, the share of wave time spent waiting, and HBM
+    read and write megabytes per dispatch: FETCH_SIZE and WRITE_SIZE (KiB)
+    each scaled by the factor that makes it read COPY_BYTES on the plain
+    copy of the same run (the copy-kernel dispatches within 20% of the
+    largest)."""
+    import csv
+    import glob
+    import statistics
+    per = {}      # kernel -> counter -> {dispatch: value}
+    dur = {}      # kernel -> {dispatch: ns}
+    for d in args.summarize_counters:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                name = r["Kernel_Name"].replace("gmb::(anonymous namespace)::", "").replace("void ", "")
+                name = name.split("(")[0]
+                if name.startswith("Cijk_"):
+                    name = "library GEMM (the bench's MFMA check)"
+                # one row per launch shape: a kernel that serves several
+                # layers runs each with a grid of its own
+                name = (name, int(r["Grid_Size"]) // max(1, int(r["Workgroup_Size"])))
+                key = (d, r.get("Dispatch_Id", ""))
+                c = per.setdefault(name, {}).setdefault(r["Counter_Name"], {})
+                c[key] = c.get(key, 0.0) + float(r["Counter_Value"])
+                dur.setdefault(name, {})[key] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+
+    def med(name, counter):
+        v = per[name].get(counter)
+        return statistics.median(v.values()) if v else None
+
+    scale = {}
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        v = [x for k in per if "copyBuffer" in k[0] for x in per[k].get(counter, {}).values()]
+        # only a copy of the calibration size (a run without one has small
+        # copies alone, whose counts say nothing about the scale)
+        if v and max(v) * 1024.0 >= COPY_BYTES / 4:
+            big = [x for x in v if x >= 0.8 * max(v)]
+            scale[counter] = COPY_BYTES / (1024.0 * statistics.mean(big))
+
+    rows = []
+    for name in per:
+        if name[0].startswith("at::") or "copyBuffer" in name[0] or "fillBuffer" in name[0]:
+            continue
+        t_ns = statistics.median(dur[name].values())
+        waves = med(name, "SQ_WAVES")
+        mfma = med(name, "SQ_VALU_MFMA_BUSY_CYCLES")
+        row = {"kernel": name[0], "workgroups": name[1],
+               "dispatches": max(len(v) for v in per[name].values()),
+               "us": t_ns / 1e3 if t_ns else None}
+        if mfma is not None and t_ns:
+            row["mfma_busy"] = mfma / (SIMDS * t_ns * 1e-9 * CLOCK_HZ)
+        for c, k in (("SQ_INSTS_VALU", "valu_per_wave"), ("SQ_INSTS_VMEM_RD", "vmem_rd_per_wave")):
+            v = med(name, c)
+            if v is not None and waves:
+                row[k] = v / waves
+        wait, wc = med(name, "SQ_WAIT_ANY"), med(name, "SQ_WAVE_CYCLES")
+        if wait is not None and wc:
+            row["wait_share"] = wait / wc
+        for c, k in (("FETCH_SIZE", "hbm_read_MB"), ("WRITE_SIZE", "hbm_write_MB")):
+            v = med(name, c)
+            if v is not None and c in scale:
+                row[k] = v * 1024.0 * scale[c] / 1e6
+        if "hbm_read_MB" in row and "hbm_write_MB" in row and t_ns:
+            row["hbm_GBps"] = (row["hbm_read_MB"] + row["hbm_write_MB"]) * 1e6 / t_ns
+        v = med(name, "SQ_LDS_BANK_CONFLICT")
+        if v is not None:
+            row["lds_bank_conflict_cycles"] = v
+        rows.append(row)
+    rows.sort(key=lambda r: -(r["us"] or 0) * r["dispatches"])
+    print(f"counter scale from the {COPY_BYTES / 2**30:.0f} GiB copy: "
+          + (", ".join(f"{c} x{f:.3f}" for c, f in scale.items()) or "no such copy in these runs") + "\n")
+    cols = ["kernel", "workgroups", "dispatches", "us", "mfma_busy", "valu_per_wave", "vmem_rd_per_wave",
+            "wait_share", "hbm_read_MB", "hbm_write_MB", "hbm_GBps", "lds_bank_conflict_cycles"]
+    print("| " + " | ".join(cols) + " |")
+    print("|" + "---|" * len(cols))
+    for r in rows:
+        cells = []
+        for c in cols:
+            v = r.get(c)
+            if v is None:
+                cells.append("")
+            elif c == "kernel":
+                cells.append(f"`{v}`")
+            elif isinstance(v, float):
+                cells.append(f"{v:.3f}" if v < 10 else f"{v:,.0f}")
+            else:
+                cells.append(str(v))
+        print("| " + " | ".join(cells) + " |")
+
+
 def summarize_pmc(args):
     """HBM bytes per launch of the gather kernel from FETCH_SIZE and
     WRITE_SIZE (KiB per dispatch), each scaled by the factor that makes the
@@ -301,6 +403,9 @@ def main():
         return
     if args.summarize_pmc:
         summarize_pmc(args)
+        return
+    if args.summarize_counters:
+        summarize_counters(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
@@ -467,20 +572,7 @@ def main():
     for ln in lanes:
         ln["csr"].check_status()
 
-    # a plain device copy of known size: the bandwidth a streaming kernel
-    # reaches on this GPU, and the calibration of the HBM byte counters
-    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
-    dst = torch.empty_like(src)
-    dst.copy_(src)
-    torch.cuda.synchronize()
-    ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    ce[0].record()
-    for _ in range(5):
-        dst.copy_(src)
-    ce[1].record()
-    torch.cuda.synchronize()
-    copy_GBps = 5 * 2 * COPY_BYTES / (ce[0].elapsed_time(ce[1]) / 1e3) / 1e9
-    del src, dst
+    copy_GBps = stream_copy(torch, dev)
 
     # sizes per batch (sampling is a pure function of the batch and its key)
     seeds_total = edges_total = 0
@@ -569,6 +661,23 @@ def backward_flops(sizes, dims) -> int:
         if l > 0:
             total += 2 * n_dst * 2 * dims[l] * dims[l + 1]
     return total
+
+
+def stream_copy(torch, dev):
+    """GB/s of a plain device copy of COPY_BYTES (read + write): the
+    bandwidth a streaming kernel reaches on this GPU, and, under a
+    counter run, the calibration of the HBM byte counters."""
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ce[0].record()
+    for _ in range(5):
+        dst.copy_(src)
+    ce[1].record()
+    torch.cuda.synchronize()
+    return 5 * 2 * COPY_BYTES / (ce[0].elapsed_time(ce[1]) / 1e3) / 1e9
 
 
 def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
@@ -722,6 +831,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         "backward_products_TFLOPs_lower_bound": bwd_flops / tb / 1e12,
         "mfma_peak_TFLOPs": FP32_MFMA_PEAK_TFLOPS,
         "gemm_check": gemm_check(torch, dev),
+        "stream_copy_GBps": stream_copy(torch, dev),
         "gather_GBps": None if args.fused else b_gather / (stage["gather"] / 1e3) / 1e9,
         "loss": {"first": float(loss_h[0]), "last_of_pass_A": float(loss_h[W + K - 1]),
                  "last": float(loss_h[-1])},
