@@ -235,6 +235,18 @@ def test_forward_more_shapes_f32(orc, dg, tiny, dims, fanouts):
     _forward_case(orc, dg, tiny, feats, w, seeds, fanouts, 34, TOL_F32)
 
 
+@pytest.mark.parametrize("d_in", [192, 256, 320])
+def test_forward_wide_inputs_many_rows_f32(orc, dg, tiny, d_in):
+    """K = 2 d_in of 384, 512 and 640 on a layer with over 8192 rows and 256
+    outputs: the fp32 slab kernel with one wave per 16 rows whose A
+    fragments take one register set (reloaded chunk by chunk), as opposed
+    to the two sets of narrower layers."""
+    feats = dg.features(10000, d_in, 61, "f32")
+    w = dg.sage_weights([d_in, 256, 8], 62)
+    seeds = dg.permutation(10000, 63)[:600]
+    _forward_case(orc, dg, tiny, feats, w, seeds, [3, 15], 64, TOL_F32)
+
+
 # ---- the forward with the feature pull folded into layer 0 -----------------
 
 def _fused_case(orc, dg, g, feats, w, seeds, fanouts, key, tol):
