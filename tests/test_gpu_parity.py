@@ -238,9 +238,9 @@ def test_forward_more_shapes_f32(orc, dg, tiny, dims, fanouts):
 @pytest.mark.parametrize("d_in", [192, 256, 320])
 def test_forward_wide_inputs_many_rows_f32(orc, dg, tiny, d_in):
     """K = 2 d_in of 384, 512 and 640 on a layer with over 8192 rows and 256
-    outputs: the fp32 slab kernel with one wave per 16 rows whose A
-    fragments take one register set (reloaded chunk by chunk), as opposed
-    to the two sets of narrower layers."""
+    outputs: the fp32 slab kernel with one wave per 16 rows and 64 columns
+    at its widest slabs (96, 128 and 160 KB of LDS), which the smaller
+    shapes of the other cases never reach."""
     feats = dg.features(10000, d_in, 61, "f32")
     w = dg.sage_weights([d_in, 256, 8], 62)
     seeds = dg.permutation(10000, 63)[:600]
