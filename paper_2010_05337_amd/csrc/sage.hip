@@ -615,22 +615,32 @@ void k_linear_f32_slab(const int32_t* sizes,
   }
 }
 
+// Workgroups per CU of the persistent slab grids.  One: a second
+// workgroup per CU barely shortens a kernel run alone (each workgroup
+// fills its own slab from L2, and that part does not shrink), while the
+// smaller grid leaves CUs, LDS and L2 bandwidth to the kernels other
+// streams run beside it (four-stream inference: +2% seeds/s with fp32
+// features, +1.5% with bf16).
 #ifndef GMB_SLAB_BLOCKS_WIDE
-#define GMB_SLAB_BLOCKS_WIDE 2
+#define GMB_SLAB_BLOCKS_WIDE 1
 #endif
 #ifndef GMB_SLAB_BLOCKS_SPLIT
-#define GMB_SLAB_BLOCKS_SPLIT 2
+#define GMB_SLAB_BLOCKS_SPLIT 1
 #endif
-constexpr int kSlabBlocksWide = GMB_SLAB_BLOCKS_WIDE;    // workgroups per CU, one wave per 16 rows
-constexpr int kSlabBlocksSplit = GMB_SLAB_BLOCKS_SPLIT;  // workgroups per CU, split-K tiles
+#ifndef GMB_SLAB_BLOCKS_BF16
+#define GMB_SLAB_BLOCKS_BF16 1
+#endif
+constexpr int kSlabBlocksWide = GMB_SLAB_BLOCKS_WIDE;    // fp32, one wave per 16 rows
+constexpr int kSlabBlocksSplit = GMB_SLAB_BLOCKS_SPLIT;  // fp32, split-K tiles
+constexpr int kSlabBlocksBf16 = GMB_SLAB_BLOCKS_BF16;    // bf16
 
 template <int NCH, int J, int SPLIT>
 void launch_slab(const int32_t* sizes, const float* hs, const float* ag, const float* ws, const float* wn,
                  const float* bias, int K, int N, int relu, float* out, int64_t cap_rows, hipStream_t s) {
-  // LDS bounds the workgroups per CU.  The persistent grid holds
-  // kSlabBlocks{Wide,Split} workgroups per CU (capped by LDS): every workgroup
-  // reloads the slab, so a smaller grid reads the weights fewer times and
-  // leaves room for kernels of other streams.
+  // The persistent grid holds kSlabBlocks{Wide,Split} workgroups per CU
+  // (capped by LDS): every workgroup reloads the slab, so a smaller grid
+  // reads the weights fewer times and leaves room for kernels of other
+  // streams.
   constexpr int BN = 16 * J;
   constexpr int ROWS = SPLIT > 1 ? 16 : 64;
   constexpr int lds = NCH * 16 * BN * 4 + (SPLIT > 1 ? 4 * J * 64 * 16 : 0);
@@ -812,7 +822,7 @@ void launch_bf16_slab(const int32_t* sizes, const uint16_t* hs, const uint16_t* 
   constexpr int J = 4, BN = 64;
   constexpr int lds = NCH * 4 * BN * 8 * 2;
   constexpr int by_lds = (160 * 1024) / lds;
-  const int per_cu = by_lds < 1 ? 1 : (by_lds > 2 ? 2 : by_lds);
+  const int per_cu = by_lds < 1 ? 1 : (by_lds > kSlabBlocksBf16 ? kSlabBlocksBf16 : by_lds);
   const int col_tiles = (N + BN - 1) / BN;
   int64_t rows = (cap_rows + 63) / 64;
   const int64_t want = (256 * per_cu + col_tiles - 1) / col_tiles;
