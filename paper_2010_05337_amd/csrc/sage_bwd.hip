@@ -890,13 +890,14 @@ hipError_t launch_xent(const float* logits, const int32_t* labels, int n, int C,
 
 int wgrad_ldp(int d_out) { return (d_out + 3) / 4 * 4; }
 
-// Row ranges of the weight gradient: about 512 workgroups over all tiles
-// (two per CU at the kernel's register use),
+// Row ranges of the weight gradient: about 256 workgroups over all tiles
+// (one per CU: with 512, twice the partial tiles to write and reduce, the
+// training iteration measured 1.3% slower; 384 was slower still),
 // at least 64 rows each, a multiple of 8 when above 8 so that the tiles of
 // one row range (workgroup ids p + k * parts) share an XCD and its L2.
 int wgrad_parts(int64_t cap_rows, int d_in, int d_out) {
   const int tiles = ((wgrad_ldp(d_out) + 63) / 64) * (2 * ((d_in + 63) / 64));
-  int parts = (512 + tiles - 1) / tiles;
+  int parts = (256 + tiles - 1) / tiles;
   const int64_t by_rows = (cap_rows + 63) / 64;
   if (parts > by_rows) parts = static_cast<int>(by_rows);
   if (parts > 8) parts = parts / 8 * 8;
