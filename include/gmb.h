@@ -290,10 +290,12 @@ size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_wei
  *   ws       device workspace of >= gmb_backward_workspace_bytes() bytes,
  *            256-byte aligned.
  * Each weight gradient is summed over the rows in a fixed order (no
- * atomics), so the last layer's gradients are the same on every run; the
- * gradient that flows into the input of layers >= 1 accumulates with fp32
- * atomic adds, so the gradients of the layers below the last can differ in
- * their last bits between runs. */
+ * atomics), so the last layer's gradients are the same on every run.  The
+ * gradient that flows into the input of layers >= 1 is pulled per source
+ * vertex from a transpose of the block whose entries take their slots by
+ * atomic counters, so each source's terms are summed in an order that can
+ * change between runs, and the gradients of the layers below the last can
+ * differ in their last bits. */
 int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
                       const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
                       const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, void* stream);
