@@ -115,9 +115,14 @@ __global__ __launch_bounds__(256) void k_loss_sum(const float* __restrict__ rows
 // array of this kernel has fewer than 2^32 bytes (checked by the launcher),
 // so loads take a uniform base and a 32-bit byte offset.
 constexpr int kWgradRed = 2 * 64 * 64;   // LDS floats of the cross-wave sum
+#ifndef GMB_WGRAD_DEPTH
+#define GMB_WGRAD_DEPTH 3
+#endif
+constexpr int kWgradDepth = GMB_WGRAD_DEPTH;   // row steps in flight per wave (loads depth - 1 ahead)
 
 template <bool VEC>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(kWgradDepth <= 4 ? 2 : 1, kWgradDepth <= 4 ? 2 : 1)))
 void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
                                                const float* __restrict__ M, int d_in,
                                                const float* __restrict__ dZ, int ldz, int ldp,
@@ -184,29 +189,28 @@ void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
     }
   };
 
-  // loads run two steps ahead of the products.  The body is unrolled three
-  // times so that every buffer keeps its registers (a copy between buffers
-  // would wait for the load); the step count is rounded up to a multiple of
-  // three, the extra steps read the range's last row and add zero, and no
-  // branch surrounds a product, so the accumulators stay in place
+  // loads run kWgradDepth - 1 steps ahead of the products.  The body is
+  // unrolled kWgradDepth times so that every buffer keeps its registers (a
+  // copy between buffers would wait for the load); the step count is
+  // rounded up to a multiple of the depth, the extra steps read the range's
+  // last row and add zero, and no branch surrounds a product, so the
+  // accumulators stay in place
   int k0 = r0 + 16 * wave;
   const int nsteps = __builtin_amdgcn_readfirstlane(k0 < r1 ? (r1 - k0 + 63) / 64 : 0);
-  float4 xa[4], za[4], xb[4], zb[4], xc[4], zc4[4];
+  constexpr int D = kWgradDepth;
+  float4 xs[D][4], zs[D][4];
   if (nsteps > 0) {
-    load(k0, xa, za);
-    load(k0 + 64, xb, zb);
+#pragma unroll
+    for (int b = 0; b + 1 < D; ++b) load(k0 + 64 * b, xs[b], zs[b]);
   }
-  for (int it = 0; it < nsteps; it += 3) {
-    load(k0 + 128, xc, zc4);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(k0, xa, za);
-    load(k0 + 192, xa, za);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(k0 + 64, xb, zb);
-    load(k0 + 256, xb, zb);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(k0 + 128, xc, zc4);
-    k0 += 192;
+  for (int it = 0; it < nsteps; it += D) {
+#pragma unroll
+    for (int b = 0; b < D; ++b) {
+      load(k0 + 64 * (b + D - 1), xs[(b + D - 1) % D], zs[(b + D - 1) % D]);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(k0 + 64 * b, xs[b], zs[b]);
+    }
+    k0 += 64 * D;
   }
   // column sums of dZ: over the lane's rows, then over q
 #pragma unroll
