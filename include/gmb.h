@@ -223,7 +223,9 @@ int64_t gmb_forward_hidden_offset(const gmb_blocks* blocks, const gmb_sage_weigh
  * Per layer: the mean of the sampled in-neighbours' rows (0 for a vertex
  * with none) accumulated in fp32, then the two products and the bias in
  * one matrix-core GEMM with fp32 accumulation.  In bf16 mode the mean and
- * the hidden activations are rounded to bf16 before the next product. */
+ * the hidden activations are rounded to bf16 before the next product.
+ * An empty batch (num_seeds == 0) has no rows in any layer: nothing is
+ * enqueued, and x and logits may be NULL. */
 int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
                      float* logits, void* ws, size_t ws_bytes, void* stream);
 
@@ -244,7 +246,9 @@ int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_wei
  *              (gmb_state_status_word): an id outside [0, num_nodes) in
  *              the gather sets GMB_STATUS_ERANGE there and gives a zero row;
  *              in the mean it is read as row 0.
- *   others     as for gmb_sage_forward (same workspace size). */
+ *   others     as for gmb_sage_forward (same workspace size; with
+ *              num_seeds == 0 nothing is enqueued and x_dst and logits
+ *              may be NULL). */
 int gmb_sage_forward_fused(const gmb_blocks* blocks, const void* feats, int64_t num_nodes, void* x_dst,
                            const gmb_sage_weights* weights, float* logits, void* ws, size_t ws_bytes,
                            uint32_t* status, void* stream);
@@ -289,6 +293,9 @@ size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_wei
  *   loss     device fp32 scalar receiving L, or NULL.
  *   ws       device workspace of >= gmb_backward_workspace_bytes() bytes,
  *            256-byte aligned.
+ * An empty batch (num_seeds == 0): the loss, a mean over no seeds, is
+ * taken as 0, every gradient array is set to 0, and x, logits and labels
+ * may be NULL.
  * Each weight gradient is summed over the rows in a fixed order (no
  * atomics), so the last layer's gradients are the same on every run.  The
  * gradient that flows into the input of layers >= 1 is pulled per source
@@ -325,7 +332,9 @@ size_t gmb_backward_embedding_workspace_bytes(const gmb_blocks* blocks, const gm
  * The rows of one mini-batch are distinct, so the update needs no atomics;
  * calls in flight together on several streams update the shared table
  * without locks (asynchronous SGD as in Hogwild, as the paper updates its
- * embeddings), and a gather running meanwhile may see old or new rows. */
+ * embeddings), and a gather running meanwhile may see old or new rows.
+ * An empty batch changes no row (the gradients and the loss as for
+ * gmb_sage_backward). */
 int gmb_sage_backward_embedding(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
                                 const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
                                 const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, float* table,

@@ -185,7 +185,7 @@ int check_forward(const gmb_blocks* blocks, const gmb_sage_weights* weights, con
                   size_t ws_bytes, ForwardPlan* p) {
   int st = plan_forward(blocks, weights, p);
   if (st != GMB_OK) return st;
-  if (!logits) return fail(GMB_EINVAL, "logits is NULL");
+  if (!logits && blocks->num_seeds > 0) return fail(GMB_EINVAL, "logits is NULL");
   if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(GMB_EINVAL, "workspace is not 256-byte aligned");
   if (ws_bytes < p->total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p->total);
@@ -441,6 +441,7 @@ int gmb_sage_forward(const gmb_blocks* blocks, const void* x, const gmb_sage_wei
   ForwardPlan p;
   int st = check_forward(blocks, weights, logits, ws, ws_bytes, &p);
   if (st != GMB_OK) return st;
+  if (blocks->num_seeds == 0) return ok();   // an empty batch: no rows anywhere
   if (!x) return fail(GMB_EINVAL, "x is NULL");
   const gmb_block& b0 = blocks->blk[0];
   return run_forward(blocks, x, b0.indices, x, std::max<int64_t>(b0.cap_src, 1), weights, logits, p, ws,
@@ -453,9 +454,11 @@ int gmb_sage_forward_fused(const gmb_blocks* blocks, const void* feats, int64_t 
   ForwardPlan p;
   int st = check_forward(blocks, weights, logits, ws, ws_bytes, &p);
   if (st != GMB_OK) return st;
-  if (!feats || !x_dst) return fail(GMB_EINVAL, "feats or x_dst is NULL");
+  if (!feats) return fail(GMB_EINVAL, "feats is NULL");
   if (num_nodes < 1 || num_nodes > kMaxInt32)
     return fail(GMB_EINVAL, "num_nodes=%lld outside 1..2^31-1", static_cast<long long>(num_nodes));
+  if (blocks->num_seeds == 0) return ok();   // an empty batch: no rows anywhere
+  if (!x_dst) return fail(GMB_EINVAL, "x_dst is NULL");
   const hipStream_t s = as_stream(stream);
   const gmb_block& b0 = blocks->blk[0];
   const int64_t row_bytes = static_cast<int64_t>(weights->dims[0]) * (weights->dtype == GMB_BF16 ? 2 : 4);
@@ -565,7 +568,6 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
   plan_forward(blocks, weights, &fp);
   st = check_grads(grads, weights);
   if (st != GMB_OK) return st;
-  if (!x || !logits || (!labels && blocks->num_seeds > 0)) return fail(GMB_EINVAL, "x, logits or labels is NULL");
   if (!fwd_ws || fwd_ws_bytes < fp.total) return fail(GMB_ENOSPC, "forward workspace missing or too small");
   if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(ws) % kAlign || reinterpret_cast<uintptr_t>(fwd_ws) % kAlign)
@@ -573,6 +575,24 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
   if (ws_bytes < p.total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p.total);
   const hipStream_t s = as_stream(stream);
   const int L = weights->num_layers;
+  if (blocks->num_seeds == 0) {
+    // an empty batch: the mean over no seeds is taken as 0, so are the
+    // gradients, and no embedding row changes
+    gmb::SgdArgs z{};
+    for (int l = 0; l < L; ++l) {
+      const int64_t n = static_cast<int64_t>(weights->dims[l]) * weights->dims[l + 1];
+      z.w[z.count] = grads->d_self[l];
+      z.n[z.count++] = n;
+      z.w[z.count] = grads->d_neigh[l];
+      z.n[z.count++] = n;
+      z.w[z.count] = grads->d_bias[l];
+      z.n[z.count++] = weights->dims[l + 1];
+    }
+    hipError_t e = gmb::launch_zero(z, loss, s);
+    if (e != hipSuccess) return hip_fail(e, "zero-fill launch");
+    return ok();
+  }
+  if (!x || !logits || !labels) return fail(GMB_EINVAL, "x, logits or labels is NULL");
   char* base = static_cast<char*>(ws);
   const char* fbase = static_cast<const char*>(fwd_ws);
   float* cur = reinterpret_cast<float*>(base + p.off_a);

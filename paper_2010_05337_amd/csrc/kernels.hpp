@@ -149,5 +149,7 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
                                 uint32_t* scan_state, int2* csc, int32_t* long_rows, float* table, const int32_t* ids,
                                 int64_t num_nodes, float lr, hipStream_t s);
 hipError_t launch_sgd(const SgdArgs& a, float lr, hipStream_t s);
+// every array of `a` (w[t], n[t]; g unused) and *scalar (if not NULL) to 0
+hipError_t launch_zero(const SgdArgs& a, float* scalar, hipStream_t s);
 
 }  // namespace gmb

@@ -865,6 +865,19 @@ __global__ __launch_bounds__(256) void k_pull_update(const int32_t* __restrict__
 
 // ---- SGD ------------------------------------------------------------------
 
+// Every listed array set to zero, and *scalar too when given (the
+// gradients and the loss of an empty batch).
+__global__ __launch_bounds__(256) void k_zero(SgdArgs a, float* scalar) {
+  if (scalar && blockIdx.x == 0 && threadIdx.x == 0) *scalar = 0.f;
+  for (int t = 0; t < a.count; ++t) {
+    float* w = a.w[t];
+    const int64_t n = a.n[t];
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+      w[i] = 0.f;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_sgd(SgdArgs a, float lr) {
   for (int t = 0; t < a.count; ++t) {
     float* w = a.w[t];
@@ -1004,6 +1017,13 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
     default: GMB_PULL(64); break;
   }
 #undef GMB_PULL
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(const SgdArgs& a, float* scalar, hipStream_t s) {
+  int64_t most = 1;
+  for (int t = 0; t < a.count; ++t) most = std::max(most, a.n[t]);
+  hipLaunchKernelGGL(k_zero, dim3(grid_of(most, 1024)), dim3(256), 0, s, a, scalar);
   return hipGetLastError();
 }
 

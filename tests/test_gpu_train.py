@@ -14,8 +14,9 @@ only by the rounding of the fp32 backward.
 
 Tolerances: the loss within 1e-5 relative; every gradient array within 1e-4
 of its largest magnitude (fp32 sums of at most a few thousand terms, split
-into partial sums; the layer-input gradients also pass through fp32 atomic
-adds); the SGD result within lr * that error plus one fp32 rounding.
+into partial sums; the layer-input gradients sum each source's terms in
+an order that atomic slot claims set anew each run); the SGD result within
+lr * that error plus one fp32 rounding.
 """
 import types
 
@@ -342,4 +343,39 @@ def test_long_transpose_lists(orc, dg, embed):
         _, _, dX, _, ref_table = orc.sage_train_step_embed(ref_blocks, table_np.astype(np.float64), ws, wn, bs,
                                                             labels, lr, emb_lr)
         check_embedding_update(orc, table_before, table, ref_blocks, ref_table, dX, emb_lr)
+    csr.check_status()
+
+
+def test_empty_batch(dg):
+    """No seeds: the forwards leave no rows, the backward writes a zero loss
+    and zero gradients (the mean over no seeds taken as 0) over arrays that
+    held other values, and the embedding step changes no table row."""
+    g = dg.er_directed(2000, 6.0, 5)
+    csr = csr_on_device(g)
+    X = dg.features(2000, 12, 6, "f32")
+    ft = torch.from_numpy(X).cuda()
+    wt = to_torch_weights(dg.sage_weights([12, 8, 5], 7))
+    blocks, host = gpu_blocks(csr, np.zeros(0, dtype=np.int64), [3, 4], 8)
+    assert all(h["n_dst"] == 0 and h["n_src"] == 0 and h["nnz"] == 0 for h in host)
+    x = gmb.gather_features(blocks, ft)
+    ws = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+    logits = gmb.sage_forward(blocks, x, wt, workspace=ws)
+    assert tuple(logits.shape) == (0, 5)
+    labels = torch.zeros(0, dtype=torch.int32, device="cuda")
+    for embedding in (None, ft.clone()):
+        grads = gmb.SageGrads(wt)
+        for a in grads.d_self + grads.d_neigh + grads.d_bias:
+            a.fill_(7.0)
+        loss = torch.full((1,), 7.0, dtype=torch.float32, device="cuda")
+        before = None if embedding is None else embedding.clone()
+        grads, loss = gmb.sage_backward(blocks, x, wt, logits, labels, ws, grads=grads, loss=loss,
+                                        embedding=embedding, emb_lr=0.5)
+        torch.cuda.synchronize()
+        assert float(loss.item()) == 0.0
+        for a in grads.d_self + grads.d_neigh + grads.d_bias:
+            assert bool((a == 0).all())
+        if embedding is not None:
+            assert torch.equal(embedding, before)
+    logits_f, x_dst = gmb.sage_forward_fused(blocks, ft, wt, workspace=ws)
+    assert tuple(logits_f.shape) == (0, 5) and x_dst.shape[0] == 0
     csr.check_status()
