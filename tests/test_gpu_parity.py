@@ -85,6 +85,24 @@ def test_sampling_rmat_hubs_bitexact(orc, dg, wide):
     csr.check_status()
 
 
+def test_sampling_wide_fanouts_on_hubs(orc, dg):
+    """Fan-outs above 64 (the one-thread-per-destination sampler, whose
+    slots are sorted in place) on rows far longer than the fan-out, and a
+    fan-out of exactly 64 (the widest lane group)."""
+    g = dg.rmat(14, 16000, 240000, (0.57, 0.19, 0.19), 17)
+    g = dg.inject_hubs(g, 4, 5000, 18)
+    csr = csr_on_device(g)
+    seeds = np.concatenate([g.hubs, dg.permutation(16000, 19)[:400]]).astype(np.int64)
+    seeds = seeds[np.sort(np.unique(seeds, return_index=True)[1])]
+    deg = g.degrees()
+    for fo, key in [([100], 21), ([70, 3], 22), ([64], 23)]:
+        _, host = gpu_blocks(csr, seeds, fo, key)
+        ref = orc.sample_blocks(g.indptr, g.indices, seeds, fo, key)
+        assert_blocks_equal(host, ref, f"fanouts {fo}")
+        assert (deg[seeds] > max(fo)).sum() >= 4   # Floyd runs on every hub
+    csr.check_status()
+
+
 def test_sampling_is_deterministic_and_keyed(dg, tiny):
     csr = csr_on_device(tiny)
     seeds = dg.permutation(10000, 5)[:500]
