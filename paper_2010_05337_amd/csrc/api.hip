@@ -604,8 +604,9 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
   int32_t* pos = reinterpret_cast<int32_t*>(base + p.off_pos);
   int2* csc = reinterpret_cast<int2*>(base + p.off_csc);
   int32_t* long_rows = reinterpret_cast<int32_t*>(base + p.off_long);
+  float* loss_rows = reinterpret_cast<float*>(base + p.off_lossrows);
   hipError_t e = gmb::launch_xent(logits, labels, blocks->num_seeds, weights->dims[L], p.ldz[L - 1], cur,
-                                  reinterpret_cast<float*>(base + p.off_lossrows), loss, cnt, p.clear_len, s);
+                                  loss_rows, cnt, p.clear_len, s);
   if (e != hipSuccess) return hip_fail(e, "loss launch");
   for (int l = L - 1; l >= 0; --l) {
     const gmb_block& bk = blocks->blk[l];
@@ -613,8 +614,11 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
     const float* h_in = l == 0 ? static_cast<const float*>(x)
                                : reinterpret_cast<const float*>(fbase + fp.off_hidden[l - 1]);
     const float* m = reinterpret_cast<const float*>(fbase + fp.off_agg[l]);
+    // the last layer's reduction also sums the loss
+    const bool top = l == L - 1;
     e = gmb::launch_wgrad(bk.sizes, h_in, m, d_in, cur, p.ldz[l], d_out, std::max<int64_t>(bk.cap_dst, 1), part,
-                          grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], s);
+                          grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], top ? loss_rows : nullptr,
+                          blocks->num_seeds, top ? loss : nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
     if (l == 0 && !embed) break;
     // dZ [W_self; W_neigh]^T: dH_self into `other`, dM; the block's

@@ -127,12 +127,14 @@ struct SgdArgs {
   int64_t n[3 * GMB_MAX_LAYERS];
 };
 hipError_t launch_xent(const float* logits, const int32_t* labels, int n, int C, int ldz, float* dz,
-                       float* loss_rows, float* loss, int32_t* clear, int64_t clear_n, hipStream_t s);
+                       float* loss_rows, int32_t* clear, int64_t clear_n, hipStream_t s);
 int wgrad_ldp(int d_out);
 int wgrad_parts(int64_t cap_rows, int d_in, int d_out);
+// With loss != NULL one more workgroup writes the mean of loss_rows[0..n_loss)
+// to *loss (the loss kernel's per-seed terms).
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
                         int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
-                        float* d_bias, hipStream_t s);
+                        float* d_bias, const float* loss_rows, int n_loss, float* loss, hipStream_t s);
 hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_out, const float* ws,
                         const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
                         const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t fanout, int32_t* cnt,

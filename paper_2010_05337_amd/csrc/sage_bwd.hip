@@ -5,7 +5,6 @@
 //   k_xent         softmax cross-entropy per target row (one wave per row):
 //                  dZ = (softmax(z) - e_y) / B, and the row's loss term; also
 //                  clears the per-source edge counters of the transposes
-//   k_loss_sum     the mean loss, one workgroup, fixed order
 //   k_wgrad        [dW_self; dW_neigh] = [H | M]^T dZ and db = sum of dZ rows:
 //                  v_mfma_f32_16x16x4_f32 with the rows of the block as the
 //                  reduction dimension; a workgroup owns a 64 x 64 tile of
@@ -13,7 +12,9 @@
 //                  rows and are summed through LDS, and every workgroup
 //                  writes its partial sums (no atomics: the same result on
 //                  every run)
-//   k_wgrad_reduce sums the partials in a fixed order into the gradients
+//   k_wgrad_reduce sums the partials in a fixed order into the gradients;
+//                  on the last layer one more workgroup sums the loss terms
+//                  into the mean loss (fixed order)
 //   k_dgrad        [dH_self | dM] = dZ [W_self; W_neigh]^T: the weights'
 //                  transpose for 64 output columns resident in LDS in MFMA
 //                  operand order, 64-row tiles, persistent over row tiles;
@@ -29,6 +30,7 @@
 //                  (both end their grids with workgroups that take the
 //                  sources with long transpose lists, hubs, one each)
 //   k_sgd          W -= lr dW over every parameter array
+//   k_zero         the gradients and the loss of an empty batch
 #include <algorithm>
 
 #include "common.hpp"
@@ -80,7 +82,10 @@ __global__ __launch_bounds__(256) void k_xent(const float* __restrict__ z, const
   if (lane == 0) loss_rows[row] = valid ? lse - zr[label] : 0.f;
 }
 
-__global__ __launch_bounds__(256) void k_loss_sum(const float* __restrict__ rows, int n, float* __restrict__ loss) {
+// The mean loss by one workgroup of 256 threads, in a fixed order.  It runs
+// as an extra workgroup of the last layer's weight-gradient reduction (the
+// launch after the loss kernel's), which saves a launch of its own.
+__device__ void loss_sum_block(const float* __restrict__ rows, int n, float* __restrict__ loss) {
   __shared__ float part[256];
   float s = 0.f;
   for (int i = threadIdx.x; i < n; i += 256) s += rows[i];
@@ -274,7 +279,13 @@ void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
 // fixed order.  Rows i < 2 d_in go to dW_self / dW_neigh, row 2 d_in to db.
 __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ partial, int parts, int d_in,
                                                       int d_out, int ldp, float* __restrict__ d_self,
-                                                      float* __restrict__ d_neigh, float* __restrict__ d_bias) {
+                                                      float* __restrict__ d_neigh, float* __restrict__ d_bias,
+                                                      const float* __restrict__ loss_rows, int n_loss,
+                                                      float* __restrict__ loss) {
+  if (loss && blockIdx.x == gridDim.x - 1) {   // the appended workgroup (uniform)
+    loss_sum_block(loss_rows, n_loss, loss);
+    return;
+  }
   __shared__ float4 red[3][64];
   const int K2 = 2 * d_in;
   const int per_row = ldp / 4;
@@ -898,10 +909,9 @@ inline unsigned grid_of(int64_t threads, int64_t cap = 65535) {
 }  // namespace
 
 hipError_t launch_xent(const float* logits, const int32_t* labels, int n, int C, int ldz, float* dz,
-                       float* loss_rows, float* loss, int32_t* clear, int64_t clear_n, hipStream_t s) {
+                       float* loss_rows, int32_t* clear, int64_t clear_n, hipStream_t s) {
   const unsigned g = static_cast<unsigned>(std::max(1, (n + 3) / 4));
   hipLaunchKernelGGL(k_xent, dim3(g), dim3(256), 0, s, logits, labels, n, C, ldz, dz, loss_rows, clear, clear_n);
-  if (loss) hipLaunchKernelGGL(k_loss_sum, dim3(1), dim3(256), 0, s, loss_rows, n, loss);
   return hipGetLastError();
 }
 
@@ -923,7 +933,7 @@ int wgrad_parts(int64_t cap_rows, int d_in, int d_out) {
 
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
                         int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
-                        float* d_bias, hipStream_t s) {
+                        float* d_bias, const float* loss_rows, int n_loss, float* loss, hipStream_t s) {
   const int parts = wgrad_parts(cap_rows, d_in, d_out);
   const int ldp = wgrad_ldp(d_out);
   const dim3 grid(parts, (ldp + 63) / 64, 2 * ((d_in + 63) / 64));
@@ -936,8 +946,9 @@ hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, in
   else
     hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
   const int64_t outs = static_cast<int64_t>(2 * d_in + 1) * (ldp / 4);
-  hipLaunchKernelGGL(k_wgrad_reduce, dim3(static_cast<unsigned>((outs + 63) / 64)), dim3(256), 0, s, partial,
-                     parts, d_in, d_out, ldp, d_self, d_neigh, d_bias);
+  const unsigned blocks = static_cast<unsigned>((outs + 63) / 64) + (loss ? 1u : 0u);
+  hipLaunchKernelGGL(k_wgrad_reduce, dim3(blocks), dim3(256), 0, s, partial, parts, d_in, d_out, ldp, d_self,
+                     d_neigh, d_bias, loss_rows, n_loss, loss);
   return hipGetLastError();
 }
 
