@@ -17,9 +17,14 @@ sampling with training of Section III-D), with per-stage event times of a
 one-stream pass and the oracle's training iteration as CPU baseline.
 
 Prints one JSON line.  value = seeds/s over the timed steps; sampled edges/s
-and gather GB/s ride along; `roofline` covers the dominant kernel, measured
-with HIP events on the stream the kernels run on; `cpu_baseline` times the
-CPU oracle on a bounded sample of the same batches (single thread).
+and gather GB/s ride along, and so does the rate of the forward with the
+feature pull folded into layer 0 (`fused_forward`); `roofline` covers the
+dominant kernel, measured with HIP events on the stream the kernels run on;
+`cpu_baseline` times the CPU oracle on a bounded sample of the same batches
+(one batch per host thread, up to 16, plus a one-thread figure).
+
+--summarize-profile, --summarize-pmc and --summarize-counters turn the
+rocprofv3 output of runs of this script into the tables kept in profiles/.
 """
 from __future__ import annotations
 
