@@ -614,13 +614,16 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
     const float* h_in = l == 0 ? static_cast<const float*>(x)
                                : reinterpret_cast<const float*>(fbase + fp.off_hidden[l - 1]);
     const float* m = reinterpret_cast<const float*>(fbase + fp.off_agg[l]);
-    // the last layer's reduction also sums the loss
+    // the last layer's reduction also sums the loss; on a layer whose input
+    // gradient runs, the reduction rides in the transpose scan's launch
     const bool top = l == L - 1;
+    const bool below = l > 0 || embed;
+    gmb::ReduceArgs fold{};
     e = gmb::launch_wgrad(bk.sizes, h_in, m, d_in, cur, p.ldz[l], d_out, std::max<int64_t>(bk.cap_dst, 1), part,
                           grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], top ? loss_rows : nullptr,
-                          blocks->num_seeds, top ? loss : nullptr, s);
+                          blocks->num_seeds, top ? loss : nullptr, below ? &fold : nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
-    if (l == 0 && !embed) break;
+    if (!below) break;
     // dZ [W_self; W_neigh]^T: dH_self into `other`, dM; the block's
     // in-edge counts per source on the way
     e = gmb::launch_dgrad(bk.sizes, cur, p.ldz[l], d_out, static_cast<const float*>(weights->w_self[l]),
@@ -634,7 +637,7 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
     e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, bk.cap_nnz, bk.fanout, dM,
                                   l == 0 ? nullptr : h_in, d_in, other, bk.cap_dst, bk.cap_src, cnt, offs, pos,
                                   scan_state, csc, long_rows, l == 0 ? table : nullptr, bk.src_ids, num_nodes,
-                                  emb_lr, s);
+                                  emb_lr, &fold, s);
     if (e != hipSuccess) return hip_fail(e, "mean-backward launch");
     std::swap(cur, other);
   }

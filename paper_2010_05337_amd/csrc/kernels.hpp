@@ -130,11 +130,27 @@ hipError_t launch_xent(const float* logits, const int32_t* labels, int n, int C,
                        float* loss_rows, int32_t* clear, int64_t clear_n, hipStream_t s);
 int wgrad_ldp(int d_out);
 int wgrad_parts(int64_t cap_rows, int d_in, int d_out);
-// With loss != NULL one more workgroup writes the mean of loss_rows[0..n_loss)
-// to *loss (the loss kernel's per-seed terms).
+// The weight gradient's second step: the partial tiles summed into the
+// gradients in a fixed order, `blocks` workgroups (the last one sums the
+// loss terms loss_rows[0 .. n_loss) into *loss when loss is not NULL).
+struct ReduceArgs {
+  const float* partial;
+  int parts, d_in, d_out, ldp;
+  float* d_self;
+  float* d_neigh;
+  float* d_bias;
+  const float* loss_rows;
+  int n_loss;
+  float* loss;
+  int blocks;
+};
+// Launches the weight gradient's products and, unless `fold` is given, its
+// reduction; with `fold` the reduction is described there for a later
+// launch to run as extra workgroups of its grid (launch_mean_backward).
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
                         int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
-                        float* d_bias, const float* loss_rows, int n_loss, float* loss, hipStream_t s);
+                        float* d_bias, const float* loss_rows, int n_loss, float* loss, ReduceArgs* fold,
+                        hipStream_t s);
 hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_out, const float* ws,
                         const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
                         const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t fanout, int32_t* cnt,
@@ -145,11 +161,13 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
 int64_t csc_scan_tiles(int64_t cap_src);
 // With table != NULL the pull applies table[ids[u]] -= lr * g instead of
 // writing the masked gradient into dH (out unused).
+// With `fold` (from launch_wgrad) the transpose scan's grid also runs that
+// reduction.
 hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                 int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
                                 uint32_t* scan_state, int2* csc, int32_t* long_rows, float* table, const int32_t* ids,
-                                int64_t num_nodes, float lr, hipStream_t s);
+                                int64_t num_nodes, float lr, const ReduceArgs* fold, hipStream_t s);
 hipError_t launch_sgd(const SgdArgs& a, float lr, hipStream_t s);
 // every array of `a` (w[t], n[t]; g unused) and *scalar (if not NULL) to 0
 hipError_t launch_zero(const SgdArgs& a, float* scalar, hipStream_t s);

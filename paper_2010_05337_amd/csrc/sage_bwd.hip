@@ -14,7 +14,10 @@
 //                  every run)
 //   k_wgrad_reduce sums the partials in a fixed order into the gradients;
 //                  on the last layer one more workgroup sums the loss terms
-//                  into the mean loss (fixed order)
+//                  into the mean loss (fixed order).  On a layer whose input
+//                  gradient runs, the same workgroups ride at the end of
+//                  that layer's k_csc_scan grid instead of a launch of
+//                  their own
 //   k_dgrad        [dH_self | dM] = dZ [W_self; W_neigh]^T: the weights'
 //                  transpose for 64 output columns resident in LDS in MFMA
 //                  operand order, 64-row tiles, persistent over row tiles;
@@ -277,24 +280,23 @@ void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
 // One float4 of output per thread group of four: group g sums the parts
 // p = g, g + 4, ... in ascending order, the four groups meet in LDS in a
 // fixed order.  Rows i < 2 d_in go to dW_self / dW_neigh, row 2 d_in to db.
-__global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ partial, int parts, int d_in,
-                                                      int d_out, int ldp, float* __restrict__ d_self,
-                                                      float* __restrict__ d_neigh, float* __restrict__ d_bias,
-                                                      const float* __restrict__ loss_rows, int n_loss,
-                                                      float* __restrict__ loss) {
-  if (loss && blockIdx.x == gridDim.x - 1) {   // the appended workgroup (uniform)
-    loss_sum_block(loss_rows, n_loss, loss);
+// Workgroup `block` of the reduction of `r` (block r.blocks - 1 sums the
+// loss when r.loss is set).
+__device__ void wgrad_reduce_block(const ReduceArgs& r, int block) {
+  if (r.loss && block == r.blocks - 1) {   // the appended workgroup (uniform)
+    loss_sum_block(r.loss_rows, r.n_loss, r.loss);
     return;
   }
   __shared__ float4 red[3][64];
+  const int d_in = r.d_in, d_out = r.d_out, ldp = r.ldp, parts = r.parts;
   const int K2 = 2 * d_in;
   const int per_row = ldp / 4;
   const int64_t total = static_cast<int64_t>(K2 + 1) * per_row;
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 64 + (threadIdx.x & 63);
+  const int64_t idx = static_cast<int64_t>(block) * 64 + (threadIdx.x & 63);
   const int g = threadIdx.x >> 6;
   const bool live = idx < total;
   const int64_t stride = static_cast<int64_t>(K2 + 1) * ldp;
-  const float* src = partial + (live ? idx * 4 : 0);
+  const float* src = r.partial + (live ? idx * 4 : 0);
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
   int p = g;
   for (; p + 4 < parts; p += 8) {
@@ -318,13 +320,15 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ 
   }
   const int i = static_cast<int>(idx / per_row);
   const int o = static_cast<int>(idx % per_row) * 4;
-  float* dst = i < d_in ? d_self + static_cast<int64_t>(i) * d_out
-                        : (i < K2 ? d_neigh + static_cast<int64_t>(i - d_in) * d_out : d_bias);
+  float* dst = i < d_in ? r.d_self + static_cast<int64_t>(i) * d_out
+                        : (i < K2 ? r.d_neigh + static_cast<int64_t>(i - d_in) * d_out : r.d_bias);
   const float v[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
   for (int j = 0; j < 4; ++j)
     if (o + j < d_out) dst[o + j] = v[j];
 }
+
+__global__ __launch_bounds__(256) void k_wgrad_reduce(ReduceArgs r) { wgrad_reduce_block(r, blockIdx.x); }
 
 // ---- input gradient -------------------------------------------------------
 
@@ -532,7 +536,14 @@ constexpr int kLongList = 16;   // transpose lists longer than this take a workg
 __global__ __launch_bounds__(256) void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ off, int32_t* __restrict__ pos,
                                                   uint32_t* __restrict__ ticket, uint64_t* __restrict__ words,
-                                                  uint32_t* __restrict__ n_long, int32_t* __restrict__ long_rows) {
+                                                  uint32_t* __restrict__ n_long, int32_t* __restrict__ long_rows,
+                                                  int scan_blocks, ReduceArgs fold) {
+  // workgroups past the scan's run the weight gradient's reduction of the
+  // same layer (independent of the scan: one launch for both)
+  if (static_cast<int>(blockIdx.x) >= scan_blocks) {
+    wgrad_reduce_block(fold, blockIdx.x - scan_blocks);
+    return;
+  }
   __shared__ int s_tile;
   __shared__ int32_t s_excl;
   __shared__ int32_t smem[4];
@@ -933,7 +944,8 @@ int wgrad_parts(int64_t cap_rows, int d_in, int d_out) {
 
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
                         int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
-                        float* d_bias, const float* loss_rows, int n_loss, float* loss, hipStream_t s) {
+                        float* d_bias, const float* loss_rows, int n_loss, float* loss, ReduceArgs* fold,
+                        hipStream_t s) {
   const int parts = wgrad_parts(cap_rows, d_in, d_out);
   const int ldp = wgrad_ldp(d_out);
   const dim3 grid(parts, (ldp + 63) / 64, 2 * ((d_in + 63) / 64));
@@ -946,9 +958,13 @@ hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, in
   else
     hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
   const int64_t outs = static_cast<int64_t>(2 * d_in + 1) * (ldp / 4);
-  const unsigned blocks = static_cast<unsigned>((outs + 63) / 64) + (loss ? 1u : 0u);
-  hipLaunchKernelGGL(k_wgrad_reduce, dim3(blocks), dim3(256), 0, s, partial, parts, d_in, d_out, ldp, d_self,
-                     d_neigh, d_bias, loss_rows, n_loss, loss);
+  const ReduceArgs r{partial, parts, d_in, d_out, ldp, d_self, d_neigh, d_bias, loss_rows, n_loss, loss,
+                     static_cast<int>((outs + 63) / 64) + (loss ? 1 : 0)};
+  if (fold) {
+    *fold = r;
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_wgrad_reduce, dim3(static_cast<unsigned>(r.blocks)), dim3(256), 0, s, r);
   return hipGetLastError();
 }
 
@@ -993,12 +1009,15 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
                                 int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
                                 uint32_t* scan_state, int2* csc, int32_t* long_rows, float* table, const int32_t* ids,
-                                int64_t num_nodes, float lr, hipStream_t s) {
+                                int64_t num_nodes, float lr, const ReduceArgs* fold, hipStream_t s) {
   const EdgeView ev{indptr, local, cap_nnz, fanout};
   // scan_state: [0] the tile ticket, [1] the long-row count, then the
   // look-back words
-  hipLaunchKernelGGL(k_csc_scan, dim3(static_cast<unsigned>(csc_scan_tiles(cap_src))), dim3(256), 0, s, sizes, cnt,
-                     off, pos, scan_state, reinterpret_cast<uint64_t*>(scan_state + 2), scan_state + 1, long_rows);
+  const int scan_blocks = static_cast<int>(csc_scan_tiles(cap_src));
+  const ReduceArgs none{};
+  hipLaunchKernelGGL(k_csc_scan, dim3(static_cast<unsigned>(scan_blocks + (fold ? fold->blocks : 0))), dim3(256), 0,
+                     s, sizes, cnt, off, pos, scan_state, reinterpret_cast<uint64_t*>(scan_state + 2), scan_state + 1,
+                     long_rows, scan_blocks, fold ? *fold : none);
   const int64_t slots = std::max<int64_t>(cap_dst, 1) * std::max(fanout, 1);
   hipLaunchKernelGGL(k_csc_fill, dim3(grid_of(slots, 1 << 16)), dim3(256), 0, s, sizes, ev, pos, off, csc);
   const int chunks = d / 4;
