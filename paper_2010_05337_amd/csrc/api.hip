@@ -554,6 +554,12 @@ int check_grads(const gmb_sage_grads* g, const gmb_sage_weights* w) {
   return GMB_OK;
 }
 
+// Transpose scans of at most this many tiles take the weight gradient's
+// products into their launch (a larger scan's own workgroups would hold
+// the CUs while the products wait behind them: measured slower on the
+// 1032-tile scan of layer 0 with learnable embeddings).
+constexpr int64_t kFoldScanTiles = 256;
+
 // The backward from the loss down; with table != NULL layer 0's input
 // gradient is applied to the embedding rows of block 0's sources.
 int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights, const float* logits,
@@ -614,14 +620,21 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
     const float* h_in = l == 0 ? static_cast<const float*>(x)
                                : reinterpret_cast<const float*>(fbase + fp.off_hidden[l - 1]);
     const float* m = reinterpret_cast<const float*>(fbase + fp.off_agg[l]);
-    // the last layer's reduction also sums the loss; on a layer whose input
-    // gradient runs, the reduction rides in the transpose scan's launch
+    // the last layer's reduction also sums the loss.  On a layer whose
+    // input gradient runs, the weight gradient's reduction rides in the
+    // transpose fill's launch, and, while the transpose scan is small
+    // enough not to hold the CUs back, its products in the scan's
+    // (described here, launched by launch_mean_backward after the input
+    // gradient)
     const bool top = l == L - 1;
     const bool below = l > 0 || embed;
+    const bool beside_scan = below && gmb::csc_scan_tiles(bk.cap_src) <= kFoldScanTiles;
+    gmb::WgradArgs defer{};
     gmb::ReduceArgs fold{};
     e = gmb::launch_wgrad(bk.sizes, h_in, m, d_in, cur, p.ldz[l], d_out, std::max<int64_t>(bk.cap_dst, 1), part,
                           grads->d_self[l], grads->d_neigh[l], grads->d_bias[l], top ? loss_rows : nullptr,
-                          blocks->num_seeds, top ? loss : nullptr, below ? &fold : nullptr, s);
+                          blocks->num_seeds, top ? loss : nullptr, beside_scan ? &defer : nullptr,
+                          below ? &fold : nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
     if (!below) break;
     // dZ [W_self; W_neigh]^T: dH_self into `other`, dM; the block's
@@ -637,7 +650,7 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
     e = gmb::launch_mean_backward(bk.sizes, bk.indptr, bk.indices, bk.cap_nnz, bk.fanout, dM,
                                   l == 0 ? nullptr : h_in, d_in, other, bk.cap_dst, bk.cap_src, cnt, offs, pos,
                                   scan_state, csc, long_rows, l == 0 ? table : nullptr, bk.src_ids, num_nodes,
-                                  emb_lr, &fold, s);
+                                  emb_lr, beside_scan ? &defer : nullptr, &fold, s);
     if (e != hipSuccess) return hip_fail(e, "mean-backward launch");
     std::swap(cur, other);
   }

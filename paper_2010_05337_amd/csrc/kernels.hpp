@@ -144,13 +144,27 @@ struct ReduceArgs {
   float* loss;
   int blocks;
 };
-// Launches the weight gradient's products and, unless `fold` is given, its
-// reduction; with `fold` the reduction is described there for a later
-// launch to run as extra workgroups of its grid (launch_mean_backward).
+// The weight gradient's products: a parts x ytiles x ztiles grid of
+// workgroups writing partial tiles (vec: 16-byte loads of H and M).
+struct WgradArgs {
+  const int32_t* sizes;
+  const float* H;
+  const float* M;
+  int d_in;
+  const float* dZ;
+  int ldz, ldp;
+  float* partial;
+  int parts, ytiles, ztiles;
+  int vec;
+};
+// Launches the weight gradient's products and its reduction, or, for
+// `defer` and `fold` when given, describes them instead, for later launches
+// to run as extra workgroups of their grids (launch_mean_backward: the
+// products beside the transpose scan, the reduction beside the fill).
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
                         int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
-                        float* d_bias, const float* loss_rows, int n_loss, float* loss, ReduceArgs* fold,
-                        hipStream_t s);
+                        float* d_bias, const float* loss_rows, int n_loss, float* loss, WgradArgs* defer,
+                        ReduceArgs* fold, hipStream_t s);
 hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_out, const float* ws,
                         const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
                         const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t fanout, int32_t* cnt,
@@ -161,13 +175,14 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
 int64_t csc_scan_tiles(int64_t cap_src);
 // With table != NULL the pull applies table[ids[u]] -= lr * g instead of
 // writing the masked gradient into dH (out unused).
-// With `fold` (from launch_wgrad) the transpose scan's grid also runs that
-// reduction.
+// With `defer` (from launch_wgrad) the transpose scan's grid also runs the
+// weight gradient's products, with `fold` the fill's grid its reduction.
 hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, const int32_t* local,
                                 int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
                                 uint32_t* scan_state, int2* csc, int32_t* long_rows, float* table, const int32_t* ids,
-                                int64_t num_nodes, float lr, const ReduceArgs* fold, hipStream_t s);
+                                int64_t num_nodes, float lr, const WgradArgs* defer, const ReduceArgs* fold,
+                                hipStream_t s);
 hipError_t launch_sgd(const SgdArgs& a, float lr, hipStream_t s);
 // every array of `a` (w[t], n[t]; g unused) and *scalar (if not NULL) to 0
 hipError_t launch_zero(const SgdArgs& a, float* scalar, hipStream_t s);

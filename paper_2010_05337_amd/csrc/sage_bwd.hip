@@ -15,9 +15,11 @@
 //   k_wgrad_reduce sums the partials in a fixed order into the gradients;
 //                  on the last layer one more workgroup sums the loss terms
 //                  into the mean loss (fixed order).  On a layer whose input
-//                  gradient runs, the same workgroups ride at the end of
-//                  that layer's k_csc_scan grid instead of a launch of
-//                  their own
+//                  gradient runs, the reduction's workgroups ride at the end
+//                  of that layer's k_csc_fill grid, and (for a small scan)
+//                  k_wgrad's at the end of its k_csc_scan grid, instead of
+//                  launches of their own (the input gradient then goes
+//                  first)
 //   k_dgrad        [dH_self | dM] = dZ [W_self; W_neigh]^T: the weights'
 //                  transpose for 64 output columns resident in LDS in MFMA
 //                  operand order, 64-row tiles, persistent over row tiles;
@@ -128,35 +130,34 @@ constexpr int kWgradRed = 2 * 64 * 64;   // LDS floats of the cross-wave sum
 #endif
 constexpr int kWgradDepth = GMB_WGRAD_DEPTH;   // row steps in flight per wave (loads depth - 1 ahead)
 
+// Workgroup (bx, by, bz) of a weight-gradient grid with gx row ranges.
 template <bool VEC>
-__global__ __launch_bounds__(256)
-__attribute__((amdgpu_waves_per_eu(kWgradDepth <= 4 ? 2 : 1, kWgradDepth <= 4 ? 2 : 1)))
-void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
-                                               const float* __restrict__ M, int d_in,
-                                               const float* __restrict__ dZ, int ldz, int ldp,
-                                               float* __restrict__ partial) {
+__device__ __forceinline__ void wgrad_block(const int32_t* __restrict__ sizes, const float* __restrict__ H,
+                                            const float* __restrict__ M, int d_in, const float* __restrict__ dZ,
+                                            int ldz, int ldp, float* __restrict__ partial, int bx, int by, int bz,
+                                            int gx) {
   __shared__ float red[kWgradRed];
   __shared__ float red_db[4][64];
   const int32_t n = load_size(&sizes[kNDst]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, c16 = lane & 15;
-  const int p = blockIdx.x;
+  const int p = bx;
   const int K2 = 2 * d_in;
   const int TI = (d_in + 63) / 64;
-  const bool from_m = static_cast<int>(blockIdx.z) >= TI;
-  const int zc = from_m ? blockIdx.z - TI : blockIdx.z;
+  const bool from_m = bz >= TI;
+  const int zc = from_m ? bz - TI : bz;
   const char* X = reinterpret_cast<const char*>(from_m ? M : H);   // uniform per workgroup
   const char* Zb = reinterpret_cast<const char*>(dZ);
   const int cb = zc * 64 + 4 * c16;           // this lane's first column of X
-  const int ob = blockIdx.y * 64 + 4 * c16;   // this lane's first column of dZ
+  const int ob = by * 64 + 4 * c16;   // this lane's first column of dZ
   const uint32_t xrow = static_cast<uint32_t>(d_in) * 4u, zrow = static_cast<uint32_t>(ldz) * 4u;
   const uint32_t ocol = static_cast<uint32_t>(ob < ldz ? ob : 0) * 4u;
   uint32_t xcol[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) xcol[t] = static_cast<uint32_t>(VEC ? (cb < d_in ? cb : 0) : (cb + t < d_in ? cb + t : 0)) * 4u;
-  // the block's actual rows split evenly over the gridDim.x ranges (16-row
+  // the block's actual rows split evenly over the gx ranges (16-row
   // granules); every range writes its partial, empty or not
-  const int rows_per_part = ((n + gridDim.x - 1) / gridDim.x + 15) / 16 * 16;
+  const int rows_per_part = ((n + gx - 1) / gx + 15) / 16 * 16;
   const int r0 = min(p * rows_per_part, n);
   const int r1 = min(r0 + rows_per_part, n);
   floatx4 acc[4][4];
@@ -267,7 +268,7 @@ void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
           *reinterpret_cast<float4*>(part + static_cast<int64_t>(from_m ? d_in + c : c) * ldp + ob) =
               make_float4(acc[t][0][r], acc[t][1][r], acc[t][2][r], acc[t][3][r]);
       }
-    if (blockIdx.z == 0 && q == 0) {
+    if (bz == 0 && q == 0) {
       float v[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
@@ -275,6 +276,14 @@ void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H,
       *reinterpret_cast<float4*>(part + static_cast<int64_t>(K2) * ldp + ob) = make_float4(v[0], v[1], v[2], v[3]);
     }
   }
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(kWgradDepth <= 4 ? 2 : 1, kWgradDepth <= 4 ? 2 : 1)))
+void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H, const float* __restrict__ M, int d_in,
+             const float* __restrict__ dZ, int ldz, int ldp, float* __restrict__ partial) {
+  wgrad_block<VEC>(sizes, H, M, d_in, dZ, ldz, ldp, partial, blockIdx.x, blockIdx.y, blockIdx.z, gridDim.x);
 }
 
 // One float4 of output per thread group of four: group g sums the parts
@@ -533,15 +542,20 @@ __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes
 constexpr int kScanTile = 1024;
 constexpr int kLongList = 16;   // transpose lists longer than this take a workgroup each
 
-__global__ __launch_bounds__(256) void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt,
-                                                  int32_t* __restrict__ off, int32_t* __restrict__ pos,
-                                                  uint32_t* __restrict__ ticket, uint64_t* __restrict__ words,
-                                                  uint32_t* __restrict__ n_long, int32_t* __restrict__ long_rows,
-                                                  int scan_blocks, ReduceArgs fold) {
-  // workgroups past the scan's run the weight gradient's reduction of the
-  // same layer (independent of the scan: one launch for both)
+template <bool VEC>
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(kWgradDepth <= 4 ? 2 : 1, kWgradDepth <= 4 ? 2 : 1)))
+void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt, int32_t* __restrict__ off,
+                int32_t* __restrict__ pos, uint32_t* __restrict__ ticket, uint64_t* __restrict__ words,
+                uint32_t* __restrict__ n_long, int32_t* __restrict__ long_rows, int scan_blocks, WgradArgs wg) {
+  // workgroups past the scan's run the same layer's weight-gradient
+  // products (independent of the scan: one launch for both; the scan's
+  // workgroups come first, so its tiles start before the products fill the
+  // CUs)
   if (static_cast<int>(blockIdx.x) >= scan_blocks) {
-    wgrad_reduce_block(fold, blockIdx.x - scan_blocks);
+    const int w = blockIdx.x - scan_blocks;
+    wgrad_block<VEC>(wg.sizes, wg.H, wg.M, wg.d_in, wg.dZ, wg.ldz, wg.ldp, wg.partial, w % wg.parts,
+                     (w / wg.parts) % wg.ytiles, w / (wg.parts * wg.ytiles), wg.parts);
     return;
   }
   __shared__ int s_tile;
@@ -606,12 +620,18 @@ __global__ __launch_bounds__(256) void k_csc_scan(const int32_t* __restrict__ si
 
 // Thread per edge slot: the edge (v <- u) takes the next place of u and
 // stores (v, 1/k_v) there.
+// Workgroups past fill_blocks run the same layer's weight-gradient
+// reduction (it only needs the products of the launch before).
 __global__ __launch_bounds__(256) void k_csc_fill(const int32_t* __restrict__ sizes, EdgeView ev,
                                                   int32_t* __restrict__ pos, const int32_t* __restrict__ off,
-                                                  int2* __restrict__ csc) {
+                                                  int2* __restrict__ csc, int fill_blocks, ReduceArgs fold) {
+  if (static_cast<int>(blockIdx.x) >= fill_blocks) {
+    wgrad_reduce_block(fold, blockIdx.x - fill_blocks);
+    return;
+  }
   for_each_edge_slot(ev, load_size(&sizes[kNDst]), load_size(&sizes[kNSrc]),
                      static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x,
-                     static_cast<int64_t>(gridDim.x) * blockDim.x, [&](int64_t v, int32_t u, int32_t k) {
+                     static_cast<int64_t>(fill_blocks) * blockDim.x, [&](int64_t v, int32_t u, int32_t k) {
                        const int32_t slot = atomicAdd(&pos[u], 1);
                        if (slot < off[u + 1] && slot < ev.cap_nnz)
                          csc[slot] = make_int2(static_cast<int32_t>(v), __float_as_int(1.f / static_cast<float>(k)));
@@ -944,8 +964,8 @@ int wgrad_parts(int64_t cap_rows, int d_in, int d_out) {
 
 hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, int d_in, const float* dZ, int ldz,
                         int d_out, int64_t cap_rows, float* partial, float* d_self, float* d_neigh,
-                        float* d_bias, const float* loss_rows, int n_loss, float* loss, ReduceArgs* fold,
-                        hipStream_t s) {
+                        float* d_bias, const float* loss_rows, int n_loss, float* loss, WgradArgs* defer,
+                        ReduceArgs* fold, hipStream_t s) {
   const int parts = wgrad_parts(cap_rows, d_in, d_out);
   const int ldp = wgrad_ldp(d_out);
   const dim3 grid(parts, (ldp + 63) / 64, 2 * ((d_in + 63) / 64));
@@ -953,18 +973,21 @@ hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, in
     return hipErrorInvalidValue;
   const bool vec = d_in % 4 == 0 && reinterpret_cast<uintptr_t>(H) % 16 == 0 &&
                    reinterpret_cast<uintptr_t>(M) % 16 == 0;
-  if (vec)
-    hipLaunchKernelGGL(k_wgrad<true>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
-  else
-    hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
   const int64_t outs = static_cast<int64_t>(2 * d_in + 1) * (ldp / 4);
   const ReduceArgs r{partial, parts, d_in, d_out, ldp, d_self, d_neigh, d_bias, loss_rows, n_loss, loss,
                      static_cast<int>((outs + 63) / 64) + (loss ? 1 : 0)};
-  if (fold) {
-    *fold = r;
-    return hipGetLastError();
+  if (defer) {
+    *defer = WgradArgs{sizes, H, M, d_in, dZ, ldz, ldp, partial, parts, static_cast<int>(grid.y),
+                       static_cast<int>(grid.z), vec ? 1 : 0};
+  } else if (vec) {
+    hipLaunchKernelGGL(k_wgrad<true>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
+  } else {
+    hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
   }
-  hipLaunchKernelGGL(k_wgrad_reduce, dim3(static_cast<unsigned>(r.blocks)), dim3(256), 0, s, r);
+  if (fold)
+    *fold = r;
+  else
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3(static_cast<unsigned>(r.blocks)), dim3(256), 0, s, r);
   return hipGetLastError();
 }
 
@@ -1009,17 +1032,27 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
                                 int64_t cap_nnz, int32_t fanout, const float* dM, const float* out, int d, float* dH,
                                 int64_t cap_dst, int64_t cap_src, int32_t* cnt, int32_t* off, int32_t* pos,
                                 uint32_t* scan_state, int2* csc, int32_t* long_rows, float* table, const int32_t* ids,
-                                int64_t num_nodes, float lr, const ReduceArgs* fold, hipStream_t s) {
+                                int64_t num_nodes, float lr, const WgradArgs* defer, const ReduceArgs* fold,
+                                hipStream_t s) {
   const EdgeView ev{indptr, local, cap_nnz, fanout};
   // scan_state: [0] the tile ticket, [1] the long-row count, then the
   // look-back words
   const int scan_blocks = static_cast<int>(csc_scan_tiles(cap_src));
-  const ReduceArgs none{};
-  hipLaunchKernelGGL(k_csc_scan, dim3(static_cast<unsigned>(scan_blocks + (fold ? fold->blocks : 0))), dim3(256), 0,
-                     s, sizes, cnt, off, pos, scan_state, reinterpret_cast<uint64_t*>(scan_state + 2), scan_state + 1,
-                     long_rows, scan_blocks, fold ? *fold : none);
+  const WgradArgs no_wg{};
+  const int wg_blocks = defer ? defer->parts * defer->ytiles * defer->ztiles : 0;
+  const dim3 scan_grid(static_cast<unsigned>(scan_blocks + wg_blocks));
+  uint64_t* words = reinterpret_cast<uint64_t*>(scan_state + 2);
+  if (!defer || defer->vec)
+    hipLaunchKernelGGL(k_csc_scan<true>, scan_grid, dim3(256), 0, s, sizes, cnt, off, pos, scan_state, words,
+                       scan_state + 1, long_rows, scan_blocks, defer ? *defer : no_wg);
+  else
+    hipLaunchKernelGGL(k_csc_scan<false>, scan_grid, dim3(256), 0, s, sizes, cnt, off, pos, scan_state, words,
+                       scan_state + 1, long_rows, scan_blocks, *defer);
   const int64_t slots = std::max<int64_t>(cap_dst, 1) * std::max(fanout, 1);
-  hipLaunchKernelGGL(k_csc_fill, dim3(grid_of(slots, 1 << 16)), dim3(256), 0, s, sizes, ev, pos, off, csc);
+  const int fill_blocks = static_cast<int>(grid_of(slots, 1 << 16));
+  const ReduceArgs no_red{};
+  hipLaunchKernelGGL(k_csc_fill, dim3(static_cast<unsigned>(fill_blocks + (fold ? fold->blocks : 0))), dim3(256), 0,
+                     s, sizes, ev, pos, off, csc, fill_blocks, fold ? *fold : no_red);
   const int chunks = d / 4;
   // each grid ends with kLongGrid workgroups for the long lists
   if (table) {
