@@ -542,21 +542,25 @@ __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes
 constexpr int kScanTile = 1024;
 constexpr int kLongList = 16;   // transpose lists longer than this take a workgroup each
 
-template <bool VEC>
-__global__ __launch_bounds__(256)
-__attribute__((amdgpu_waves_per_eu(kWgradDepth <= 4 ? 2 : 1, kWgradDepth <= 4 ? 2 : 1)))
+// WG = 0: the scan alone (its own small register and LDS footprint);
+// 1, 2: workgroups past the scan's run the same layer's weight-gradient
+// products (16-byte or scalar loads of H and M), independent of the scan:
+// one launch for both; the scan's workgroups come first, so its tiles
+// start before the products fill the CUs.
+constexpr int wg_occupancy(int wg) { return wg == 0 ? 8 : (kWgradDepth <= 4 ? 2 : 1); }
+
+template <int WG>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(wg_occupancy(WG), wg_occupancy(WG))))
 void k_csc_scan(const int32_t* __restrict__ sizes, int32_t* __restrict__ cnt, int32_t* __restrict__ off,
                 int32_t* __restrict__ pos, uint32_t* __restrict__ ticket, uint64_t* __restrict__ words,
                 uint32_t* __restrict__ n_long, int32_t* __restrict__ long_rows, int scan_blocks, WgradArgs wg) {
-  // workgroups past the scan's run the same layer's weight-gradient
-  // products (independent of the scan: one launch for both; the scan's
-  // workgroups come first, so its tiles start before the products fill the
-  // CUs)
-  if (static_cast<int>(blockIdx.x) >= scan_blocks) {
-    const int w = blockIdx.x - scan_blocks;
-    wgrad_block<VEC>(wg.sizes, wg.H, wg.M, wg.d_in, wg.dZ, wg.ldz, wg.ldp, wg.partial, w % wg.parts,
-                     (w / wg.parts) % wg.ytiles, w / (wg.parts * wg.ytiles), wg.parts);
-    return;
+  if constexpr (WG != 0) {
+    if (static_cast<int>(blockIdx.x) >= scan_blocks) {
+      const int w = blockIdx.x - scan_blocks;
+      wgrad_block<WG == 1>(wg.sizes, wg.H, wg.M, wg.d_in, wg.dZ, wg.ldz, wg.ldp, wg.partial, w % wg.parts,
+                           (w / wg.parts) % wg.ytiles, w / (wg.parts * wg.ytiles), wg.parts);
+      return;
+    }
   }
   __shared__ int s_tile;
   __shared__ int32_t s_excl;
@@ -1042,11 +1046,14 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
   const int wg_blocks = defer ? defer->parts * defer->ytiles * defer->ztiles : 0;
   const dim3 scan_grid(static_cast<unsigned>(scan_blocks + wg_blocks));
   uint64_t* words = reinterpret_cast<uint64_t*>(scan_state + 2);
-  if (!defer || defer->vec)
-    hipLaunchKernelGGL(k_csc_scan<true>, scan_grid, dim3(256), 0, s, sizes, cnt, off, pos, scan_state, words,
-                       scan_state + 1, long_rows, scan_blocks, defer ? *defer : no_wg);
+  if (!defer)
+    hipLaunchKernelGGL(k_csc_scan<0>, scan_grid, dim3(256), 0, s, sizes, cnt, off, pos, scan_state, words,
+                       scan_state + 1, long_rows, scan_blocks, no_wg);
+  else if (defer->vec)
+    hipLaunchKernelGGL(k_csc_scan<1>, scan_grid, dim3(256), 0, s, sizes, cnt, off, pos, scan_state, words,
+                       scan_state + 1, long_rows, scan_blocks, *defer);
   else
-    hipLaunchKernelGGL(k_csc_scan<false>, scan_grid, dim3(256), 0, s, sizes, cnt, off, pos, scan_state, words,
+    hipLaunchKernelGGL(k_csc_scan<2>, scan_grid, dim3(256), 0, s, sizes, cnt, off, pos, scan_state, words,
                        scan_state + 1, long_rows, scan_blocks, *defer);
   const int64_t slots = std::max<int64_t>(cap_dst, 1) * std::max(fanout, 1);
   const int fill_blocks = static_cast<int>(grid_of(slots, 1 << 16));
