@@ -42,6 +42,29 @@ def test_no_oracle_symbols_in_library(L):
             getattr(L, n)
 
 
+def test_product_and_oracle_share_no_code():
+    """The HIP path and the oracle are written apart: no source of the
+    package names the oracle, no source of the oracle names the package or
+    its kernels' sources, and neither includes a header of the other."""
+    def sources(d, exts):
+        for base, _, files in os.walk(os.path.join(ROOT, d)):
+            if "__pycache__" in base or "_build" in base:
+                continue
+            for f in files:
+                if f.endswith(exts):
+                    yield os.path.join(base, f)
+    prod = list(sources("paper_2010_05337_amd", (".py", ".hip", ".hpp", ".h", ".cpp")))
+    orc = list(sources("oracle", (".py", ".c", ".h")))
+    assert prod and orc
+    for f in prod:
+        text = open(f).read()
+        assert not re.search(r"^\s*(import|from)\s+oracle\b|\borc_[a-z]|\boracle\.", text, re.M), f
+    for f in orc:
+        text = open(f).read()
+        assert not re.search(r"^\s*(import|from)\s+paper_2010_05337_amd\b|#\s*include\s*[<\"].*"
+                             r"(gmb\.h|kernels\.hpp|common\.hpp|scan\.hpp|philox\.hpp)", text, re.M), f
+
+
 def test_abi_version(L):
     assert L.gmb_abi_version() == 1
 
