@@ -540,15 +540,41 @@ def main():
         b = i % nb
         ln = lanes[i % nstreams]
         with torch.cuda.stream(streams[i % nstreams]):
-            blocks = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b),
-                                       workspace=ln["ws_sample"])
-            gmb.gather_features(blocks, feats, out=ln["x"])
+            ln["blocks"] = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b),
+                                             workspace=ln["ws_sample"])
+            gmb.gather_features(ln["blocks"], feats, out=ln["x"])
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     for i in range(K):
         step_sg(i, S)
     torch.cuda.synchronize()
     T2 = time.perf_counter() - t2
+    for ln in lanes:
+        ln["csr"].check_status()
+
+    # pass C split: the same K steps with only the sampling, then with only
+    # the gather (each lane gathering the batch it sampled last), S streams
+    # in flight; together with pass C they show whether the two stages
+    # overlap or compete for the memory system
+    def step_s(i, nstreams):
+        b = i % nb
+        ln = lanes[i % nstreams]
+        with torch.cuda.stream(streams[i % nstreams]):
+            ln["blocks"] = gmb.sample_blocks(ln["csr"], batches[b], fanouts, wl.batch_key(b),
+                                             workspace=ln["ws_sample"])
+
+    def step_g(i, nstreams):
+        ln = lanes[i % nstreams]
+        with torch.cuda.stream(streams[i % nstreams]):
+            gmb.gather_features(ln["blocks"], feats, out=ln["x"])
+    split = {}
+    for what, fn in (("sample_only", step_s), ("gather_only", step_g)):
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for i in range(K):
+            fn(i, S)
+        torch.cuda.synchronize()
+        split[what] = time.perf_counter() - t
     for ln in lanes:
         ln["csr"].check_status()
 
@@ -632,7 +658,10 @@ def main():
                                 "frac_of_peak": (b_sample + b_gather) / (ts + tg) / 1e9 / HBM_PEAK_GBPS,
                                 "pipelined_GBps": (b_sample + b_gather) / T2 / 1e9,
                                 "pipelined_frac_of_peak": (b_sample + b_gather) / T2 / 1e9 / HBM_PEAK_GBPS,
-                                "pipelined_streams": S}
+                                "pipelined_streams": S,
+                                "pipelined_us_per_batch": 1e6 * T2 / K,
+                                "pipelined_sample_only_us_per_batch": 1e6 * split["sample_only"] / K,
+                                "pipelined_gather_only_us_per_batch": 1e6 * split["gather_only"] / K}
     res["stream_copy_GBps"] = copy_GBps
     peak = BF16_MFMA_PEAK_TFLOPS if bf16 else FP32_MFMA_PEAK_TFLOPS
     res["forward"] = {"alg_bytes": b_fwd, "linear_flops": flops,
