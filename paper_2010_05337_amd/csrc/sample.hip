@@ -350,7 +350,10 @@ __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* 
 // table[u] while it is rewritten: they see either a tag or the local id,
 // never their own tag, so their flag is 0 either way, and either one gives
 // them the right local id; so the table store needs no ordering within
-// this kernel.
+// this kernel.  After the last hop no kernel reads a new vertex's slot
+// (the cleanup reads only the seeds' slots), so the last hop leaves its
+// new vertices' tags in place: its repeats then always take the LDS or the
+// deferred route, and the cleanup resets the slots as it does the others.
 template <int NV, bool WIDE, int ITEMS>
 __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga, int32_t* ids,
                                                        uint32_t* table, uint32_t* status) {
@@ -427,7 +430,7 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
     if ((flags >> q) & 1u) {
       ids[r] = u[q];
       a.local[base + q] = r;
-      table[u[q]] = static_cast<uint32_t>(r);   // read by later kernels only
+      if (a.next_sizes) table[u[q]] = static_cast<uint32_t>(r);   // read by the later hops
       s_pos[threadIdx.x * ITEMS + q] = r;
 #pragma unroll
       for (int v = 1; v < NV; ++v) {
