@@ -382,7 +382,7 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
     if (e != hipSuccess) return hip_fail(e, "relabel launch");
   }
   const gmb::HopArgs& last = hops[num_layers - 1];
-  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, num_seeds, table, csr->num_nodes, status,
+  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, table, csr->num_nodes,
                           gmb::DeferredArgs{last.local, last.sizes, std::max<int64_t>(last.cap_nnz, 1)}, s);
   if (e != hipSuccess) return hip_fail(e, "cleanup launch");
   *out = res;

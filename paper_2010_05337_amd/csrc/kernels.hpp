@@ -100,9 +100,8 @@ hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h,
                          const DeferredArgs& fix, hipStream_t s);
 hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
                          int items, int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s);
-hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src, int32_t num_seeds,
-                          uint32_t* table, int64_t num_nodes, uint32_t* status, const DeferredArgs& fix,
-                          hipStream_t s);
+hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src, uint32_t* table,
+                          int64_t num_nodes, const DeferredArgs& fix, hipStream_t s);
 
 // gather.hip
 hipError_t launch_gather(const int32_t* ids, const int32_t* n_dev, int64_t n_cap, const void* feats,

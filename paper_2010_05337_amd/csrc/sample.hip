@@ -25,9 +25,9 @@
 //   k_assign(h)   scan of the "first occurrence" flags (new vertex number
 //                 n_dst + rank) together with the degree scans of the new
 //                 vertices for the later hops; writes every edge's local id
-//   k_cleanup     table entries of every vertex of the batch back to empty;
-//                 a seed whose slot does not hold its position was listed
-//                 twice
+//   k_cleanup     the table back to empty (the whole table when that is
+//                 cheaper, else the slots of the batch's vertices); the
+//                 last hop's deferred local ids
 #include <algorithm>
 
 #include "common.hpp"
@@ -78,9 +78,9 @@ __global__ __launch_bounds__(256) void k_state_init(uint32_t* table, uint32_t* s
   if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
 
-// One workgroup.  Seeds -> ids[0:B] and their table slots (atomicMin, so a
-// vertex listed twice keeps its first position); segment 0's degree scans
-// for every hop; clears the look-back words and the size words.
+// One workgroup.  Seeds -> ids[0:B]; segment 0's degree scans for every
+// hop; clears the look-back words and the size words.  (The seeds' table
+// slots are written by the first hop's sampling kernel.)
 constexpr int kSeedItems = 4;
 // one workgroup: 1024 threads while the register budget allows (NV <= 4)
 template <int NV>
@@ -239,12 +239,14 @@ __global__ __launch_bounds__(256) void k_sample(CsrArgs ga, const int32_t* ids, 
   row_range_t<WIDE>(g, vc, begin, end);
   deferred_store(fix, tid, it);
   if (p >= n_dst) return;
-  // first hop: the seed's table slot is its position.  A plain store: the
-  // edges emitted meanwhile lower slots to tags >= 2^31 only, so the slot
-  // ends at p whatever the order; a seed listed twice leaves one of its
-  // copies disagreeing with the slot, which the cleanup reports.
+  // first hop: the seed's table slot is its position, lowered with
+  // atomicMin: the edges emitted meanwhile lower slots to tags >= 2^31
+  // only, so the slot ends at p whatever the order, and a seed listed
+  // twice finds its other copy's position there (checked at the end, so
+  // that the wait for the old value does not hold up the sampling)
+  uint32_t seed_old = kEmpty;
   if (check_seeds && lane == 0) {
-    if (valid) table[v] = static_cast<uint32_t>(p);
+    if (valid) seed_old = atomicMin(&table[v], static_cast<uint32_t>(p));
     else raise_status(status, GMB_STATUS_ERANGE);
   }
   if (!valid) return;   // an invalid vertex's clamped degree was 0
@@ -280,6 +282,7 @@ __global__ __launch_bounds__(256) void k_sample(CsrArgs ga, const int32_t* ids, 
     }
   }
   if (pos >= 0) emit_edge(pos, u, nbr, table, g.num_nodes, status);
+  if (seed_old < kEdgeTag) raise_status(status, GMB_STATUS_EDUP);
 }
 
 // Fan-outs above 64: one thread per destination; the block's output row
@@ -300,9 +303,9 @@ __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* 
   const int32_t n_dst = load_size(&sizes[kNDst]);
   if (p >= n_dst) return;
   const int32_t v = ids[p];
-  if (check_seeds) {   // the seed's table slot (see k_sample)
-    if (valid_vertex(v, g.num_nodes)) table[v] = static_cast<uint32_t>(p);
-    else raise_status(status, GMB_STATUS_ERANGE);
+  if (check_seeds) {   // the seed's table slot and the repeat check (see k_sample)
+    if (!valid_vertex(v, g.num_nodes)) raise_status(status, GMB_STATUS_ERANGE);
+    else if (atomicMin(&table[v], static_cast<uint32_t>(p)) < kEdgeTag) raise_status(status, GMB_STATUS_EDUP);
   }
   if (!valid_vertex(v, g.num_nodes)) return;
   int64_t begin, end;
@@ -473,22 +476,28 @@ __global__ __launch_bounds__(kScanBlock) void k_assign(AssignArgs a, CsrArgs ga,
   }
 }
 
-// Resets the table entries of every vertex of the batch and resolves the
-// last hop's deferred local ids (the table is not read for those).
-__global__ __launch_bounds__(256) void k_cleanup(const int32_t* ids, int64_t cap_src, int32_t num_seeds,
-                                                 const int32_t* final_sizes, uint32_t* table,
-                                                 int64_t num_nodes, uint32_t* status, DeferredArgs fix) {
+// Resolves the last hop's deferred local ids (the table is not read for
+// those) and clears the table: if `whole`, every slot, thread i storing
+// slots 4i..4i+3 with one 16-byte store (the table is 16-byte aligned) and
+// the first threads the num_nodes % 4 slots past the last full group; else
+// the slots of the batch's vertices, one random store each.
+__global__ __launch_bounds__(256) void k_cleanup(const int32_t* ids, int64_t cap_src, const int32_t* final_sizes,
+                                                 uint32_t* table, int64_t num_nodes, int whole, DeferredArgs fix) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   DeferredItem it = deferred_read(fix, i);
+  if (whole) {
+    deferred_fetch(fix, it);
+    deferred_store(fix, i, it);
+    const int64_t full = num_nodes >> 2;
+    if (i < full) reinterpret_cast<uint4*>(table)[i] = make_uint4(kEmpty, kEmpty, kEmpty, kEmpty);
+    if (i < (num_nodes & 3)) table[(full << 2) + i] = kEmpty;
+    return;
+  }
   const int32_t n = load_size(&final_sizes[kNSrc]);
   const int32_t u = ids[i < cap_src ? i : cap_src - 1];
   const bool ok = i < n && valid_vertex(u, num_nodes);
-  // a seed's slot still holds its position unless the seed list holds the
-  // vertex twice (no later step writes a seed's slot)
-  const uint32_t slot = (ok && i < num_seeds) ? table[u] : static_cast<uint32_t>(i);
   deferred_fetch(fix, it);
   deferred_store(fix, i, it);
-  if (slot != static_cast<uint32_t>(i)) raise_status(status, GMB_STATUS_EDUP);
   if (ok) table[u] = kEmpty;
 }
 
@@ -597,12 +606,15 @@ hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, 
   return hipGetLastError();
 }
 
-hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src, int32_t num_seeds,
-                          uint32_t* table, int64_t num_nodes, uint32_t* status, const DeferredArgs& fix,
-                          hipStream_t s) {
-  const int64_t threads = std::max(cap_src, fix.cap);
-  hipLaunchKernelGGL(k_cleanup, dim3(grid_for(threads)), dim3(256), 0, s, ids,
-                     std::max<int64_t>(cap_src, 1), num_seeds, final_sizes, table, num_nodes, status, fix);
+hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src, uint32_t* table,
+                          int64_t num_nodes, const DeferredArgs& fix, hipStream_t s) {
+  // the whole table in 16-byte stores costs about as much HBM time as
+  // eight random 4-byte stores per slot it covers; clear it whole when it
+  // has no more than eight slots per possible source of the batch
+  const bool whole = num_nodes <= 8 * std::max<int64_t>(cap_src, 1);
+  const int64_t threads = std::max(whole ? std::max<int64_t>(num_nodes / 4, 4) : cap_src, fix.cap);
+  hipLaunchKernelGGL(k_cleanup, dim3(grid_for(threads)), dim3(256), 0, s, ids, std::max<int64_t>(cap_src, 1),
+                     final_sizes, table, num_nodes, whole ? 1 : 0, fix);
   return hipGetLastError();
 }
 

@@ -115,13 +115,29 @@ def test_sampling_is_deterministic_and_keyed(dg, tiny):
     assert not np.array_equal(a[1]["nbr"], c[1]["nbr"])
 
 
-def test_state_is_clean_after_each_call(dg, tiny):
-    csr = csr_on_device(tiny)
-    seeds = dg.permutation(10000, 6)[:64]
-    gpu_blocks(csr, seeds, [5, 5], 1)
+def _table_is_clear(csr):
     torch.cuda.synchronize()
     table = csr.state[256:256 + 4 * csr.num_nodes].view(torch.int32)
-    assert bool((table == -1).all())
+    return bool((table == -1).all())
+
+
+@pytest.mark.parametrize("n, num_seeds, fanouts, whole", [
+    (10000, 64, [5, 5], True), (10000, 8, [2], False), (10003, 64, [5, 5], True), (10003, 8, [2], False)])
+def test_state_is_clean_after_each_call(orc, dg, n, num_seeds, fanouts, whole):
+    """The cleanup clears the dedup table in one of two ways: all of it
+    with 16-byte stores when it holds at most eight slots per possible
+    source of the batch, else the slots of the batch's vertices one by one;
+    10,003 vertices leave three slots past the last 16-byte group."""
+    print(f"ER N={n}, {num_seeds} seeds, fanouts={fanouts}", flush=True)
+    g = dg.er_directed(n, 10.0, 101)
+    csr = csr_on_device(g)
+    seeds = dg.permutation(n, 6)[:num_seeds]
+    for key in (1, 2):
+        blocks, host = gpu_blocks(csr, seeds, fanouts, key)
+        assert (n <= 8 * blocks.input_capacity) == whole
+        assert_blocks_equal(host, orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, key), f"key {key}")
+        assert _table_is_clear(csr)
+    csr.check_status()
 
 
 def test_device_errors_are_reported(orc, dg, tiny):
@@ -134,6 +150,13 @@ def test_device_errors_are_reported(orc, dg, tiny):
     with pytest.raises(gmb.GmbError) as e:
         csr.check_status()
     assert e.value.code == -5
+    assert _table_is_clear(csr)
+    # a repeated seed under fan-outs above 64 (the one-thread sampler)
+    gpu_blocks(csr, [7, 3, 9, 3], [70], 1)
+    with pytest.raises(gmb.GmbError) as e:
+        csr.check_status()
+    assert e.value.code == -5
+    assert _table_is_clear(csr)
     # the state is usable again afterwards
     seeds = dg.permutation(10000, 9)[:64]
     _, host = gpu_blocks(csr, seeds, [5, 5], 2)
