@@ -11,7 +11,8 @@
  * Conventions shared by every entry point
  *   - Pointers documented "device" are HIP device pointers; "host" are host
  *     pointers.  Device buffers are owned by the caller; the library never
- *     allocates, frees or keeps device memory.
+ *     allocates or frees device memory, and keeps none but the fixed scratch
+ *     array of gmb_sample_blocks_noalloc (a static device array).
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     All device work of a call is enqueued on that stream; a call returns
  *     as soon as the work is enqueued, unless it says it synchronises.
@@ -182,6 +183,35 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
                       const int32_t* fanouts, int32_t num_layers, uint64_t seed,
                       void* state, size_t state_bytes, void* ws, size_t ws_bytes,
                       gmb_blocks* out, void* stream);
+
+/* ---- sampling without allocation ---------------------------------------- */
+
+/* Bytes of the fixed device scratch of gmb_sample_blocks_noalloc. */
+#define GMB_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* For callers that cannot allocate device memory or cannot pass a
+ * workspace: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  The same sampling as gmb_sample_blocks (same
+ * kernels, the same blocks bit for bit), with the scratch that the call
+ * needs besides its outputs (the relabel scans' look-back words and tickets,
+ * the running edge counts) in a fixed array of GMB_NOALLOC_SCRATCH_BYTES
+ * that the library holds in device memory, one copy per GPU, from the first
+ * call on that GPU until the process ends.  The call allocates nothing.
+ *   out_buf    device buffer for the blocks, 256-byte aligned, caller-owned;
+ *              gmb_sample_workspace_bytes(...) bytes for the same shapes
+ *              always suffice (the blocks take its first part).  The blocks
+ *              point into it and stay valid until it is reused.
+ *   others     as for gmb_sample_blocks.
+ * Errors: those of gmb_sample_blocks, and GMB_ENOSPC when the shapes need
+ * more scratch than the fixed array holds (about 8 bytes per 1000 edges of
+ * a hop's capacity); nothing is enqueued then.  The scratch is cleared by
+ * the call's own first kernel.  Every call on one GPU shares that GPU's
+ * array: calls that overlap in time on one GPU (other streams, other host
+ * threads) race and give wrong blocks, so order them on one stream. */
+int gmb_sample_blocks_noalloc(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds,
+                              const int32_t* fanouts, int32_t num_layers, uint64_t seed,
+                              void* state, size_t state_bytes, void* out_buf, size_t out_bytes,
+                              gmb_blocks* out, void* stream);
 
 /* Synchronises `stream` and copies the device sizes to host
  * sizes[num_layers][3] = {n_dst, n_src, nnz} (layer order). */

@@ -33,7 +33,7 @@ EXPORTS = (
     "gmb_read_sizes", "gmb_gather_features", "gmb_forward_workspace_bytes",
     "gmb_forward_hidden_offset", "gmb_sage_forward", "gmb_sage_forward_fused", "gmb_backward_workspace_bytes",
     "gmb_sage_backward", "gmb_sgd_update", "gmb_backward_embedding_workspace_bytes",
-    "gmb_sage_backward_embedding",
+    "gmb_sage_backward_embedding", "gmb_sample_blocks_noalloc",
 )
 
 
@@ -104,6 +104,9 @@ def lib() -> ctypes.CDLL:
         L.gmb_sample_blocks.restype = ctypes.c_int
         L.gmb_sample_blocks.argtypes = [ctypes.POINTER(CsrStruct), vp, i32, vp, i32, u64, vp, sz, vp,
                                         sz, ctypes.POINTER(BlocksStruct), vp]
+        L.gmb_sample_blocks_noalloc.restype = ctypes.c_int
+        L.gmb_sample_blocks_noalloc.argtypes = [ctypes.POINTER(CsrStruct), vp, i32, vp, i32, u64, vp, sz, vp,
+                                                sz, ctypes.POINTER(BlocksStruct), vp]
         L.gmb_read_sizes.restype = ctypes.c_int
         L.gmb_read_sizes.argtypes = [ctypes.POINTER(BlocksStruct), vp, vp]
         L.gmb_gather_features.restype = ctypes.c_int

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "gmb.h"
@@ -57,10 +58,17 @@ struct HopPlan {
 struct SamplePlan {
   int num_layers;
   HopPlan hop[GMB_MAX_LAYERS];
-  size_t off_ids, off_sizes, off_zero;
-  int64_t num_zero_words;
-  int32_t num_size_words;   // 4 per layer, then the running edge count of every hop
+  // the blocks (outputs), relative to the output buffer
+  size_t off_ids, off_sizes;
   int64_t cap_ids;
+  size_t out_total;
+  // scratch, relative to the scratch buffer: the look-back words and
+  // tickets of the relabel scans (cleared by the seed kernel), the running
+  // edge count of every hop
+  size_t off_zero, off_totals;
+  int64_t num_zero_words;
+  size_t scratch_total;
+  // one workspace holding both: the outputs, then the scratch
   size_t total;
 };
 
@@ -82,7 +90,6 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
 
   SamplePlan p{};
   p.num_layers = num_layers;
-  size_t off = 0;
   int64_t cap_dst = num_seeds;
   int64_t zero_words = 0;
   for (int h = 0; h < num_layers; ++h) {
@@ -105,14 +112,11 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
     cap_dst = hp.cap_src;
   }
   p.cap_ids = p.hop[num_layers - 1].cap_src;
+  size_t off = 0;
   p.off_ids = off;
   off = align_up(off + sizeof(int32_t) * std::max<int64_t>(p.cap_ids, 1));
-  p.num_size_words = 4 * num_layers + kTotalsWords;
   p.off_sizes = off;
-  off = align_up(off + sizeof(int32_t) * p.num_size_words);
-  p.off_zero = off;
-  p.num_zero_words = zero_words;
-  off = align_up(off + sizeof(uint64_t) * zero_words);
+  off = align_up(off + sizeof(int32_t) * 4 * num_layers);
   for (int h = 0; h < num_layers; ++h) {
     HopPlan& hp = p.hop[h];
     hp.off_indptr = off;
@@ -122,8 +126,159 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
     hp.off_local = off;
     off = align_up(off + sizeof(int32_t) * std::max<int64_t>(hp.cap_nnz, 1));
   }
-  p.total = off;
+  p.out_total = off;
+  off = 0;
+  p.off_zero = off;
+  p.num_zero_words = zero_words;
+  off = align_up(off + sizeof(uint64_t) * zero_words);
+  p.off_totals = off;
+  off = align_up(off + sizeof(int32_t) * kTotalsWords);
+  p.scratch_total = off;
+  p.total = p.out_total + p.scratch_total;
   *plan = p;
+  return GMB_OK;
+}
+
+// Host-side checks shared by the sampling entry points (the buffers for the
+// blocks and the scratch are checked by each).
+int check_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, const int32_t* fanouts,
+                   int32_t num_layers, void* state, size_t state_bytes, SamplePlan* p) {
+  if (!csr) return fail(GMB_EINVAL, "csr is NULL");
+  if (!csr->indptr || (!csr->indices && csr->num_edges > 0))
+    return fail(GMB_EINVAL, "csr has a NULL array");
+  if (csr->indptr_bits != 32 && csr->indptr_bits != 64)
+    return fail(GMB_EINVAL, "indptr_bits=%d (32 or 64)", csr->indptr_bits);
+  if (csr->num_edges < 0 || (csr->indptr_bits == 32 && csr->num_edges > kMaxInt32))
+    return fail(GMB_EINVAL, "num_edges=%lld does not fit the row-offset type", static_cast<long long>(csr->num_edges));
+  if (num_seeds > 0 && !seeds) return fail(GMB_EINVAL, "seeds is NULL");
+  int st = plan_sampling(num_seeds, fanouts, num_layers, csr->num_nodes, p);
+  if (st != GMB_OK) return st;
+  if (!state) return fail(GMB_EINVAL, "state is NULL");
+  if (reinterpret_cast<uintptr_t>(state) % kAlign) return fail(GMB_EINVAL, "state must be 256-byte aligned");
+  const size_t need = kStateHeader + align_up(sizeof(uint32_t) * static_cast<size_t>(csr->num_nodes));
+  if (state_bytes < need) return fail(GMB_ENOSPC, "state holds %zu bytes, %zu needed", state_bytes, need);
+  return GMB_OK;
+}
+
+// Enqueues the sampling kernels: the blocks go to `outb` (plan offsets
+// off_ids, off_sizes and the hops'), the scratch words to `scr`.
+int run_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, int32_t num_layers, uint64_t seed,
+                 void* state, const SamplePlan& p, char* outb, char* scr, gmb_blocks* out, hipStream_t s) {
+  int32_t* ids = reinterpret_cast<int32_t*>(outb + p.off_ids);
+  int32_t* sizes = reinterpret_cast<int32_t*>(outb + p.off_sizes);
+  uint64_t* zero = reinterpret_cast<uint64_t*>(scr + p.off_zero);
+  int32_t* totals = reinterpret_cast<int32_t*>(scr + p.off_totals);
+  uint32_t* status = static_cast<uint32_t*>(state);
+  uint32_t* table = reinterpret_cast<uint32_t*>(static_cast<char*>(state) + kStateHeader);
+
+  gmb::CsrArgs g{csr->indptr, csr->indices, csr->num_nodes, csr->indptr_bits == 64 ? 1 : 0};
+  gmb::HopArgs hops[GMB_MAX_LAYERS];
+  gmb_blocks res{};
+  res.num_layers = num_layers;
+  res.num_seeds = num_seeds;
+  for (int h = 0; h < num_layers; ++h) {
+    const HopPlan& hp = p.hop[h];
+    gmb::HopArgs& a = hops[h];
+    a.sizes = sizes + 4 * hp.layer;
+    a.indptr = reinterpret_cast<int32_t*>(outb + hp.off_indptr);
+    a.nbr = reinterpret_cast<int32_t*>(outb + hp.off_nbr);
+    a.local = reinterpret_cast<int32_t*>(outb + hp.off_local);
+    a.tiles = zero + hp.tiles_word;
+    a.ticket = reinterpret_cast<uint32_t*>(zero + hp.ticket_word);
+    a.tile_stride = hp.tile_stride;
+    a.cap_dst = hp.cap_dst;
+    a.cap_nnz = hp.cap_nnz;
+    a.cap_src = hp.cap_src;
+    a.fanout = hp.fanout;
+    a.layer = hp.layer;
+    gmb_block& bk = res.blk[hp.layer];
+    bk.indptr = a.indptr;
+    bk.indices = a.local;
+    bk.nbr = a.nbr;
+    bk.src_ids = ids;
+    bk.sizes = a.sizes;
+    bk.cap_dst = hp.cap_dst;
+    bk.cap_src = hp.cap_src;
+    bk.cap_nnz = hp.cap_nnz;
+    bk.fanout = hp.fanout;
+    bk.layer = hp.layer;
+  }
+
+  gmb::SeedArgs sa{};
+  sa.seeds = seeds;
+  sa.num_seeds = num_seeds;
+  sa.first_sizes = 4 * p.hop[0].layer;
+  sa.ids = ids;
+  sa.zero = zero;
+  sa.num_zero = p.num_zero_words;
+  sa.sizes = sizes;
+  sa.num_size_words = 4 * num_layers;
+  sa.totals = totals;
+  for (int h = 0; h < num_layers; ++h) {
+    sa.indptr[h] = hops[h].indptr;
+    sa.fanout[h] = hops[h].fanout;
+  }
+  const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
+  hipError_t e = gmb::launch_seed_scan(sa, num_layers, g, s);
+  if (e != hipSuccess) return hip_fail(e, "seed launch");
+  for (int h = 0; h < num_layers; ++h) {
+    // the first hop has nothing deferred: word 3 of a block's sizes is 0
+    gmb::DeferredArgs fix{hops[0].local, hops[0].sizes + 3 - gmb::kNnz, 1};
+    if (h > 0) fix = gmb::DeferredArgs{hops[h - 1].local, hops[h - 1].sizes, std::max<int64_t>(hops[h - 1].cap_nnz, 1)};
+    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, h == 0 ? 1 : 0, fix, s);
+    if (e != hipSuccess) return hip_fail(e, "sample launch");
+    gmb::AssignArgs aa{};
+    aa.nbr = hops[h].nbr;
+    aa.local = hops[h].local;
+    aa.sizes = hops[h].sizes;
+    aa.next_sizes = (h + 1 < num_layers) ? hops[h + 1].sizes : nullptr;
+    aa.tiles = hops[h].tiles;
+    aa.tile_stride = hops[h].tile_stride;
+    aa.ticket = hops[h].ticket;
+    aa.totals = totals;
+    aa.hop = h;
+    for (int v = 1; h + v < num_layers; ++v) {
+      aa.indptr[v] = hops[h + v].indptr;
+      aa.fanout[v] = hops[h + v].fanout;
+    }
+    e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, p.hop[h].items, ids, table, status, s);
+    if (e != hipSuccess) return hip_fail(e, "relabel launch");
+  }
+  const gmb::HopArgs& last = hops[num_layers - 1];
+  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, table, csr->num_nodes,
+                          gmb::DeferredArgs{last.local, last.sizes, std::max<int64_t>(last.cap_nnz, 1)}, s);
+  if (e != hipSuccess) return hip_fail(e, "cleanup launch");
+  *out = res;
+  return ok();
+}
+
+// The scratch of gmb_sample_blocks_noalloc: a fixed array in device memory
+// that every GPU the library runs on holds once, until the process ends.
+// Host code never uses the name itself (on the host it is only a stand-in
+// for the symbol): it uses the address hipGetSymbolAddress returns for the
+// current device, taken once per device.
+constexpr size_t kNoAllocScratchBytes = GMB_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`.
+int noalloc_scratch(char** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(GMB_EDEVICE, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || reinterpret_cast<uintptr_t>(p) % kAlign) return fail(GMB_EDEVICE, "scratch symbol has no aligned device address");
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *ptr = g_scratch_ptr[dev];
   return GMB_OK;
 }
 
@@ -279,114 +434,35 @@ size_t gmb_sample_workspace_bytes(int32_t num_seeds, const int32_t* fanouts, int
 int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds,
                       const int32_t* fanouts, int32_t num_layers, uint64_t seed, void* state,
                       size_t state_bytes, void* ws, size_t ws_bytes, gmb_blocks* out, void* stream) {
-  if (!csr) return fail(GMB_EINVAL, "csr is NULL");
-  if (!out) return fail(GMB_EINVAL, "out is NULL");
-  if (!csr->indptr || (!csr->indices && csr->num_edges > 0))
-    return fail(GMB_EINVAL, "csr has a NULL array");
-  if (csr->indptr_bits != 32 && csr->indptr_bits != 64)
-    return fail(GMB_EINVAL, "indptr_bits=%d (32 or 64)", csr->indptr_bits);
-  if (csr->num_edges < 0 || (csr->indptr_bits == 32 && csr->num_edges > kMaxInt32))
-    return fail(GMB_EINVAL, "num_edges=%lld does not fit the row-offset type", static_cast<long long>(csr->num_edges));
-  if (num_seeds > 0 && !seeds) return fail(GMB_EINVAL, "seeds is NULL");
   SamplePlan p;
-  int st = plan_sampling(num_seeds, fanouts, num_layers, csr->num_nodes, &p);
+  int st = check_sampling(csr, seeds, num_seeds, fanouts, num_layers, state, state_bytes, &p);
   if (st != GMB_OK) return st;
-  if (!state) return fail(GMB_EINVAL, "state is NULL");
-  if (state_bytes < gmb_sampler_state_bytes(csr->num_nodes))
-    return fail(GMB_ENOSPC, "state holds %zu bytes, %zu needed", state_bytes, gmb_sampler_state_bytes(csr->num_nodes));
   if (!ws) return fail(GMB_EINVAL, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(ws) % kAlign || reinterpret_cast<uintptr_t>(state) % kAlign)
-    return fail(GMB_EINVAL, "workspace and state must be 256-byte aligned");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(GMB_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < p.total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p.total);
-
   char* base = static_cast<char*>(ws);
-  int32_t* ids = reinterpret_cast<int32_t*>(base + p.off_ids);
-  int32_t* sizes = reinterpret_cast<int32_t*>(base + p.off_sizes);
-  uint64_t* zero = reinterpret_cast<uint64_t*>(base + p.off_zero);
-  uint32_t* status = static_cast<uint32_t*>(state);
-  uint32_t* table = reinterpret_cast<uint32_t*>(static_cast<char*>(state) + kStateHeader);
-  const hipStream_t s = as_stream(stream);
+  return run_sampling(csr, seeds, num_seeds, num_layers, seed, state, p, base, base + p.out_total, out,
+                      as_stream(stream));
+}
 
-  gmb::CsrArgs g{csr->indptr, csr->indices, csr->num_nodes, csr->indptr_bits == 64 ? 1 : 0};
-  int32_t* totals = sizes + 4 * num_layers;
-  gmb::HopArgs hops[GMB_MAX_LAYERS];
-  gmb_blocks res{};
-  res.num_layers = num_layers;
-  res.num_seeds = num_seeds;
-  for (int h = 0; h < num_layers; ++h) {
-    const HopPlan& hp = p.hop[h];
-    gmb::HopArgs& a = hops[h];
-    a.sizes = sizes + 4 * hp.layer;
-    a.indptr = reinterpret_cast<int32_t*>(base + hp.off_indptr);
-    a.nbr = reinterpret_cast<int32_t*>(base + hp.off_nbr);
-    a.local = reinterpret_cast<int32_t*>(base + hp.off_local);
-    a.tiles = zero + hp.tiles_word;
-    a.ticket = reinterpret_cast<uint32_t*>(zero + hp.ticket_word);
-    a.tile_stride = hp.tile_stride;
-    a.cap_dst = hp.cap_dst;
-    a.cap_nnz = hp.cap_nnz;
-    a.cap_src = hp.cap_src;
-    a.fanout = hp.fanout;
-    a.layer = hp.layer;
-    gmb_block& bk = res.blk[hp.layer];
-    bk.indptr = a.indptr;
-    bk.indices = a.local;
-    bk.nbr = a.nbr;
-    bk.src_ids = ids;
-    bk.sizes = a.sizes;
-    bk.cap_dst = hp.cap_dst;
-    bk.cap_src = hp.cap_src;
-    bk.cap_nnz = hp.cap_nnz;
-    bk.fanout = hp.fanout;
-    bk.layer = hp.layer;
-  }
-
-  gmb::SeedArgs sa{};
-  sa.seeds = seeds;
-  sa.num_seeds = num_seeds;
-  sa.first_sizes = 4 * p.hop[0].layer;
-  sa.ids = ids;
-  sa.zero = zero;
-  sa.num_zero = p.num_zero_words;
-  sa.sizes = sizes;
-  sa.num_size_words = p.num_size_words;
-  sa.totals = totals;
-  for (int h = 0; h < num_layers; ++h) {
-    sa.indptr[h] = hops[h].indptr;
-    sa.fanout[h] = hops[h].fanout;
-  }
-  const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
-  hipError_t e = gmb::launch_seed_scan(sa, num_layers, g, s);
-  if (e != hipSuccess) return hip_fail(e, "seed launch");
-  for (int h = 0; h < num_layers; ++h) {
-    // the first hop has nothing deferred: word 3 of a block's sizes is 0
-    gmb::DeferredArgs fix{hops[0].local, hops[0].sizes + 3 - gmb::kNnz, 1};
-    if (h > 0) fix = gmb::DeferredArgs{hops[h - 1].local, hops[h - 1].sizes, std::max<int64_t>(hops[h - 1].cap_nnz, 1)};
-    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, h == 0 ? 1 : 0, fix, s);
-    if (e != hipSuccess) return hip_fail(e, "sample launch");
-    gmb::AssignArgs aa{};
-    aa.nbr = hops[h].nbr;
-    aa.local = hops[h].local;
-    aa.sizes = hops[h].sizes;
-    aa.next_sizes = (h + 1 < num_layers) ? hops[h + 1].sizes : nullptr;
-    aa.tiles = hops[h].tiles;
-    aa.tile_stride = hops[h].tile_stride;
-    aa.ticket = hops[h].ticket;
-    aa.totals = totals;
-    aa.hop = h;
-    for (int v = 1; h + v < num_layers; ++v) {
-      aa.indptr[v] = hops[h + v].indptr;
-      aa.fanout[v] = hops[h + v].fanout;
-    }
-    e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, p.hop[h].items, ids, table, status, s);
-    if (e != hipSuccess) return hip_fail(e, "relabel launch");
-  }
-  const gmb::HopArgs& last = hops[num_layers - 1];
-  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, table, csr->num_nodes,
-                          gmb::DeferredArgs{last.local, last.sizes, std::max<int64_t>(last.cap_nnz, 1)}, s);
-  if (e != hipSuccess) return hip_fail(e, "cleanup launch");
-  *out = res;
-  return ok();
+int gmb_sample_blocks_noalloc(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, const int32_t* fanouts,
+                              int32_t num_layers, uint64_t seed, void* state, size_t state_bytes, void* out_buf,
+                              size_t out_bytes, gmb_blocks* out, void* stream) {
+  SamplePlan p;
+  int st = check_sampling(csr, seeds, num_seeds, fanouts, num_layers, state, state_bytes, &p);
+  if (st != GMB_OK) return st;
+  if (!out_buf) return fail(GMB_EINVAL, "output buffer is NULL");
+  if (reinterpret_cast<uintptr_t>(out_buf) % kAlign) return fail(GMB_EINVAL, "output buffer must be 256-byte aligned");
+  if (out_bytes < p.out_total)
+    return fail(GMB_ENOSPC, "output buffer holds %zu bytes, %zu needed", out_bytes, p.out_total);
+  if (p.scratch_total > kNoAllocScratchBytes)
+    return fail(GMB_ENOSPC, "these shapes need %zu bytes of scratch, above the fixed %zu of the no-allocation entry point",
+                p.scratch_total, kNoAllocScratchBytes);
+  char* scratch_ptr = nullptr;
+  st = noalloc_scratch(&scratch_ptr);
+  if (st != GMB_OK) return st;
+  return run_sampling(csr, seeds, num_seeds, num_layers, seed, state, p, static_cast<char*>(out_buf), scratch_ptr,
+                      out, as_stream(stream));
 }
 
 int gmb_read_sizes(const gmb_blocks* blocks, int64_t* sizes, void* stream) {

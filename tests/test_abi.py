@@ -154,3 +154,27 @@ def test_forward_rejects_bad_arguments_on_host(L):
     b.blk[1].cap_src = 385    # block 1's sources must be block 0's destinations
     assert L.gmb_forward_workspace_bytes(ctypes.byref(b), ctypes.byref(w)) == 0
     assert b"destinations" in L.gmb_last_error()
+
+
+def test_sample_noalloc_rejects_bad_arguments_on_host(L):
+    """The no-allocation entry point checks its output buffer and the
+    sampling arguments before it touches the device (or its scratch)."""
+    import paper_2010_05337_amd as gmb
+    fake = ctypes.c_void_p(1 << 20)
+    csr = gmb.CsrStruct(100, 500, 1 << 20, 32, 0, 1 << 21)
+    out = gmb.BlocksStruct()
+    need = L.gmb_sample_workspace_bytes(10, _fo(5, 3), 2, 100)
+    assert need > 0
+
+    def call(buf, nbytes, fo=_fo(5, 3), L_=2):
+        return L.gmb_sample_blocks_noalloc(ctypes.byref(csr), fake, 10, fo, L_, 1, fake, 1 << 20, buf, nbytes,
+                                           ctypes.byref(out), None)
+
+    assert call(None, need) == -1
+    assert b"output buffer" in L.gmb_last_error()
+    assert call(ctypes.c_void_p((1 << 20) + 64), need) == -1
+    assert b"aligned" in L.gmb_last_error()
+    assert call(fake, 256) == -2
+    assert b"output buffer holds" in L.gmb_last_error()
+    assert call(fake, need, fo=_fo(5, 0)) == -1
+    assert call(fake, need, L_=9) == -1
