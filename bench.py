@@ -388,17 +388,24 @@ def summarize_pmc(args):
     print(json.dumps(out, indent=1))
 
 
-def gather_traffic():
-    """Measured HBM bytes per gather launch, if the stored counter summary
-    was taken on the current gather kernel; otherwise None."""
+def gather_traffic(workload: str):
+    """Measured HBM bytes per gather launch and where they come from: the
+    stored counter summary of the products2m workload, if it was taken on the
+    current gather kernel (digest of its source); otherwise (None, reason)."""
+    if workload != "products2m":
+        return None, f"no counter run stored for the {workload} workload"
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
-        return None
-    if t.get("gather_source_sha256_16") != _source_digest(GATHER_SOURCE):
-        return None
-    return t["traffic_bytes_per_launch"]
+        return None, "no stored counter summary"
+    digest = _source_digest(GATHER_SOURCE)
+    if t.get("gather_source_sha256_16") != digest:
+        return None, "the stored counter summary predates the current gather kernel"
+    return t["traffic_bytes_per_launch"], (
+        f"not measured in this run: {os.path.relpath(TRAFFIC_FILE, ROOT)}, two rocprofv3 --pmc runs "
+        f"(FETCH_SIZE, WRITE_SIZE) of the command recorded there, calibrated by a 1 GiB copy; "
+        f"gather.hip digest {digest} matches")
 
 
 def main():
@@ -673,9 +680,11 @@ def main():
                                     "table, only block 0's destination rows gathered)"}
     # dominant kernel of the path: the feature gather, one launch per step,
     # timed in the isolated pass (the K launches after warm-up and pass A)
+    traffic, traffic_source = gather_traffic(args.workload)
     res["roofline"] = {"kernel": "k_gather", "bound": "hbm",
                        "achieved": b_gather / tg / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                       "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": gather_traffic(),
+                       "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": traffic,
+                       "traffic_source": traffic_source,
                        "alg_bytes_per_launch": b_gather / K, "avg_launch_ms": 1e3 * tg / K,
                        "launches": f"{args.warmup + PASS_A_RUNS * K}..{args.warmup + (PASS_A_RUNS + 1) * K - 1} "
                                    "(pass B)"}
@@ -961,12 +970,41 @@ def cpu_baseline(args, wl, csr, batches, fanouts, feats, weights, ws_sample, x_b
     per_batch = []
     bitexact = True
     max_err = 0.0
+    import oracle
+    ws64, wn64, bs64 = wl.weights.as_f64()
+    stage = {"sample_relabel": [], "gather": [], "forward": []}
+    hubs = getattr(wl.graph, "hubs", None)
+    hub_rows = []
     for b in range(n):
+        # the same steps as _oracle_infer_batch, each timed on its own
         t0 = time.perf_counter()
-        ref, X, logits = _oracle_infer_batch(wl, fanouts, b)
-        per_batch.append(time.perf_counter() - t0)
+        ref = oracle.sample_blocks(wl.graph.indptr, wl.graph.indices, wl.batches[b], fanouts, wl.batch_key(b))
+        t1 = time.perf_counter()
+        X = oracle.gather(wl.feats, ref[0].src)
+        t2 = time.perf_counter()
+        logits, _ = oracle.sage_forward(ref, oracle.widen(X, wl.cfg.feat_dtype), ws64, wn64, bs64)
+        t3 = time.perf_counter()
+        stage["sample_relabel"].append(t1 - t0)
+        stage["gather"].append(t2 - t1)
+        stage["forward"].append(t3 - t2)
+        per_batch.append(t3 - t0)
         t += per_batch[-1]
         seeds_done += len(wl.batches[b])
+        if hubs is not None and len(hubs):
+            # hub occurrences per hop (hop h samples layer L-1-h): hubs among
+            # the hop's destinations, edges sampled from hub rows, edges
+            # that sampled a hub
+            L = len(ref)
+            row = []
+            for h in range(L):
+                r = ref[L - 1 - h]
+                dst = r.src[:r.n_dst]
+                is_hub_dst = np.isin(dst, hubs)
+                from_hub = int(np.diff(r.indptr)[is_hub_dst].sum())
+                row.append({"hop": h, "layer": L - 1 - h, "n_dst": int(r.n_dst), "nnz": int(r.nnz),
+                            "hub_dsts": int(is_hub_dst.sum()), "edges_from_hub_rows": from_hub,
+                            "edges_to_hubs": int(np.isin(r.nbr, hubs).sum())})
+            hub_rows.append(row)
         # the GPU result of the same batch
         blocks = gmb.sample_blocks(csr, batches[b], fanouts, wl.batch_key(b), workspace=ws_sample)
         x = gmb.gather_features(blocks, feats, out=x_buf)
@@ -993,8 +1031,14 @@ def cpu_baseline(args, wl, csr, batches, fanouts, feats, weights, ws_sample, x_b
                       f"thread on {nt} threads, sample+gather+forward in fp64 plain C, {t_all:.1f} s wall",
             "single_thread": {"value": seeds_done / t, "unit": "seeds/s", "cores": 1,
                               "batch_s_median": float(np.median(per_batch)),
+                              "stage_s_median": {k: float(np.median(v)) for k, v in stage.items()},
                               "sample": f"first {n} batches one after another, {t:.1f} s"},
             "host": host_info()}
+    if hub_rows:
+        # per hop, the median over the timed batches
+        base["hub_occurrences_per_hop"] = [
+            {k: (int(np.median([r[h][k] for r in hub_rows])) if k not in ("hop", "layer") else hub_rows[0][h][k])
+             for k in hub_rows[0][h]} for h in range(len(hub_rows[0]))]
     par = {"batches": n, "sample_relabel_gather_bitexact": bitexact, "logits_max_rel_err": max_err}
     return base, par
 

@@ -1,8 +1,9 @@
 """GPU parity on the 111M-node workload (3.2e9 edges, int64 row offsets,
-bf16 x128, fan-outs 15/10/5, batch 1000): the first 32 batches of the epoch
-bit for bit for sampling, relabel and gather, the forward of the first 4
-within 2e-2.  Generating the workload takes a few minutes and about 90 GB of
-host memory, so the test runs only when GMB_BIG=1 is set.
+bf16 x128, fan-outs 15/10/5, batch 1000): the first 16 batches of the epoch
+bit for bit for sampling, relabel and gather, the forward of the first 2
+within 2e-2.  It is the only workload whose row offsets exceed 2^31.
+Generating it takes about a minute and about 90 GB of host memory; the test
+is skipped, with that reason, on a host with less memory available.
 """
 import os
 
@@ -14,14 +15,30 @@ pytestmark = pytest.mark.gpu
 
 if not torch.cuda.is_available():
     pytest.skip("no GPU on this machine", allow_module_level=True)
-if os.environ.get("GMB_BIG") != "1":
-    pytest.skip("the 111M-node workload runs with GMB_BIG=1", allow_module_level=True)
+
+
+def _mem_available_gb() -> float:
+    try:
+        with open("/proc/meminfo") as f:
+            for line in f:
+                if line.startswith("MemAvailable:"):
+                    return int(line.split()[1]) / 2 ** 20
+    except OSError:
+        pass
+    return 0.0
+
+
+NEED_GB = 110
+if _mem_available_gb() < NEED_GB:
+    pytest.skip(f"the 111M-node workload needs about {NEED_GB} GB of host memory "
+                f"({_mem_available_gb():.0f} GB available)", allow_module_level=True)
 
 import paper_2010_05337_amd as gmb  # noqa: E402
 from datagen.configs import make_workload  # noqa: E402
 from gpu_util import assert_blocks_equal, rowwise_rel_err, tensor_bits, tensor_f64, to_torch_weights  # noqa: E402
 
 
+@pytest.mark.timeout(900)
 def test_papers111m_first_batches(orc):
     from concurrent.futures import ThreadPoolExecutor
     wl = make_workload("papers111m")
@@ -37,8 +54,8 @@ def test_papers111m_first_batches(orc):
     feats = torch.from_numpy(wl.feats.view(np.int16)).cuda().view(torch.bfloat16)
     weights = to_torch_weights(wl.weights)
     ws, wn, bs = wl.weights.as_f64()
-    nb = min(32, len(wl.batches))
-    n_fwd = 4
+    nb = min(16, len(wl.batches))
+    n_fwd = 2
     orc.lib()
 
     def oracle_batch(b):

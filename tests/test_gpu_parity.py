@@ -122,7 +122,8 @@ def _table_is_clear(csr):
 
 
 @pytest.mark.parametrize("n, num_seeds, fanouts, whole", [
-    (10000, 64, [5, 5], True), (10000, 8, [2], False), (10003, 64, [5, 5], True), (10003, 8, [2], False)])
+    (10000, 64, [5, 5], True), (10000, 8, [2], False), (10003, 64, [5, 5], True), (10003, 8, [2], False),
+    (200_000, 8, [3, 3], False)])
 def test_state_is_clean_after_each_call(orc, dg, n, num_seeds, fanouts, whole):
     """The cleanup clears the dedup table in one of two ways: all of it
     with 16-byte stores when it holds at most eight slots per possible
