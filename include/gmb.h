@@ -150,7 +150,9 @@ uint32_t* gmb_state_status_word(void* state);
 
 /* Synchronises `stream`, reads and clears the status word and returns the
  * matching status (GMB_ERANGE before GMB_EDUP before GMB_EDEVICE for
- * GMB_STATUS_INTERNAL), or GMB_OK. */
+ * GMB_STATUS_INTERNAL), or GMB_OK.  After GMB_STATUS_INTERNAL it also
+ * clears the state's table again (and synchronises once more), since the
+ * failed call may have left slots behind. */
 int gmb_read_status(void* state, void* stream);
 
 /* ---- sampling (Section II-B, steps (i)-(ii), recursive per layer) ------- */
@@ -194,7 +196,8 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
  * that forbid hipMalloc.  The same sampling as gmb_sample_blocks (same
  * kernels, the same blocks bit for bit), with the scratch that the call
  * needs besides its outputs (the relabel scans' look-back words and tickets,
- * the running edge counts) in a fixed array of GMB_NOALLOC_SCRATCH_BYTES
+ * the running edge counts, the dedup's routed pairs and answers) in a fixed
+ * array of GMB_NOALLOC_SCRATCH_BYTES
  * that the library holds in device memory, one copy per GPU, from the first
  * call on that GPU until the process ends.  The call allocates nothing.
  *   out_buf    device buffer for the blocks, 256-byte aligned, caller-owned;
@@ -203,8 +206,9 @@ int gmb_sample_blocks(const gmb_csr* csr, const int32_t* seeds, int32_t num_seed
  *              point into it and stay valid until it is reused.
  *   others     as for gmb_sample_blocks.
  * Errors: those of gmb_sample_blocks, and GMB_ENOSPC when the shapes need
- * more scratch than the fixed array holds (about 8 bytes per 1000 edges of
- * a hop's capacity); nothing is enqueued then.  The scratch is cleared by
+ * more scratch than the fixed array holds (about 12 bytes per edge and per
+ * destination of the last hop's capacity: 13 MB for 1000 seeds and fan-outs
+ * 15, 10, 5); nothing is enqueued then.  The scratch is cleared by
  * the call's own first kernel.  Every call on one GPU shares that GPU's
  * array: calls that overlap in time on one GPU (other streams, other host
  * threads) race and give wrong blocks, so order them on one stream. */

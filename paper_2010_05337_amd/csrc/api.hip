@@ -39,6 +39,8 @@ int hip_fail(hipError_t e, const char* what) {
 constexpr size_t kAlign = 256;
 constexpr int64_t kMaxInt32 = 0x7FFFFFFF;
 constexpr size_t kStateHeader = 256;
+// largest fan-out: one destination's edges must fit one relabel tile
+constexpr int kMaxFanout = gmb::kScanBlock * 16;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -53,6 +55,8 @@ struct HopPlan {
   size_t off_indptr, off_nbr, off_local;
   int64_t tiles_word, ticket_word, tile_stride;
   int items;
+  bool table;                      // dedup through the state's per-vertex table (small hops)
+  int32_t span, routers, owners;   // else by owners: destinations per router, routers, owners
 };
 
 struct SamplePlan {
@@ -64,8 +68,9 @@ struct SamplePlan {
   size_t out_total;
   // scratch, relative to the scratch buffer: the look-back words and
   // tickets of the relabel scans (cleared by the seed kernel), the running
-  // edge count of every hop
-  size_t off_zero, off_totals;
+  // edge count of every hop, and the dedup's pairs, answers, owner offsets
+  // and router regions (one set, reused by every hop)
+  size_t off_zero, off_totals, off_pairs, off_res, off_owner, off_rs;
   int64_t num_zero_words;
   size_t scratch_total;
   // one workspace holding both: the outputs, then the scratch
@@ -86,7 +91,8 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
   if (num_seeds > num_nodes)
     return fail(GMB_EINVAL, "num_seeds=%d exceeds num_nodes (seeds must be distinct)", num_seeds);
   for (int l = 0; l < num_layers; ++l)
-    if (fanouts[l] < 1) return fail(GMB_EINVAL, "fanouts[%d]=%d < 1", l, fanouts[l]);
+    if (fanouts[l] < 1 || fanouts[l] > kMaxFanout)
+      return fail(GMB_EINVAL, "fanouts[%d]=%d outside 1..%d", l, fanouts[l], kMaxFanout);
 
   SamplePlan p{};
   p.num_layers = num_layers;
@@ -100,12 +106,30 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
     hp.cap_nnz = cap_dst * static_cast<int64_t>(hp.fanout);
     hp.cap_src = cap_dst + std::min<int64_t>(hp.cap_nnz, num_nodes);
     // every position (edge, source) and every edge tag must fit in 31 bits
-    if (hp.cap_nnz >= kMaxInt32 || hp.cap_src >= kMaxInt32)
+    if (hp.cap_nnz >= kMaxInt32 || hp.cap_src >= kMaxInt32 || hp.cap_nnz + hp.cap_dst >= kMaxInt32)
       return fail(GMB_EINVAL, "hop %d: capacity %lld edges / %lld sources exceeds 2^31-1", h,
                   static_cast<long long>(hp.cap_nnz), static_cast<long long>(hp.cap_src));
-    // the relabel scan of hop h carries 1 + (later hops) values
+    // The hops before the last dedup through the per-vertex table while
+    // their fan-outs allow the group sampler (few edges, few table lines);
+    // the last hop, and every hop after one that cannot, by owners.  The
+    // relabel scan of hop h carries 1 + (later hops) values.
     hp.items = gmb::scan_items_for(hp.cap_nnz);
-    hp.tile_stride = gmb::scan_tiles(hp.cap_nnz, hp.items);
+    hp.table = h + 1 < num_layers && hp.fanout <= 64 && (h == 0 || p.hop[h - 1].table);
+    if (hp.table) {
+      hp.tile_stride = gmb::scan_tiles(hp.cap_nnz, hp.items);
+    } else {
+      // a relabel tile is one router: `span` destinations whose edges fit it
+      while (gmb::kScanBlock * hp.items < hp.fanout) hp.items *= 2;
+      hp.span = std::min(gmb::kMaxSpan, std::max(1, gmb::kScanBlock * hp.items / hp.fanout));
+      const int64_t routers = std::max<int64_t>(1, (hp.cap_dst + hp.span - 1) / hp.span);
+      if (routers > gmb::kMaxRouters)
+        return fail(GMB_EINVAL, "hop %d: %lld destinations need %lld routers, above %d", h,
+                    static_cast<long long>(hp.cap_dst), static_cast<long long>(routers), gmb::kMaxRouters);
+      hp.routers = static_cast<int32_t>(routers);
+      hp.owners = static_cast<int32_t>(std::min<int64_t>(
+          gmb::kMaxOwners, std::max<int64_t>(1, (hp.cap_nnz + hp.cap_dst + gmb::kOwnerPairs - 1) / gmb::kOwnerPairs)));
+      hp.tile_stride = hp.routers;
+    }
     hp.tiles_word = zero_words;
     zero_words += hp.tile_stride * (num_layers - h);
     hp.ticket_word = zero_words++;
@@ -133,6 +157,22 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
   off = align_up(off + sizeof(uint64_t) * zero_words);
   p.off_totals = off;
   off = align_up(off + sizeof(int32_t) * kTotalsWords);
+  int64_t pairs = 1, owner_words = 1, routers = 1;
+  for (int h = 0; h < num_layers; ++h) {
+    const HopPlan& hp = p.hop[h];
+    if (hp.table) continue;
+    pairs = std::max(pairs, hp.cap_nnz + hp.cap_dst);
+    owner_words = std::max(owner_words, static_cast<int64_t>(hp.owners + 1) * hp.routers);
+    routers = std::max<int64_t>(routers, hp.routers);
+  }
+  p.off_pairs = off;
+  off = align_up(off + 8 * static_cast<size_t>(pairs));
+  p.off_res = off;
+  off = align_up(off + 4 * static_cast<size_t>(pairs));
+  p.off_owner = off;
+  off = align_up(off + 4 * static_cast<size_t>(owner_words));
+  p.off_rs = off;
+  off = align_up(off + 4 * static_cast<size_t>(routers));
   p.scratch_total = off;
   p.total = p.out_total + p.scratch_total;
   *plan = p;
@@ -221,33 +261,82 @@ int run_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, in
   const uint32_t k0 = static_cast<uint32_t>(seed), k1 = static_cast<uint32_t>(seed >> 32);
   hipError_t e = gmb::launch_seed_scan(sa, num_layers, g, s);
   if (e != hipSuccess) return hip_fail(e, "seed launch");
+  uint2* pairs = reinterpret_cast<uint2*>(scr + p.off_pairs);
+  int32_t* answers = reinterpret_cast<int32_t*>(scr + p.off_res);
+  int32_t* owner_off = reinterpret_cast<int32_t*>(scr + p.off_owner);
+  int32_t* region = reinterpret_cast<int32_t*>(scr + p.off_rs);
   for (int h = 0; h < num_layers; ++h) {
+    const HopPlan& hp = p.hop[h];
     // the first hop has nothing deferred: word 3 of a block's sizes is 0
     gmb::DeferredArgs fix{hops[0].local, hops[0].sizes + 3 - gmb::kNnz, 1};
     if (h > 0) fix = gmb::DeferredArgs{hops[h - 1].local, hops[h - 1].sizes, std::max<int64_t>(hops[h - 1].cap_nnz, 1)};
-    e = gmb::launch_sample(g, ids, hops[h], table, status, k0, k1, h == 0 ? 1 : 0, fix, s);
-    if (e != hipSuccess) return hip_fail(e, "sample launch");
-    gmb::AssignArgs aa{};
-    aa.nbr = hops[h].nbr;
-    aa.local = hops[h].local;
-    aa.sizes = hops[h].sizes;
-    aa.next_sizes = (h + 1 < num_layers) ? hops[h + 1].sizes : nullptr;
-    aa.tiles = hops[h].tiles;
-    aa.tile_stride = hops[h].tile_stride;
-    aa.ticket = hops[h].ticket;
-    aa.totals = totals;
-    aa.hop = h;
-    for (int v = 1; h + v < num_layers; ++v) {
-      aa.indptr[v] = hops[h + v].indptr;
-      aa.fanout[v] = hops[h + v].fanout;
+    if (hp.table) {
+      e = gmb::launch_sample_table(g, ids, hops[h], table, status, k0, k1, h == 0 ? 1 : 0, fix, s);
+      if (e != hipSuccess) return hip_fail(e, "sample launch");
+      gmb::AssignArgs aa{};
+      aa.nbr = hops[h].nbr;
+      aa.local = hops[h].local;
+      aa.sizes = hops[h].sizes;
+      aa.next_sizes = (h + 1 < num_layers) ? hops[h + 1].sizes : nullptr;
+      aa.tiles = hops[h].tiles;
+      aa.tile_stride = hops[h].tile_stride;
+      aa.ticket = hops[h].ticket;
+      aa.totals = totals;
+      aa.hop = h;
+      for (int v = 1; h + v < num_layers; ++v) {
+        aa.indptr[v] = hops[h + v].indptr;
+        aa.fanout[v] = hops[h + v].fanout;
+      }
+      e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, hp.items, ids, table, status, s);
+      if (e != hipSuccess) return hip_fail(e, "relabel launch");
+      continue;
     }
-    e = gmb::launch_assign(aa, num_layers - h, g, hops[h].cap_nnz, p.hop[h].items, ids, table, status, s);
+    gmb::RouteArgs ra{hops[h].sizes, hops[h].indptr, ids, hops[h].nbr, pairs, owner_off, region,
+                      csr->num_nodes, hp.span, hp.routers, hp.owners};
+    if (hp.fanout <= 64) {
+      gmb::SampleArgs sa{ids, hops[h].sizes, hops[h].indptr, hops[h].nbr, status, hp.fanout, hp.layer, k0, k1,
+                         h == 0 ? 1 : 0, fix};
+      e = gmb::launch_sample_route(g, sa, ra, s);
+      if (e != hipSuccess) return hip_fail(e, "sample launch");
+    } else {
+      e = gmb::launch_sample(g, ids, hops[h], status, k0, k1, h == 0 ? 1 : 0, fix, s);
+      if (e != hipSuccess) return hip_fail(e, "sample launch");
+      e = gmb::launch_route(ra, s);
+      if (e != hipSuccess) return hip_fail(e, "route launch");
+    }
+    gmb::OwnerArgs oa{pairs, owner_off, region, answers, table, status, hp.routers, hp.owners};
+    e = gmb::launch_owner(oa, s);
+    if (e != hipSuccess) return hip_fail(e, "owner launch");
+    gmb::RankArgs rk{};
+    rk.pairs = pairs;
+    rk.res = answers;
+    rk.indptr0 = hops[h].indptr;
+    rk.local = hops[h].local;
+    rk.sizes = hops[h].sizes;
+    rk.next_sizes = (h + 1 < num_layers) ? hops[h + 1].sizes : nullptr;
+    rk.tiles = hops[h].tiles;
+    rk.tile_stride = hops[h].tile_stride;
+    rk.ticket = hops[h].ticket;
+    rk.totals = totals;
+    rk.hop = h;
+    rk.span = hp.span;
+    for (int v = 1; h + v < num_layers; ++v) {
+      rk.indptr[v] = hops[h + v].indptr;
+      rk.fanout[v] = hops[h + v].fanout;
+    }
+    e = gmb::launch_rank(rk, num_layers - h, g, hp.routers, hp.items, ids, status, s);
     if (e != hipSuccess) return hip_fail(e, "relabel launch");
   }
+  // the last hop's deferred ids; the slots the table hops recorded (their
+  // sources: the seeds and the vertices they added) back to empty
+  int table_hops = 0;
+  while (table_hops < num_layers && p.hop[table_hops].table) ++table_hops;
   const gmb::HopArgs& last = hops[num_layers - 1];
-  e = gmb::launch_cleanup(ids, last.sizes, p.cap_ids, table, csr->num_nodes,
-                          gmb::DeferredArgs{last.local, last.sizes, std::max<int64_t>(last.cap_nnz, 1)}, s);
-  if (e != hipSuccess) return hip_fail(e, "cleanup launch");
+  const int32_t* clear = table_hops ? hops[table_hops - 1].sizes : nullptr;
+  const int64_t clear_cap = table_hops ? hops[table_hops - 1].cap_src : 0;
+  e = gmb::launch_fix(gmb::DeferredArgs{last.local, last.sizes, std::max<int64_t>(last.cap_nnz, 1)}, ids, clear,
+                      clear_cap, table, csr->num_nodes, s);
+  if (e != hipSuccess) return hip_fail(e, "deferred-id launch");
   *out = res;
   return ok();
 }
@@ -408,19 +497,34 @@ int gmb_sampler_state_init(void* state, size_t state_bytes, int64_t num_nodes, v
 
 int gmb_read_status(void* state, void* stream) {
   if (!state) return fail(GMB_EINVAL, "state is NULL");
-  uint32_t word = 0;
+  // the status word and (at byte 8) the vertex count written by the init
+  uint32_t head[4] = {0, 0, 0, 0};
   hipError_t e = hipStreamSynchronize(as_stream(stream));
   if (e != hipSuccess) return hip_fail(e, "stream synchronize");
-  e = hipMemcpy(&word, state, sizeof word, hipMemcpyDeviceToHost);
+  e = hipMemcpy(head, state, sizeof head, hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "status read");
+  const uint32_t word = head[0];
   if (word != 0) {
     e = hipMemset(state, 0, sizeof word);
     if (e != hipSuccess) return hip_fail(e, "status clear");
   }
+  if (word & GMB_STATUS_INTERNAL) {
+    // the relabel numbered some vertices wrongly, so the call's cleanup may
+    // have missed table slots: clear the whole table again
+    int64_t n = 0;
+    std::memcpy(&n, head + 2, sizeof n);
+    if (n >= 1 && n <= kMaxInt32) {
+      uint32_t* table = reinterpret_cast<uint32_t*>(static_cast<char*>(state) + kStateHeader);
+      e = gmb::launch_state_init(table, static_cast<uint32_t*>(state), n, as_stream(stream));
+      if (e == hipSuccess) e = hipStreamSynchronize(as_stream(stream));
+      if (e != hipSuccess) return hip_fail(e, "state re-init");
+    }
+  }
   if (word & GMB_STATUS_ERANGE) return fail(GMB_ERANGE, "a vertex id outside [0, num_nodes) was found on the device");
   if (word & GMB_STATUS_EDUP) return fail(GMB_EDUP, "the seed list holds a vertex more than once");
   if (word & GMB_STATUS_INTERNAL)
-    return fail(GMB_EDEVICE, "a bounded wait in the relabel scan ran out (the blocks of that call are wrong)");
+    return fail(GMB_EDEVICE, "a bounded wait in the relabel scan ran out: the blocks of that call are wrong "
+                             "(the sampler state has been cleared again)");
   return ok();
 }
 

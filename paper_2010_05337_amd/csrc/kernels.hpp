@@ -27,7 +27,7 @@ struct HopArgs {
   int32_t* local;        // [cap_nnz]
   uint64_t* tiles;       // look-back words of this hop's relabel scan
   uint32_t* ticket;
-  int64_t tile_stride;   // words per scanned value
+  int64_t tile_stride;   // words per scanned value (= routers)
   int items;             // relabel scan items per thread
   int64_t cap_dst, cap_nnz, cap_src;
   int fanout;
@@ -35,9 +35,9 @@ struct HopArgs {
 };
 
 constexpr int kScanBlock = 256;
-// Items per thread of a relabel scan tile (kScanBlock threads): 2, 4, 8 or
-// 16.  Small hops take small tiles so that their random reads spread over
-// many CUs; large hops take large tiles, which cuts tickets and look-back.
+// Items per thread of a relabel tile (kScanBlock threads): 2, 4, 8 or 16.
+// Small hops take small tiles so that their random reads spread over many
+// CUs; large hops take large tiles, which cuts tickets and look-back.
 inline int64_t scan_tiles(int64_t n, int items) {
   const int64_t tile = static_cast<int64_t>(kScanBlock) * items;
   return n <= 0 ? 1 : (n + tile - 1) / tile;
@@ -47,6 +47,102 @@ inline int scan_items_for(int64_t cap_nnz) {
     if (scan_tiles(cap_nnz, items) >= 128) return items;
   return 2;
 }
+
+// Local ids that a hop's relabel left deferred (entries -(e0 + 1): copy the
+// local id of edge e0); the next kernel on the stream resolves them.  The
+// edge count is sizes[kNnz]; cap (>= 1) bounds it and every read of local.
+// Nothing to resolve: any local array of cap entries and an edge count of 0.
+struct DeferredArgs {
+  int32_t* local;
+  const int32_t* sizes;
+  int64_t cap;
+};
+
+// Relabel arguments of a table hop `hop` (k_assign).  Value v >= 1 of its
+// scan belongs to hop hop + v: indptr[v], fanout[v].
+struct AssignArgs {
+  const int32_t* nbr;
+  int32_t* local;
+  int32_t* sizes;
+  int32_t* next_sizes;   // nullptr after the last hop
+  uint64_t* tiles;
+  int64_t tile_stride;
+  uint32_t* ticket;
+  int32_t* totals;
+  int hop;
+  int32_t* indptr[GMB_MAX_LAYERS];
+  int32_t fanout[GMB_MAX_LAYERS];
+};
+
+// Dedup by owners (sample.hip): a router takes `span` destinations, whose
+// edges fit one relabel tile (span * fanout <= kScanBlock * items), and
+// routes them with the destinations themselves (at most kMaxRouteEntries
+// pairs); an owner's LDS hash table has kOwnerSlots slots.
+constexpr int kMaxRouters = 2048;
+constexpr int kMaxOwners = 4096;
+constexpr int kMaxRouteEntries = 8192;
+constexpr int kMaxSpan = 1024;
+constexpr int kOwnerSlots = 8192;
+// pairs per owner the plan aims at, at full capacity (half the table)
+constexpr int64_t kOwnerPairs = 4096;
+
+// Sampling arguments of one hop (fan-out f, model layer `layer`); the
+// first hop also checks the seeds (check_seeds).  fix: the previous hop's
+// deferred local ids, resolved by the same grid.
+struct SampleArgs {
+  const int32_t* ids;
+  const int32_t* sizes;
+  const int32_t* indptr;   // the hop's block row offsets
+  int32_t* nbr;
+  uint32_t* status;
+  int fanout, layer;
+  uint32_t k0, k1;
+  int check_seeds;
+  DeferredArgs fix;
+};
+
+// Router arguments of one hop (k_route).
+struct RouteArgs {
+  const int32_t* sizes;    // the hop's size words (n_dst)
+  const int32_t* indptr;   // the hop's block row offsets [n_dst + 1]
+  const int32_t* ids;      // the destinations: ids[0 .. n_dst)
+  const int32_t* nbr;      // the hop's sampled vertices [nnz]
+  uint2* pairs;            // [cap_dst + cap_nnz] (key, value)
+  int32_t* off;            // [(owners + 1) * routers], owner-major
+  int32_t* rs;             // [routers] region start of each router
+  int64_t num_nodes;
+  int32_t span, routers, owners;
+};
+
+// Owner arguments of one hop (k_owner).
+struct OwnerArgs {
+  const uint2* pairs;
+  const int32_t* off;
+  const int32_t* rs;
+  int32_t* res;            // [cap_dst + cap_nnz] answers, at the pairs' positions
+  uint32_t* table;         // the state's per-vertex table (overflow only)
+  uint32_t* status;
+  int32_t routers, owners;
+};
+
+// Relabel arguments of hop `hop` (k_rank).  Value v >= 1 of its scan
+// belongs to hop hop + v: indptr[v], fanout[v].
+struct RankArgs {
+  const uint2* pairs;
+  const int32_t* res;
+  const int32_t* indptr0;  // this hop's block row offsets (router ranges)
+  int32_t* local;
+  int32_t* sizes;
+  int32_t* next_sizes;     // nullptr after the last hop
+  uint64_t* tiles;
+  int64_t tile_stride;
+  uint32_t* ticket;
+  int32_t* totals;
+  int hop;
+  int32_t span;
+  int32_t* indptr[GMB_MAX_LAYERS];
+  int32_t fanout[GMB_MAX_LAYERS];
+};
 
 // Arguments of the seed kernel (segment 0: the seeds).  Per hop v:
 // indptr[v] its block row offsets, fanout[v] its fan-out.  totals[v] is
@@ -66,42 +162,31 @@ struct SeedArgs {
   int32_t fanout[GMB_MAX_LAYERS];
 };
 
-// Arguments of hop `hop`'s relabel.  Value v >= 1 of its scan belongs to
-// hop hop + v: indptr[v], fanout[v].
-struct AssignArgs {
-  const int32_t* nbr;
-  int32_t* local;
-  int32_t* sizes;
-  int32_t* next_sizes;   // nullptr after the last hop
-  uint64_t* tiles;
-  int64_t tile_stride;
-  uint32_t* ticket;
-  int32_t* totals;
-  int hop;
-  int32_t* indptr[GMB_MAX_LAYERS];
-  int32_t fanout[GMB_MAX_LAYERS];
-};
-
-// Local ids that a hop's relabel left deferred (entries -(e0 + 1): copy the
-// local id of edge e0); the next kernel on the stream resolves them.  The
-// edge count is sizes[kNnz]; cap (>= 1) bounds it and every read of local.
-// Nothing to resolve: any local array of cap entries and an edge count of 0.
-struct DeferredArgs {
-  int32_t* local;
-  const int32_t* sizes;
-  int64_t cap;
-};
-
 // sample.hip
 hipError_t launch_state_init(uint32_t* table, uint32_t* status, int64_t num_nodes, hipStream_t s);
 hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, hipStream_t s);
-hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* table,
-                         uint32_t* status, uint32_t k0, uint32_t k1, int first_hop,
-                         const DeferredArgs& fix, hipStream_t s);
-hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz,
-                         int items, int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s);
-hipError_t launch_cleanup(const int32_t* ids, const int32_t* final_sizes, int64_t cap_src, uint32_t* table,
-                          int64_t num_nodes, const DeferredArgs& fix, hipStream_t s);
+// Table hops (fan-outs up to 64): sampling with the first-edge atomics on
+// the state's table, then the relabel scan.
+hipError_t launch_sample_table(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* table,
+                               uint32_t* status, uint32_t k0, uint32_t k1, int first_hop, const DeferredArgs& fix,
+                               hipStream_t s);
+hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, int64_t cap_nnz, int items,
+                         int32_t* ids, uint32_t* table, uint32_t* status, hipStream_t s);
+// Owner hops with fan-outs above 64: sampling alone (then launch_route).
+hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* status, uint32_t k0,
+                         uint32_t k1, int first_hop, const DeferredArgs& fix, hipStream_t s);
+hipError_t launch_route(const RouteArgs& a, hipStream_t s);
+// Sampling and routing in one launch (fan-outs up to 64); otherwise
+// launch_sample then launch_route.
+hipError_t launch_sample_route(const CsrArgs& g, const SampleArgs& sa, const RouteArgs& ra, hipStream_t s);
+hipError_t launch_owner(const OwnerArgs& a, hipStream_t s);
+hipError_t launch_rank(const RankArgs& a, int num_values, const CsrArgs& g, int routers, int items, int32_t* ids,
+                       uint32_t* status, hipStream_t s);
+// The last hop's deferred local ids; with clear_sizes, also the table
+// slots of ids[0 .. clear_sizes[kNSrc]) (the vertices the table hops
+// recorded) back to empty.
+hipError_t launch_fix(const DeferredArgs& fix, const int32_t* ids, const int32_t* clear_sizes, int64_t clear_cap,
+                      uint32_t* table, int64_t num_nodes, hipStream_t s);
 
 // gather.hip
 hipError_t launch_gather(const int32_t* ids, const int32_t* n_dev, int64_t n_cap, const void* feats,

@@ -21,8 +21,12 @@ __device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint3
                                                  uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint32_t a0 = 0xD2511F53u * c0, h0 = __umulhi(0xD2511F53u, c0);
-    const uint32_t a2 = 0xCD9E8D57u * c2, h2 = __umulhi(0xCD9E8D57u, c2);
+    // one 32x32->64-bit product per lane pair (a single v_mad_u64_u32
+    // instead of a low and a high multiply)
+    const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * c0;
+    const uint64_t p2 = static_cast<uint64_t>(0xCD9E8D57u) * c2;
+    const uint32_t a0 = static_cast<uint32_t>(p0), h0 = static_cast<uint32_t>(p0 >> 32);
+    const uint32_t a2 = static_cast<uint32_t>(p2), h2 = static_cast<uint32_t>(p2 >> 32);
     const uint32_t n0 = h2 ^ c1 ^ k0;
     const uint32_t n2 = h0 ^ c3 ^ k1;
     c0 = n0;
