@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -200,6 +201,19 @@ int check_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, 
   return GMB_OK;
 }
 
+// The owners' LDS table size limit: kOwnerSlots, or a smaller power of two
+// from the environment variable GMB_OWNER_TABLE_SLOTS (64 .. kOwnerSlots), a
+// test hook that makes owners overflow into the state table so that path
+// runs on small inputs.
+int32_t owner_slots() {
+  const char* v = std::getenv("GMB_OWNER_TABLE_SLOTS");
+  if (!v) return gmb::kOwnerSlots;
+  const long x = std::strtol(v, nullptr, 10);
+  int32_t slots = 64;
+  while (slots < x && slots < gmb::kOwnerSlots) slots *= 2;
+  return slots;
+}
+
 // Enqueues the sampling kernels: the blocks go to `outb` (plan offsets
 // off_ids, off_sizes and the hops'), the scratch words to `scr`.
 int run_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, int32_t num_layers, uint64_t seed,
@@ -304,7 +318,7 @@ int run_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, in
       e = gmb::launch_route(ra, s);
       if (e != hipSuccess) return hip_fail(e, "route launch");
     }
-    gmb::OwnerArgs oa{pairs, owner_off, region, answers, table, status, hp.routers, hp.owners};
+    gmb::OwnerArgs oa{pairs, owner_off, region, answers, table, status, hp.routers, hp.owners, owner_slots()};
     e = gmb::launch_owner(oa, s);
     if (e != hipSuccess) return hip_fail(e, "owner launch");
     gmb::RankArgs rk{};

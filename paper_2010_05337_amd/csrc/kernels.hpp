@@ -123,6 +123,7 @@ struct OwnerArgs {
   uint32_t* table;         // the state's per-vertex table (overflow only)
   uint32_t* status;
   int32_t routers, owners;
+  int32_t max_slots;       // LDS table size limit, a power of two in 64 .. kOwnerSlots
 };
 
 // Relabel arguments of hop `hop` (k_rank).  Value v >= 1 of its scan

@@ -837,7 +837,7 @@ __global__ __launch_bounds__(kOwnerBlock) void k_owner(OwnerArgs a) {
   if (threadIdx.x == 0) s_seg[W] = M;
   // table size: a power of two >= 2 M (load <= 1/2), 64 .. kOwnerSlots
   int logc = 6;
-  while ((1 << logc) < 2 * static_cast<int64_t>(M) && (1 << logc) < kOwnerSlots) ++logc;
+  while ((1 << logc) < 2 * static_cast<int64_t>(M) && (1 << logc) < a.max_slots) ++logc;
   const int C = 1 << logc, shift = 32 - logc;
   for (int i = threadIdx.x; i < C; i += kOwnerBlock) {
     s_key[i] = kEmptyKey;
@@ -1256,7 +1256,8 @@ hipError_t launch_sample_route(const CsrArgs& g, const SampleArgs& sa, const Rou
 }
 
 hipError_t launch_owner(const OwnerArgs& a, hipStream_t s) {
-  if (a.routers < 1 || a.routers > kMaxRouters || a.owners < 1 || a.owners > kMaxOwners)
+  if (a.routers < 1 || a.routers > kMaxRouters || a.owners < 1 || a.owners > kMaxOwners || a.max_slots < 64 ||
+      a.max_slots > kOwnerSlots || (a.max_slots & (a.max_slots - 1)))
     return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_owner, dim3(static_cast<unsigned>(a.owners)), dim3(kOwnerBlock), 0, s, a);
   return hipGetLastError();

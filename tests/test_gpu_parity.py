@@ -340,3 +340,27 @@ def test_forward_fused_hubs(orc, dg):
     seeds = np.concatenate([np.asarray(g.hubs, np.int32),
                             dg.permutation(20000, 65)[:300][~np.isin(dg.permutation(20000, 65)[:300], g.hubs)]])
     _fused_case(orc, dg, g, feats, w, seeds.astype(np.int32), [25, 10], 66, TOL_BF16)
+
+
+@pytest.mark.parametrize("fanouts, num_seeds", [([12, 8, 5], 3000), ([70], 300), ([6, 30], 800)])
+def test_owner_overflow_path(orc, dg, fanouts, num_seeds, monkeypatch):
+    """An owner whose vertices do not fit its LDS table redoes its pairs
+    through the state's per-vertex table: forced here with a 64-slot limit
+    (the test hook GMB_OWNER_TABLE_SLOTS), every block must still equal the
+    oracle's, repeated seeds must still be reported, and the table must be
+    clear afterwards."""
+    monkeypatch.setenv("GMB_OWNER_TABLE_SLOTS", "64")
+    g = dg.rmat(15, 30_000, 250_000, (0.57, 0.19, 0.19), 9)
+    csr = csr_on_device(g)
+    seeds = dg.permutation(g.num_nodes, 4)[:num_seeds]
+    for key in (3, 4):
+        print(f"overflow path: fanouts {fanouts}, {num_seeds} seeds, key {key}", flush=True)
+        _, host = gpu_blocks(csr, seeds, fanouts, key)
+        assert_blocks_equal(host, orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, key), f"key {key}")
+        assert _table_is_clear(csr)
+    csr.check_status()
+    gpu_blocks(csr, np.concatenate([seeds[:50], seeds[:1]]), fanouts, 5)
+    with pytest.raises(gmb.GmbError) as e:
+        csr.check_status()
+    assert e.value.code == -5
+    assert _table_is_clear(csr)
