@@ -58,6 +58,7 @@ typedef enum { GMB_F32 = 0, GMB_BF16 = 1 } gmb_dtype;
 #define GMB_STATUS_ERANGE 1u
 #define GMB_STATUS_EDUP 2u
 #define GMB_STATUS_INTERNAL 4u   /* a bounded wait inside the relabel scan ran out */
+#define GMB_STATUS_INVALID 8u    /* gmb_validate_blocks found an inconsistent block */
 
 /* In-neighbour CSR of the input graph G(V, E) (Section II-A): row v lists
  * the sources u of the edges u -> v, so sampling row v samples the vertices
@@ -150,7 +151,7 @@ uint32_t* gmb_state_status_word(void* state);
 
 /* Synchronises `stream`, reads and clears the status word and returns the
  * matching status (GMB_ERANGE before GMB_EDUP before GMB_EDEVICE for
- * GMB_STATUS_INTERNAL), or GMB_OK.  After GMB_STATUS_INTERNAL it also
+ * GMB_STATUS_INTERNAL or GMB_STATUS_INVALID), or GMB_OK.  After GMB_STATUS_INTERNAL it also
  * clears the state's table again (and synchronises once more), since the
  * failed call may have left slots behind. */
 int gmb_read_status(void* state, void* stream);
@@ -216,6 +217,18 @@ int gmb_sample_blocks_noalloc(const gmb_csr* csr, const int32_t* seeds, int32_t 
                               const int32_t* fanouts, int32_t num_layers, uint64_t seed,
                               void* state, size_t state_bytes, void* out_buf, size_t out_bytes,
                               gmb_blocks* out, void* stream);
+
+/* Debug check of sampled blocks (run after every gmb_sample_blocks and
+ * gmb_sample_blocks_noalloc call when the environment variable GMB_VALIDATE
+ * is set to 1): enqueues on `stream` a device check of each block's
+ * invariants (sizes within the capacities; row offsets rising from 0 to nnz
+ * with at most `fanout` edges per row; every edge's local id below n_src and
+ * naming the edge's sampled vertex in src_ids; every sampled vertex inside
+ * the graph).  A violation sets GMB_STATUS_INVALID in the state's status
+ * word, which gmb_read_status reports as GMB_EDEVICE.  The check reads only
+ * within the blocks' capacities, whatever their size words hold.  It does
+ * not check that src_ids is duplicate-free (the oracle tests do). */
+int gmb_validate_blocks(const gmb_csr* csr, const gmb_blocks* blocks, void* state, void* stream);
 
 /* Synchronises `stream` and copies the device sizes to host
  * sizes[num_layers][3] = {n_dst, n_src, nnz} (layer order). */

@@ -34,6 +34,7 @@ EXPORTS = (
     "gmb_forward_hidden_offset", "gmb_sage_forward", "gmb_sage_forward_fused", "gmb_backward_workspace_bytes",
     "gmb_sage_backward", "gmb_sgd_update", "gmb_backward_embedding_workspace_bytes",
     "gmb_sage_backward_embedding", "gmb_sample_blocks_noalloc",
+    "gmb_validate_blocks",
 )
 
 
@@ -107,6 +108,8 @@ def lib() -> ctypes.CDLL:
         L.gmb_sample_blocks_noalloc.restype = ctypes.c_int
         L.gmb_sample_blocks_noalloc.argtypes = [ctypes.POINTER(CsrStruct), vp, i32, vp, i32, u64, vp, sz, vp,
                                                 sz, ctypes.POINTER(BlocksStruct), vp]
+        L.gmb_validate_blocks.restype = ctypes.c_int
+        L.gmb_validate_blocks.argtypes = [ctypes.POINTER(CsrStruct), ctypes.POINTER(BlocksStruct), vp, vp]
         L.gmb_read_sizes.restype = ctypes.c_int
         L.gmb_read_sizes.argtypes = [ctypes.POINTER(BlocksStruct), vp, vp]
         L.gmb_gather_features.restype = ctypes.c_int
@@ -246,6 +249,12 @@ class Blocks:
         out = (ctypes.c_int64 * (3 * self.num_layers))()
         _check(lib().gmb_read_sizes(ctypes.byref(self.struct), out, _stream_handle()))
         return [tuple(int(out[3 * l + i]) for i in range(3)) for l in range(self.num_layers)]
+
+    def validate(self):
+        """Enqueues the device consistency check of the blocks; a violation
+        shows in the next csr.check_status() (GmbError EDEVICE)."""
+        _check(lib().gmb_validate_blocks(ctypes.byref(self.csr.struct), ctypes.byref(self.struct),
+                                         ctypes.c_void_p(self.csr.state.data_ptr()), _stream_handle()))
 
     def blocks(self):
         """Per-layer Block views cut to the device sizes (synchronises)."""

@@ -214,6 +214,9 @@ int32_t owner_slots() {
   return slots;
 }
 
+int enqueue_validation(const gmb_csr* csr, const gmb_blocks* b, uint32_t* status, hipStream_t s);
+bool validate_every_call();
+
 // Enqueues the sampling kernels: the blocks go to `outb` (plan offsets
 // off_ids, off_sizes and the hops'), the scratch words to `scr`.
 int run_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, int32_t num_layers, uint64_t seed,
@@ -352,7 +355,25 @@ int run_sampling(const gmb_csr* csr, const int32_t* seeds, int32_t num_seeds, in
                       clear_cap, table, csr->num_nodes, s);
   if (e != hipSuccess) return hip_fail(e, "deferred-id launch");
   *out = res;
+  if (validate_every_call()) return enqueue_validation(csr, out, status, s);
   return ok();
+}
+
+// Enqueues the consistency check of every block (gmb_validate_blocks).
+int enqueue_validation(const gmb_csr* csr, const gmb_blocks* b, uint32_t* status, hipStream_t s) {
+  for (int l = 0; l < b->num_layers; ++l) {
+    const gmb_block& k = b->blk[l];
+    gmb::ValidateArgs v{k.indptr, k.indices, k.nbr, k.src_ids, k.sizes, k.cap_dst, k.cap_src, k.cap_nnz, k.fanout};
+    hipError_t e = gmb::launch_validate(v, csr->num_nodes, status, s);
+    if (e != hipSuccess) return hip_fail(e, "validation launch");
+  }
+  return GMB_OK;
+}
+
+// GMB_VALIDATE=1 in the environment: every sampling call checks its blocks.
+bool validate_every_call() {
+  const char* v = std::getenv("GMB_VALIDATE");
+  return v && v[0] == '1';
 }
 
 // The scratch of gmb_sample_blocks_noalloc: a fixed array in device memory
@@ -539,6 +560,7 @@ int gmb_read_status(void* state, void* stream) {
   if (word & GMB_STATUS_INTERNAL)
     return fail(GMB_EDEVICE, "a bounded wait in the relabel scan ran out: the blocks of that call are wrong "
                              "(the sampler state has been cleared again)");
+  if (word & GMB_STATUS_INVALID) return fail(GMB_EDEVICE, "gmb_validate_blocks found an inconsistent block");
   return ok();
 }
 
@@ -581,6 +603,16 @@ int gmb_sample_blocks_noalloc(const gmb_csr* csr, const int32_t* seeds, int32_t 
   if (st != GMB_OK) return st;
   return run_sampling(csr, seeds, num_seeds, num_layers, seed, state, p, static_cast<char*>(out_buf), scratch_ptr,
                       out, as_stream(stream));
+}
+
+int gmb_validate_blocks(const gmb_csr* csr, const gmb_blocks* blocks, void* state, void* stream) {
+  if (!csr) return fail(GMB_EINVAL, "csr is NULL");
+  if (csr->num_nodes < 1 || csr->num_nodes > kMaxInt32)
+    return fail(GMB_EINVAL, "num_nodes=%lld outside 1..2^31-1", static_cast<long long>(csr->num_nodes));
+  int st = check_blocks(blocks);
+  if (st != GMB_OK) return st;
+  if (!state) return fail(GMB_EINVAL, "state is NULL");
+  return enqueue_validation(csr, blocks, static_cast<uint32_t*>(state), as_stream(stream));
 }
 
 int gmb_read_sizes(const gmb_blocks* blocks, int64_t* sizes, void* stream) {

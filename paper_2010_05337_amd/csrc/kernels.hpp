@@ -163,6 +163,17 @@ struct SeedArgs {
   int32_t fanout[GMB_MAX_LAYERS];
 };
 
+// One block's arrays and bounds, for the consistency check (k_validate).
+struct ValidateArgs {
+  const int32_t* indptr;
+  const int32_t* local;
+  const int32_t* nbr;
+  const int32_t* ids;
+  const int32_t* sizes;
+  int64_t cap_dst, cap_src, cap_nnz;
+  int fanout;
+};
+
 // sample.hip
 hipError_t launch_state_init(uint32_t* table, uint32_t* status, int64_t num_nodes, hipStream_t s);
 hipError_t launch_seed_scan(const SeedArgs& a, int num_values, const CsrArgs& g, hipStream_t s);
@@ -186,6 +197,11 @@ hipError_t launch_rank(const RankArgs& a, int num_values, const CsrArgs& g, int 
 // The last hop's deferred local ids; with clear_sizes, also the table
 // slots of ids[0 .. clear_sizes[kNSrc]) (the vertices the table hops
 // recorded) back to empty.
+// Checks one block's invariants (sizes within the capacities, row offsets
+// from 0 to nnz with at most `fanout` edges per row, every local id below
+// n_src and naming the edge's sampled vertex, every sampled vertex in the
+// graph) and sets GMB_STATUS_INVALID in *status on a violation.
+hipError_t launch_validate(const ValidateArgs& b, int64_t num_nodes, uint32_t* status, hipStream_t s);
 hipError_t launch_fix(const DeferredArgs& fix, const int32_t* ids, const int32_t* clear_sizes, int64_t clear_cap,
                       uint32_t* table, int64_t num_nodes, hipStream_t s);
 

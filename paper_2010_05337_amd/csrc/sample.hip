@@ -1115,6 +1115,39 @@ __global__ __launch_bounds__(256) void k_fix(DeferredArgs fix, const int32_t* id
   if (i < n && valid_vertex(u, num_nodes)) table[u] = kEmpty;
 }
 
+// The consistency check of one block (see launch_validate).  Every read is
+// bounded by the capacities, whatever the size words hold.
+__global__ __launch_bounds__(256) void k_validate(ValidateArgs b, int64_t num_nodes, uint32_t* status) {
+  const int32_t n_dst = load_size(&b.sizes[kNDst]);
+  const int32_t n_src = load_size(&b.sizes[kNSrc]);
+  const int32_t nnz = load_size(&b.sizes[kNnz]);
+  const bool sizes_ok = n_dst >= 0 && n_dst <= b.cap_dst && n_src >= n_dst && n_src <= b.cap_src && nnz >= 0 &&
+                        nnz <= b.cap_nnz;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (!sizes_ok) {
+    if (i == 0) raise_status(status, GMB_STATUS_INVALID);
+    return;
+  }
+  bool bad = false;
+  if (i <= n_dst) {
+    const int32_t a = b.indptr[i];
+    if (i == 0) bad |= a != 0;
+    if (i == n_dst) bad |= a != nnz;
+    if (i < n_dst) {
+      const int32_t c = b.indptr[i + 1];
+      bad |= c < a || c - a > b.fanout;
+    }
+  }
+  if (i < nnz) {
+    const int32_t l = b.local[i];
+    const int32_t u = b.nbr[i];
+    bad |= !valid_vertex(u, num_nodes);
+    if (l < 0 || l >= n_src) bad = true;
+    else bad |= b.ids[l] != u;
+  }
+  if (bad) raise_status(status, GMB_STATUS_INVALID);
+}
+
 inline unsigned grid_for(int64_t threads, int block = 256) {
   int64_t g = (threads + block - 1) / block;
   return static_cast<unsigned>(g < 1 ? 1 : g);
@@ -1297,6 +1330,12 @@ hipError_t launch_rank(const RankArgs& a, int num_values, const CsrArgs& g, int 
 #undef GMB_RANK
 #undef GMB_RANK_W
 #undef GMB_RANK_I
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const ValidateArgs& b, int64_t num_nodes, uint32_t* status, hipStream_t s) {
+  hipLaunchKernelGGL(k_validate, dim3(grid_for(std::max(b.cap_dst + 1, b.cap_nnz))), dim3(256), 0, s, b, num_nodes,
+                     status);
   return hipGetLastError();
 }
 

@@ -34,6 +34,7 @@ static void run_shape(int32_t B, std::vector<int32_t> fanouts, int64_t N, std::v
   CHECK(gmb_sample_blocks(&csr, static_cast<const int32_t*>(fake(4)), B, fanouts.data(), L, 0x1234, fake(3), sb,
                           fake(5), ws, &out, nullptr) == 0);
   CHECK(out.num_layers == L && out.num_seeds == B);
+  CHECK(gmb_validate_blocks(&csr, &out, fake(3), nullptr) == 0);
   CHECK(gmb_gather_features(out.blk[0].src_ids, out.blk[0].sizes + 1, out.blk[0].cap_src, fake(6), N, dims[0], 0,
                             fake(7), gmb_state_status_word(fake(3)), nullptr) == 0);
   gmb_sage_weights w{};
@@ -77,6 +78,7 @@ static void run_shape(int32_t B, std::vector<int32_t> fanouts, int64_t N, std::v
 }
 
 int main() {
+  setenv("GMB_VALIDATE", "1", 1);   // the sampling calls also enqueue the block check
   run_shape(1000, {15, 10, 5}, 2449029, {100, 256, 256, 47}, false);
   run_shape(4000, {25, 10}, 2449029, {128, 256, 47}, false);
   run_shape(1000, {15, 10, 5}, 111059956, {128, 256, 256, 172}, true);

@@ -32,6 +32,7 @@ hipError_t launch_owner(const OwnerArgs&, hipStream_t) { return hipSuccess; }
 hipError_t launch_rank(const RankArgs&, int, const CsrArgs&, int, int, int32_t*, uint32_t*, hipStream_t) {
   return hipSuccess;
 }
+hipError_t launch_validate(const ValidateArgs&, int64_t, uint32_t*, hipStream_t) { return hipSuccess; }
 hipError_t launch_fix(const DeferredArgs&, const int32_t*, const int32_t*, int64_t, uint32_t*, int64_t, hipStream_t) {
   return hipSuccess;
 }

@@ -364,3 +364,49 @@ def test_owner_overflow_path(orc, dg, fanouts, num_seeds, monkeypatch):
         csr.check_status()
     assert e.value.code == -5
     assert _table_is_clear(csr)
+
+
+def test_validation_mode_passes_on_real_blocks(orc, dg, tiny, monkeypatch):
+    """GMB_VALIDATE=1: every sampling call also runs the device check of its
+    blocks; on the library's own output it finds nothing (ER, R-MAT with
+    hubs, fan-outs above 64, the owners' overflow path)."""
+    monkeypatch.setenv("GMB_VALIDATE", "1")
+    csr = csr_on_device(tiny)
+    gpu_blocks(csr, dg.permutation(10000, 5)[:500], [10, 10], 3)
+    csr.check_status()
+    g = dg.rmat(15, 30_000, 250_000, (0.57, 0.19, 0.19), 9)
+    csr = csr_on_device(g)
+    seeds = dg.permutation(g.num_nodes, 4)[:800]
+    for fo in ([15, 10, 5], [70], [6, 30]):
+        gpu_blocks(csr, seeds, fo, 7)
+        csr.check_status()
+    monkeypatch.setenv("GMB_OWNER_TABLE_SLOTS", "64")
+    gpu_blocks(csr, seeds, [12, 8], 8)
+    csr.check_status()
+
+
+def test_validation_finds_a_corrupted_block(dg, tiny):
+    """The check reports a block whose local id names the wrong vertex, one
+    whose local id is out of range and one whose row offsets fall; the
+    state works again afterwards."""
+    csr = csr_on_device(tiny)
+    seeds = dg.permutation(10000, 5)[:300]
+    for what in ("wrong vertex", "out of range", "falling offsets"):
+        print(f"corruption: {what}", flush=True)
+        blocks = gmb.sample_blocks(csr, torch.from_numpy(seeds).cuda(), [5, 5], 3)
+        blocks.validate()
+        csr.check_status()
+        b = blocks.blocks()[0]
+        if what == "wrong vertex":
+            b.indices[0] = (b.indices[0] + 1) % b.n_src
+        elif what == "out of range":
+            b.indices[1] = b.n_src
+        else:
+            b.indptr[2] = b.indptr[1] - 1
+        blocks.validate()
+        with pytest.raises(gmb.GmbError) as e:
+            csr.check_status()
+        assert e.value.code == -3
+    blocks = gmb.sample_blocks(csr, torch.from_numpy(seeds).cuda(), [5, 5], 4)
+    blocks.validate()
+    csr.check_status()
