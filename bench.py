@@ -69,7 +69,7 @@ def parse():
                          "with its own sampler state and workspaces")
     ap.add_argument("--mode", choices=("infer", "train"), default="infer",
                     help="infer: sample + gather + forward (the default); train: the whole "
-                         "training iteration, + loss, backward and SGD (fp32 workloads)")
+                         "training iteration, + loss, backward and SGD (bf16 workloads: fp32 master weights)")
     ap.add_argument("--lr", type=float, default=0.01, help="SGD step size of --mode train")
     ap.add_argument("--embed", action="store_true",
                     help="--mode train: the layer-0 inputs are learnable vertex embeddings (a table "
@@ -459,8 +459,8 @@ def main():
     batches = [torch.from_numpy(b).to(dev) for b in wl.batches]
     nb = len(batches)
     if args.mode == "train":
-        if bf16:
-            print("--mode train runs fp32 workloads only", file=sys.stderr)
+        if bf16 and args.embed:
+            print("--embed runs fp32 workloads only (the embeddings are fp32)", file=sys.stderr)
             sys.exit(2)
         run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen)
         return
@@ -761,6 +761,9 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
     emb = dict(embedding=feats, emb_lr=args.lr) if args.embed else {}
     logits = torch.empty((cfg.batch, C), dtype=torch.float32, device=dev)
     grads = gmb.SageGrads(weights)
+    # a bf16 model trains fp32 master weights and keeps its bf16 matrices as
+    # their rounded copies
+    master = weights.master() if weights.dtype == gmb.GMB_BF16 else None
     K, W = args.steps, args.warmup
     losses = torch.zeros(W + 2 * K, dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
@@ -775,7 +778,10 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         lg = forward(blocks, x, b)
         gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
                           workspace=ws_bwd, **emb)
-        gmb.sgd_update(weights, grads, args.lr)
+        if master is not None:
+            gmb.sgd_update_bf16(weights, master, grads, args.lr)
+        else:
+            gmb.sgd_update(weights, grads, args.lr)
 
     def step(i):
         b = i % nb
@@ -827,7 +833,10 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         gmb.sage_backward(blocks, x, weights, lg, labels[b], ws_fwd, grads=grads, loss=losses[i:i + 1],
                           workspace=ws_bwd, **emb)
         e[4].record(comp)
-        gmb.sgd_update(weights, grads, args.lr)
+        if master is not None:
+            gmb.sgd_update_bf16(weights, master, grads, args.lr)
+        else:
+            gmb.sgd_update(weights, grads, args.lr)
         e[5].record(comp)
     torch.cuda.synchronize()
     T1 = time.perf_counter() - t1
@@ -845,7 +854,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         sizes = blocks.sizes()
         seeds_total += batches[b].numel()
         edges_total += sum(s[2] for s in sizes)
-        b_gather += alg_gather_bytes(sizes[0][1], cfg.feat_dim, 4)
+        b_gather += alg_gather_bytes(sizes[0][1], cfg.feat_dim, 2 if master is not None else 4)
         fwd_flops += linear_flops(sizes, cfg.dims)
         bwd_flops += backward_flops(sizes, cfg.dims)
     tf, tb = stage["forward"] / 1e3, stage["backward"] / 1e3
@@ -858,12 +867,14 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": 1e3 * T / K,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {cfg.num_nodes}-node graph, {g.num_edges} edges, feats f32 "
+        "dtype": cfg.feat_dtype, "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {cfg.num_nodes}-node graph, {g.num_edges} edges, feats "
+                               f"{cfg.feat_dtype} "
                                f"x{cfg.feat_dim}, SAGE {'-'.join(map(str, cfg.dims))}, fanouts {fanouts}, batch "
                                f"{cfg.batch}, {nb} batches per epoch, SGD lr {args.lr}",
                    "batch": cfg.batch, "fanouts": fanouts, "dims": list(cfg.dims), "batches_per_epoch": nb,
-                   "mode": "train", "fused": bool(args.fused), "embed": bool(args.embed)},
+                   "mode": "train", "fused": bool(args.fused), "embed": bool(args.embed),
+                   "weights": "bf16 matrices, fp32 master weights, fp32 backward" if master is not None else "f32"},
         "epoch_s": nb * T / K,
         "pass_a_runs_seeds_per_s": [seeds_total / t for t in runs],
         "sampled_edges_per_s": edges_total / T,
@@ -900,7 +911,7 @@ def _oracle_train_batch(wl, fanouts, lab_all, lr, b, weights=None):
     ws, wn, bs = weights if weights is not None else wl.weights.as_f64()
     seeds_np = wl.batches[b]
     ref = oracle.sample_blocks(g.indptr, g.indices, seeds_np, fanouts, wl.batch_key(b))
-    X = oracle.gather(wl.feats, ref[0].src).astype(np.float64)
+    X = oracle.widen(oracle.gather(wl.feats, ref[0].src), wl.cfg.feat_dtype)
     return oracle.sage_train_step(ref, X, ws, wn, bs, lab_all[seeds_np], lr)
 
 

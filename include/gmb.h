@@ -314,8 +314,9 @@ typedef struct {
 } gmb_sage_grads;
 
 /* Bytes of workspace gmb_sage_backward needs (0 for bad arguments,
- * including a model the training step does not support: bf16 weights,
- * hidden dims not a multiple of 4, a dims[l] above 640 for l >= 2). */
+ * including a model the training step does not support: hidden dims not a
+ * multiple of 4, a dims[l] above 640 for l >= 2).  For bf16 weights it
+ * includes fp32 copies of what the backward reads. */
 size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_weights* weights);
 
 /* Gradients of the loss L = (1/B) sum over the B seeds of the softmax
@@ -329,7 +330,12 @@ size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_wei
  * its destination rows plus, over every block edge (v <- u), its share
  * (dZ W_neigh^T)[v] / k_v of the mean.
  *   blocks, x, weights  as given to the gmb_sage_forward call that produced
- *                       `logits`; fp32 only.
+ *                       `logits`, fp32 or bf16.  A bf16 model's backward
+ *                       first widens block 0's destination rows of x, every
+ *                       layer's kept mean and hidden output and the matrices
+ *                       to fp32 (inside `ws`), then runs the fp32 backward
+ *                       on them: fp32 products, fp32 gradients (update
+ *                       with gmb_sgd_update_bf16).
  *   logits   device fp32 [num_seeds, dims[L]] from that call.
  *   labels   device int32 [num_seeds], the class of each seed in
  *            [0, dims[L]) (a label outside it is a data error: that row's
@@ -390,6 +396,16 @@ int gmb_sage_backward_embedding(const gmb_blocks* blocks, const void* x, const g
 /* One SGD step: every weight array W -= lr * dW, every bias b -= lr * db,
  * in place on the device arrays that `weights` points to (fp32). */
 int gmb_sgd_update(const gmb_sage_weights* weights, const gmb_sage_grads* grads, float lr, void* stream);
+
+/* One SGD step of a bf16 model (the trainer's update of Section III-E with
+ * the dense parameters kept in fp32): the fp32 master weights `master`
+ * (same dims, dtype GMB_F32) take W -= lr * dW and b -= lr * db, then
+ * every bf16 matrix of `weights` becomes its master rounded to the nearest
+ * bf16 (ties to even), and each bias of `weights`, when it is not the
+ * master's own array, a copy of the master's.  All device arrays,
+ * caller-owned, updated in place on `stream`. */
+int gmb_sgd_update_bf16(const gmb_sage_weights* weights, const gmb_sage_weights* master, const gmb_sage_grads* grads,
+                        float lr, void* stream);
 
 #ifdef __cplusplus
 }

@@ -34,7 +34,7 @@ EXPORTS = (
     "gmb_forward_hidden_offset", "gmb_sage_forward", "gmb_sage_forward_fused", "gmb_backward_workspace_bytes",
     "gmb_sage_backward", "gmb_sgd_update", "gmb_backward_embedding_workspace_bytes",
     "gmb_sage_backward_embedding", "gmb_sample_blocks_noalloc",
-    "gmb_validate_blocks",
+    "gmb_validate_blocks", "gmb_sgd_update_bf16",
 )
 
 
@@ -139,6 +139,9 @@ def lib() -> ctypes.CDLL:
         L.gmb_sage_backward_embedding.argtypes = [ctypes.POINTER(BlocksStruct), vp, ctypes.POINTER(WeightsStruct),
                                                   vp, vp, vp, sz, ctypes.POINTER(GradsStruct), vp, vp, sz, vp,
                                                   ctypes.c_int64, ctypes.c_float, vp]
+        L.gmb_sgd_update_bf16.restype = ctypes.c_int
+        L.gmb_sgd_update_bf16.argtypes = [ctypes.POINTER(WeightsStruct), ctypes.POINTER(WeightsStruct),
+                                          ctypes.POINTER(GradsStruct), ctypes.c_float, vp]
         L.gmb_sgd_update.restype = ctypes.c_int
         L.gmb_sgd_update.argtypes = [ctypes.POINTER(WeightsStruct), ctypes.POINTER(GradsStruct),
                                      ctypes.c_float, vp]
@@ -377,6 +380,11 @@ class SageWeights:
     def torch_dtype(self):
         return torch.bfloat16 if self.dtype == GMB_BF16 else torch.float32
 
+    def master(self) -> "SageWeights":
+        """fp32 copies of the matrices (the biases are shared): the master
+        weights that sgd_update_bf16 updates for a bf16 model."""
+        return SageWeights([w.float() for w in self.w_self], [w.float() for w in self.w_neigh], self.bias)
+
 
 def forward_workspace_bytes(blocks: Blocks, weights: SageWeights) -> int:
     return lib().gmb_forward_workspace_bytes(ctypes.byref(blocks.struct), ctypes.byref(weights.struct))
@@ -536,3 +544,11 @@ def sgd_update(weights: SageWeights, grads: SageGrads, lr: float):
     """W -= lr * dW and b -= lr * db in place (fp32 weights)."""
     _check(lib().gmb_sgd_update(ctypes.byref(weights.struct), ctypes.byref(grads.struct), float(lr),
                                 _stream_handle()))
+
+
+def sgd_update_bf16(weights: SageWeights, master: SageWeights, grads: SageGrads, lr: float):
+    """One SGD step of a bf16 model: the fp32 master weights W -= lr * dW,
+    then the bf16 matrices become the new masters rounded to nearest even
+    (the biases, fp32 in both, are updated in the master and copied)."""
+    _check(lib().gmb_sgd_update_bf16(ctypes.byref(weights.struct), ctypes.byref(master.struct),
+                                     ctypes.byref(grads.struct), float(lr), _stream_handle()))

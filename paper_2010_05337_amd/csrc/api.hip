@@ -709,12 +709,59 @@ struct BackwardPlan {
   int64_t scan_len;                            // ints of one layer's scan state
   int64_t clear_len;                           // ints cleared at the start (counters + scan states)
   size_t total;
+  // bf16 models: fp32 copies of what the backward reads (the forward
+  // workspace laid out for fp32, block 0's destination rows of x, the
+  // matrices), after the fp32 backward's own workspace
+  size_t off_shadow, off_x32, off_w32[GMB_MAX_LAYERS][2];
+  size_t fp32_total;
 };
 
 // embed: layer 0's inputs are learnable vertex embeddings, so the backward
 // also runs layer 0's input gradient and its transpose (the rows it needs:
 // layer 0's destinations for the self part and the mean's gradient).
+int plan_backward_f32(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* plan, bool embed);
+
+// The fp32 weights struct of a bf16 model's training step: the same dims
+// and biases, the matrices at the fp32 copies of the plan in `ws`.
+gmb_sage_weights widened_weights(const gmb_sage_weights* w, const BackwardPlan& p, char* ws) {
+  gmb_sage_weights w32 = *w;
+  w32.dtype = GMB_F32;
+  for (int l = 0; l < w->num_layers; ++l) {
+    w32.w_self[l] = ws + p.off_w32[l][0];
+    w32.w_neigh[l] = ws + p.off_w32[l][1];
+  }
+  return w32;
+}
+
 int plan_backward(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* plan, bool embed) {
+  if (!w) return fail(GMB_EINVAL, "weights is NULL");
+  if (w->dtype != GMB_BF16) return plan_backward_f32(b, w, plan, embed);
+  if (embed) return fail(GMB_EINVAL, "learnable embeddings are fp32 only");
+  // the fp32 backward on fp32 copies, then room for the copies
+  gmb_sage_weights w32 = *w;
+  w32.dtype = GMB_F32;
+  BackwardPlan p;
+  int st = plan_backward_f32(b, &w32, &p, false);
+  if (st != GMB_OK) return st;
+  ForwardPlan fp32;
+  plan_forward(b, &w32, &fp32);
+  size_t off = p.total;
+  p.fp32_total = p.total;
+  p.off_shadow = off;
+  off = align_up(off + fp32.total);
+  p.off_x32 = off;
+  off = align_up(off + 4 * static_cast<size_t>(std::max<int64_t>(b->blk[0].cap_dst, 1)) * w->dims[0]);
+  for (int l = 0; l < w->num_layers; ++l)
+    for (int k = 0; k < 2; ++k) {
+      p.off_w32[l][k] = off;
+      off = align_up(off + 4 * static_cast<size_t>(w->dims[l]) * w->dims[l + 1]);
+    }
+  p.total = off;
+  *plan = p;
+  return GMB_OK;
+}
+
+int plan_backward_f32(const gmb_blocks* b, const gmb_sage_weights* w, BackwardPlan* plan, bool embed) {
   ForwardPlan fp;
   int st = plan_forward(b, w, &fp);
   if (st != GMB_OK) return st;
@@ -807,6 +854,41 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
   if (ws_bytes < p.total) return fail(GMB_ENOSPC, "workspace holds %zu bytes, %zu needed", ws_bytes, p.total);
   const hipStream_t s = as_stream(stream);
   const int L = weights->num_layers;
+  if (weights->dtype == GMB_BF16 && blocks->num_seeds > 0) {
+    // a bf16 model: widen what the backward reads to fp32 (block 0's
+    // destination rows of x, every layer's mean and hidden output in the
+    // fp32 layout, the matrices), then the fp32 backward on the copies
+    if (!x) return fail(GMB_EINVAL, "x is NULL");
+    char* base = static_cast<char*>(ws);
+    const gmb_sage_weights w32 = widened_weights(weights, p, base);
+    ForwardPlan f32;
+    plan_forward(blocks, &w32, &f32);
+    const char* fsrc = static_cast<const char*>(fwd_ws);
+    gmb::WidenArgs wa{};
+    auto add = [&](const void* src, void* dst, const int32_t* rows_dev, int64_t cap_rows, int64_t cols) {
+      wa.src[wa.count] = static_cast<const uint16_t*>(src);
+      wa.dst[wa.count] = static_cast<float*>(dst);
+      wa.rows_dev[wa.count] = rows_dev;
+      wa.cap_rows[wa.count] = cap_rows;
+      wa.cols[wa.count++] = cols;
+    };
+    const gmb_block& b0 = blocks->blk[0];
+    add(x, base + p.off_x32, b0.sizes + gmb::kNDst, std::max<int64_t>(b0.cap_dst, 1), weights->dims[0]);
+    for (int l = 0; l < L; ++l) {
+      const gmb_block& bk = blocks->blk[l];
+      add(fsrc + fp.off_agg[l], base + p.off_shadow + f32.off_agg[l], bk.sizes + gmb::kNDst,
+          std::max<int64_t>(bk.cap_dst, 1), weights->dims[l]);
+      if (l + 1 < L)
+        add(fsrc + fp.off_hidden[l], base + p.off_shadow + f32.off_hidden[l], bk.sizes + gmb::kNDst,
+            std::max<int64_t>(bk.cap_dst, 1), weights->dims[l + 1]);
+      add(weights->w_self[l], base + p.off_w32[l][0], nullptr, weights->dims[l], weights->dims[l + 1]);
+      add(weights->w_neigh[l], base + p.off_w32[l][1], nullptr, weights->dims[l], weights->dims[l + 1]);
+    }
+    hipError_t e = gmb::launch_widen(wa, s);
+    if (e != hipSuccess) return hip_fail(e, "widen launch");
+    return run_backward(blocks, base + p.off_x32, &w32, logits, labels, base + p.off_shadow, f32.total, grads, loss,
+                        ws, p.fp32_total, nullptr, 0, 0.f, stream);
+  }
   if (blocks->num_seeds == 0) {
     // an empty batch: the mean over no seeds is taken as 0, so are the
     // gradients, and no embedding row changes
@@ -937,6 +1019,42 @@ int gmb_sgd_update(const gmb_sage_weights* weights, const gmb_sage_grads* grads,
     a.n[a.count++] = n;
     a.w[a.count] = const_cast<float*>(weights->bias[l]);
     a.g[a.count] = grads->d_bias[l];
+    a.n[a.count++] = weights->dims[l + 1];
+  }
+  hipError_t e = gmb::launch_sgd(a, lr, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(e, "update launch");
+  return ok();
+}
+
+int gmb_sgd_update_bf16(const gmb_sage_weights* weights, const gmb_sage_weights* master, const gmb_sage_grads* grads,
+                        float lr, void* stream) {
+  if (!weights || !master) return fail(GMB_EINVAL, "weights or master is NULL");
+  if (weights->dtype != GMB_BF16 || master->dtype != GMB_F32)
+    return fail(GMB_EINVAL, "weights must be bf16 and master fp32");
+  if (weights->num_layers != master->num_layers || weights->num_layers < 1 || weights->num_layers > GMB_MAX_LAYERS)
+    return fail(GMB_EINVAL, "weights and master differ in layers (or none)");
+  for (int l = 0; l <= weights->num_layers; ++l)
+    if (weights->dims[l] != master->dims[l]) return fail(GMB_EINVAL, "dims[%d] differ", l);
+  int st = check_grads(grads, weights);
+  if (st != GMB_OK) return st;
+  gmb::SgdArgs a{};
+  for (int l = 0; l < weights->num_layers; ++l) {
+    if (!weights->w_self[l] || !weights->w_neigh[l] || !weights->bias[l] || !master->w_self[l] ||
+        !master->w_neigh[l] || !master->bias[l])
+      return fail(GMB_EINVAL, "layer %d weight is NULL", l);
+    const int64_t n = static_cast<int64_t>(weights->dims[l]) * weights->dims[l + 1];
+    const void* lo[2] = {weights->w_self[l], weights->w_neigh[l]};
+    const void* hi[2] = {master->w_self[l], master->w_neigh[l]};
+    float* const g[2] = {grads->d_self[l], grads->d_neigh[l]};
+    for (int k = 0; k < 2; ++k) {
+      a.w[a.count] = static_cast<float*>(const_cast<void*>(hi[k]));
+      a.g[a.count] = g[k];
+      a.lo[a.count] = static_cast<uint16_t*>(const_cast<void*>(lo[k]));
+      a.n[a.count++] = n;
+    }
+    a.w[a.count] = const_cast<float*>(master->bias[l]);
+    a.g[a.count] = grads->d_bias[l];
+    a.mirror[a.count] = weights->bias[l] == master->bias[l] ? nullptr : const_cast<float*>(weights->bias[l]);
     a.n[a.count++] = weights->dims[l + 1];
   }
   hipError_t e = gmb::launch_sgd(a, lr, as_stream(stream));

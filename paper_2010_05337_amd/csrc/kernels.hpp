@@ -226,6 +226,24 @@ struct SgdArgs {
   float* w[3 * GMB_MAX_LAYERS];
   const float* g[3 * GMB_MAX_LAYERS];
   int64_t n[3 * GMB_MAX_LAYERS];
+  // after the update, optionally: the new value rounded to bf16 (RNE) into
+  // lo[t], and/or copied into mirror[t] (the bf16 model's matrices and
+  // biases, kept beside fp32 master weights)
+  uint16_t* lo[3 * GMB_MAX_LAYERS];
+  float* mirror[3 * GMB_MAX_LAYERS];
+};
+
+// bf16 -> fp32 copies for the training step of a bf16 model: segment t is
+// rows x cols elements, rows = *rows_dev[t] clamped to cap_rows[t] when
+// rows_dev[t] is given, else cap_rows[t].
+constexpr int kMaxWiden = 4 * GMB_MAX_LAYERS + 2;
+struct WidenArgs {
+  int count;
+  const uint16_t* src[kMaxWiden];
+  float* dst[kMaxWiden];
+  const int32_t* rows_dev[kMaxWiden];
+  int64_t cap_rows[kMaxWiden];
+  int64_t cols[kMaxWiden];
 };
 hipError_t launch_xent(const float* logits, const int32_t* labels, int n, int C, int ldz, float* dz,
                        float* loss_rows, int32_t* clear, int64_t clear_n, hipStream_t s);
@@ -285,6 +303,7 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
                                 int64_t num_nodes, float lr, const WgradArgs* defer, const ReduceArgs* fold,
                                 hipStream_t s);
 hipError_t launch_sgd(const SgdArgs& a, float lr, hipStream_t s);
+hipError_t launch_widen(const WidenArgs& a, hipStream_t s);
 // every array of `a` (w[t], n[t]; g unused) and *scalar (if not NULL) to 0
 hipError_t launch_zero(const SgdArgs& a, float* scalar, hipStream_t s);
 

@@ -928,10 +928,45 @@ __global__ __launch_bounds__(256) void k_sgd(SgdArgs a, float lr) {
   for (int t = 0; t < a.count; ++t) {
     float* w = a.w[t];
     const float* g = a.g[t];
+    uint16_t* lo = a.lo[t];
+    float* mirror = a.mirror[t];
     const int64_t n = a.n[t];
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
-         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-      w[i] -= lr * g[i];
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+      const float v = w[i] - lr * g[i];
+      w[i] = v;
+      if (lo) lo[i] = f32_to_bf16(v);
+      if (mirror) mirror[i] = v;
+    }
+  }
+}
+
+// bf16 -> fp32, eight elements per step where a segment allows it.
+__global__ __launch_bounds__(256) void k_widen(WidenArgs a) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (int t = 0; t < a.count; ++t) {
+    int64_t rows = a.cap_rows[t];
+    if (a.rows_dev[t]) {
+      const int64_t r = load_size(a.rows_dev[t]);
+      rows = r < 0 ? 0 : (r < rows ? r : rows);
+    }
+    const int64_t n = rows * a.cols[t];
+    const uint16_t* src = a.src[t];
+    float* dst = a.dst[t];
+    const int64_t n8 = n / 8;
+    for (int64_t i = tid; i < n8; i += stride) {
+      const uint4 x = *reinterpret_cast<const uint4*>(src + 8 * i);
+      const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+      float4 lo, hi;
+      lo.x = bf16_to_f32(static_cast<uint16_t>(w[0])); lo.y = bf16_to_f32(static_cast<uint16_t>(w[0] >> 16));
+      lo.z = bf16_to_f32(static_cast<uint16_t>(w[1])); lo.w = bf16_to_f32(static_cast<uint16_t>(w[1] >> 16));
+      hi.x = bf16_to_f32(static_cast<uint16_t>(w[2])); hi.y = bf16_to_f32(static_cast<uint16_t>(w[2] >> 16));
+      hi.z = bf16_to_f32(static_cast<uint16_t>(w[3])); hi.w = bf16_to_f32(static_cast<uint16_t>(w[3] >> 16));
+      *reinterpret_cast<float4*>(dst + 8 * i) = lo;
+      *reinterpret_cast<float4*>(dst + 8 * i + 4) = hi;
+    }
+    for (int64_t i = 8 * n8 + tid; i < n; i += stride) dst[i] = bf16_to_f32(src[i]);
   }
 }
 
@@ -1094,6 +1129,13 @@ hipError_t launch_zero(const SgdArgs& a, float* scalar, hipStream_t s) {
   int64_t most = 1;
   for (int t = 0; t < a.count; ++t) most = std::max(most, a.n[t]);
   hipLaunchKernelGGL(k_zero, dim3(grid_of(most, 1024)), dim3(256), 0, s, a, scalar);
+  return hipGetLastError();
+}
+
+hipError_t launch_widen(const WidenArgs& a, hipStream_t s) {
+  int64_t most = 1;
+  for (int t = 0; t < a.count; ++t) most = std::max(most, a.cap_rows[t] * a.cols[t] / 8);
+  hipLaunchKernelGGL(k_widen, dim3(grid_of(most, 4096)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

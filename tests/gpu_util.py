@@ -129,3 +129,74 @@ def compare_train_step(orc, out, ref_blocks, X, w, labels, lr, wt, exact_hidden)
             assert np.abs(got - want).max() <= bound, (l, np.abs(got - want).max(), bound)
             assert not torch.equal(a, old) or np.abs(gr).max() == 0.0
     return errs
+
+
+TOL_BF16 = 2e-2
+
+
+def bf16_bits(a: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round to nearest even (the generator's)."""
+    from datagen import bf16_bits_from_f32
+    return bf16_bits_from_f32(np.ascontiguousarray(a, dtype=np.float32))
+
+
+def compare_train_step_bf16(orc, loss, grads, ref_blocks, X, w, labels, lr, master_before, master, wt):
+    """A bf16 model's training step against the oracle's fp64 step on the
+    same blocks and the same (bf16-exact) inputs: the loss and every
+    gradient within TOL_BF16 (the forward rounds the mean and the hidden
+    activations to bf16); the update W - lr dW in fp32 (to one unit in the
+    last place) on the fp32 master weights with the GPU's own gradients, the
+    bf16 matrices exactly
+    the masters rounded to nearest even, and the masters within lr times the
+    gradient tolerance of the oracle's step."""
+    ws, wn, bs = w.as_f64()
+    ref_loss, _, (dWs, dWn, dbs), (nws, nwn, nbs) = orc.sage_train_step(ref_blocks, X, ws, wn, bs, labels, lr)
+    assert abs(loss - ref_loss) <= TOL_BF16 * max(1.0, abs(ref_loss)), (loss, ref_loss)
+    errs = {}
+    for l in range(len(ws)):
+        for name, got, want in (("W_self", grads.d_self[l], dWs[l]), ("W_neigh", grads.d_neigh[l], dWn[l]),
+                                ("b", grads.d_bias[l], dbs[l])):
+            errs[f"{name}{l}"] = max_rel(got.cpu().numpy(), want)
+    print(f"bf16 step: loss {loss:.6g} (oracle {ref_loss:.6g}); gradient errors {errs}", flush=True)
+    assert all(e <= TOL_BF16 for e in errs.values()), errs
+    lr32 = np.float32(lr)
+    for k, (before, after, g_list, want_list, lo_list) in enumerate((
+            (master_before[0], master.w_self, grads.d_self, nws, wt.w_self),
+            (master_before[1], master.w_neigh, grads.d_neigh, nwn, wt.w_neigh),
+            (master_before[2], master.bias, grads.d_bias, nbs, wt.bias))):
+        for l, (b0, a, g, want, lo) in enumerate(zip(before, after, g_list, want_list, lo_list)):
+            a_h = a.cpu().numpy()
+            # W - lr dW in fp32: the product rounded once, or fused into the
+            # sum; they differ by at most the product's rounding plus the
+            # result's, one unit in the last place of each
+            w0, step = b0.cpu().numpy(), lr32 * g.cpu().numpy()
+            expect = w0 - step
+            ulps = np.spacing(np.abs(step)) + np.spacing(np.abs(expect))
+            assert (np.abs(a_h - expect) <= ulps).all(), (k, l, "master update", np.abs(a_h - expect).max())
+            if k < 2:
+                assert np.array_equal(lo.view(torch.int16).cpu().numpy().view(np.uint16), bf16_bits(a_h)), (k, l)
+            bound = lr * TOL_BF16 * max(np.abs(g.cpu().numpy()).max(), 1e-30) + 2.0 ** -22 * np.abs(want).max()
+            assert np.abs(a_h.astype(np.float64) - want).max() <= bound, (k, l)
+    return errs
+
+
+def margin_biases(orc, ref, X, w):
+    """Hidden-layer biases that keep every pre-activation of this batch away
+    from zero by at least half of its column's largest magnitude (column c
+    positive for even c, negative for odd c): the forward's fp32 error (at
+    most 1e-4 of a row's largest value) then cannot move any value across
+    the ReLU, and the fp32 and fp64 masks agree.  Checked from the oracle's
+    values."""
+    ws, wn, _ = w.as_f64()
+    bias = [b.copy() for b in w.bias]
+    H = X
+    for l, blk in enumerate(ref[:-1]):
+        m = orc.mean_aggregate(blk, H)
+        z = H[:blk.n_dst] @ ws[l] + m @ wn[l]
+        spread = np.abs(z).max(axis=0, initial=0.0)
+        sign = np.where(np.arange(z.shape[1]) % 2 == 0, 1.0, -1.0)
+        bias[l] = (sign * (1.5 * spread + 0.5)).astype(np.float32)
+        pre = z + bias[l].astype(np.float64)
+        assert np.abs(pre).min(initial=1.0) > 1e-3 * np.abs(pre).max(initial=0.0), l
+        H = np.maximum(pre, 0.0)
+    return bias

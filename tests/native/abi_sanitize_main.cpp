@@ -59,6 +59,31 @@ static void run_shape(int32_t B, std::vector<int32_t> fanouts, int64_t N, std::v
     g.d_neigh[l] = static_cast<float*>(fake(60 + l));
     g.d_bias[l] = static_cast<float*>(fake(70 + l));
   }
+  // the same model in bf16: forward, backward on widened copies, the update
+  // of fp32 masters
+  {
+    gmb_sage_weights wb = w;
+    wb.dtype = GMB_BF16;
+    const size_t fwb = gmb_forward_workspace_bytes(&out, &wb);
+    CHECK(fwb > 0);
+    CHECK(gmb_sage_forward(&out, fake(8), &wb, static_cast<float*>(fake(9)), fake(40), fwb, nullptr) == 0);
+    const size_t bwb = gmb_backward_workspace_bytes(&out, &wb);
+    if (bwb > 0) {
+      gmb_sage_grads gb{};
+      gb.num_layers = L;
+      for (int l = 0; l < L; ++l) {
+        gb.d_self[l] = static_cast<float*>(fake(80 + l));
+        gb.d_neigh[l] = static_cast<float*>(fake(90 + l));
+        gb.d_bias[l] = static_cast<float*>(fake(100 + l));
+      }
+      CHECK(gmb_sage_backward(&out, fake(8), &wb, static_cast<const float*>(fake(9)),
+                              static_cast<const int32_t*>(fake(42)), fake(40), fwb, &gb, static_cast<float*>(fake(43)),
+                              fake(44), bwb, nullptr) == 0);
+      CHECK(gmb_backward_embedding_workspace_bytes(&out, &wb) == 0);
+      CHECK(gmb_sgd_update_bf16(&wb, &w, &gb, 0.01f, nullptr) == 0);
+      CHECK(gmb_sgd_update_bf16(&w, &w, &gb, 0.01f, nullptr) == GMB_EINVAL);
+    }
+  }
   const size_t bw = gmb_backward_workspace_bytes(&out, &w);
   if (bw > 0) {
     CHECK(gmb_sage_backward(&out, fake(8), &w, static_cast<const float*>(fake(9)), static_cast<const int32_t*>(fake(42)),

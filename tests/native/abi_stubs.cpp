@@ -69,6 +69,7 @@ hipError_t launch_mean_backward(const int32_t*, const int32_t*, const int32_t*, 
   return hipSuccess;
 }
 hipError_t launch_sgd(const SgdArgs&, float, hipStream_t) { return hipSuccess; }
+hipError_t launch_widen(const WidenArgs&, hipStream_t) { return hipSuccess; }
 hipError_t launch_zero(const SgdArgs&, float*, hipStream_t) { return hipSuccess; }
 
 }  // namespace gmb

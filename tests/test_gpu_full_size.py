@@ -22,7 +22,7 @@ if not torch.cuda.is_available():
 
 import paper_2010_05337_amd as gmb  # noqa: E402
 from datagen.configs import make_workload  # noqa: E402
-from gpu_util import (assert_blocks_equal, compare_train_step, rowwise_rel_err, tensor_bits,  # noqa: E402
+from gpu_util import (margin_biases, assert_blocks_equal, compare_train_step, rowwise_rel_err, tensor_bits,  # noqa: E402
                       tensor_f64, to_torch_feats, to_torch_weights)
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
@@ -157,39 +157,17 @@ def test_streams_reproduce_one_stream(setup):
         ln.csr.check_status()
 
 
-def margin_biases(orc, ref, X, w):
-    """Hidden-layer biases that keep every pre-activation of this batch away
-    from zero by at least half of its column's largest magnitude (column c
-    positive for even c, negative for odd c): the forward's fp32 error (at
-    most 1e-4 of a row's largest value) then cannot move any value across
-    the ReLU, and the fp32 and fp64 masks agree.  Checked from the oracle's
-    values."""
-    ws, wn, _ = w.as_f64()
-    bias = [b.copy() for b in w.bias]
-    H = X
-    for l, blk in enumerate(ref[:-1]):
-        m = orc.mean_aggregate(blk, H)
-        z = H[:blk.n_dst] @ ws[l] + m @ wn[l]
-        spread = np.abs(z).max(axis=0, initial=0.0)
-        sign = np.where(np.arange(z.shape[1]) % 2 == 0, 1.0, -1.0)
-        bias[l] = (sign * (1.5 * spread + 0.5)).astype(np.float32)
-        pre = z + bias[l].astype(np.float64)
-        assert np.abs(pre).min(initial=1.0) > 1e-3 * np.abs(pre).max(initial=0.0), l
-        H = np.maximum(pre, 0.0)
-    return bias
-
-
 def test_full_size_training_step(orc, dg, setup):
     """Batch 0 of the epoch: sample, gather, forward, loss, backward and one
     SGD step on the device, in the buffers bench.py's training mode uses,
     against the oracle's fp64 step."""
     wl, csr, feats, _, _, _ = setup
     cfg, g = wl.cfg, wl.graph
-    if cfg.feat_dtype != "f32":
-        pytest.skip("the training step is fp32 only")
     seeds = wl.batches[0]
     ref = orc.sample_blocks(g.indptr, g.indices, seeds, list(cfg.fanouts), wl.batch_key(0))
-    X = orc.gather(wl.feats, ref[0].src).astype(np.float64)
+    X = orc.widen(orc.gather(wl.feats, ref[0].src), cfg.feat_dtype)
+    if cfg.feat_dtype == "bf16":
+        return _bf16_training_step(orc, dg, wl, csr, feats, ref, X)
     w = types.SimpleNamespace(**vars(wl.weights))
     w.bias = margin_biases(orc, ref, X, wl.weights)
     w.as_f64 = lambda: ([a.astype(np.float64) for a in w.w_self], [a.astype(np.float64) for a in w.w_neigh],
@@ -208,6 +186,30 @@ def test_full_size_training_step(orc, dg, setup):
     torch.cuda.synchronize()
     out = dict(hidden=hidden, grads=grads, loss=float(loss.item()), before=before)
     compare_train_step(orc, out, ref, X, w, labels, lr, wt, exact_hidden=False)
+    csr.check_status()
+
+
+def _bf16_training_step(orc, dg, wl, csr, feats, ref, X):
+    """test_full_size_training_step for a bf16 workload: fp32 master weights,
+    the oracle's fp64 step within 2e-2 (see test_bf16_train_step_matches_the_oracle)."""
+    from gpu_util import compare_train_step_bf16
+    cfg, g = wl.cfg, wl.graph
+    w = types.SimpleNamespace(**vars(wl.weights))
+    w.bias = margin_biases(orc, ref, X, wl.weights)
+    base = wl.weights.as_f64()
+    w.as_f64 = lambda: (base[0], base[1], [b.astype(np.float64) for b in w.bias])
+    wt = to_torch_weights(w)
+    master = wt.master()
+    lane = Lane(csr, wl, feats, wt)
+    print(f"{cfg.name}: bf16 training step on batch 0, {len(wl.batches[0])} seeds", flush=True)
+    blocks, x, logits, _ = lane.run(wl, feats, wt, 0)
+    assert_blocks_equal(host_blocks(blocks), ref, f"{cfg.name} batch 0")
+    labels = dg.labels(g.num_nodes, cfg.dims[-1], 7)[wl.batches[0]]
+    grads, loss = gmb.sage_backward(blocks, x, wt, logits, torch.from_numpy(labels).cuda(), lane.ws_fwd)
+    before = [[t.clone() for t in arrs] for arrs in (master.w_self, master.w_neigh, master.bias)]
+    gmb.sgd_update_bf16(wt, master, grads, 0.1)
+    torch.cuda.synchronize()
+    compare_train_step_bf16(orc, float(loss.item()), grads, ref, X, w, labels, 0.1, before, master, wt)
     csr.check_status()
 
 
@@ -289,11 +291,11 @@ def test_full_size_embedding_step(orc, dg, setup):
     test)."""
     wl, csr, feats, _, _, _ = setup
     cfg, g = wl.cfg, wl.graph
-    if cfg.feat_dtype != "f32":
-        pytest.skip("the training step is fp32 only")
     seeds = wl.batches[0]
     ref = orc.sample_blocks(g.indptr, g.indices, seeds, list(cfg.fanouts), wl.batch_key(0))
-    X = orc.gather(wl.feats, ref[0].src).astype(np.float64)
+    X = orc.widen(orc.gather(wl.feats, ref[0].src), cfg.feat_dtype)
+    if cfg.feat_dtype == "bf16":
+        return _bf16_training_step(orc, dg, wl, csr, feats, ref, X)
     w = types.SimpleNamespace(**vars(wl.weights))
     w.bias = margin_biases(orc, ref, X, wl.weights)
     w.as_f64 = lambda: ([a.astype(np.float64) for a in w.w_self], [a.astype(np.float64) for a in w.w_neigh],

@@ -33,7 +33,7 @@ import paper_2010_05337_amd as gmb  # noqa: E402
 from gpu_util import (assert_blocks_equal, compare_train_step, csr_on_device, gpu_blocks, max_rel,  # noqa: E402
                       run_train_step, to_torch_weights)
 
-from gpu_util import TOL_GRAD  # noqa: E402
+from gpu_util import TOL_GRAD, bf16_bits, compare_train_step_bf16  # noqa: E402
 
 
 def exact_graph(n, seed, min_deg=8, spread=9, broadcaster=None):
@@ -168,8 +168,9 @@ def test_sgd_steps_lower_the_loss(dg):
 
 
 def test_backward_rejects_unsupported_models(dg):
-    """bf16 weights and hidden widths that are not a multiple of 4 are
-    refused before any launch."""
+    """Hidden widths that are not a multiple of 4 are refused before any
+    launch, and so are learnable embeddings with bf16 weights; the bf16
+    backward itself is accepted."""
     n = 2000
     g = dg.er_directed(n, 8.0, 41)
     csr = csr_on_device(g)
@@ -186,6 +187,10 @@ def test_backward_rejects_unsupported_models(dg):
         x = gmb.gather_features(blocks, ft)
         ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
         logits = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd)
+        if dtype == "bf16":
+            assert gmb.backward_workspace_bytes(blocks, wt) > 0
+            assert gmb.backward_embedding_workspace_bytes(blocks, wt) == 0
+            continue
         assert gmb.backward_workspace_bytes(blocks, wt) == 0
         with pytest.raises(gmb.GmbError):
             gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd)
@@ -379,3 +384,74 @@ def test_empty_batch(dg):
     logits_f, x_dst = gmb.sage_forward_fused(blocks, ft, wt, workspace=ws)
     assert tuple(logits_f.shape) == (0, 5) and x_dst.shape[0] == 0
     csr.check_status()
+
+
+
+@pytest.mark.parametrize("dims,fanouts,n_seeds", [([16, 32, 8], [4, 2], 64), ([128, 256, 47], [8, 4], 150),
+                                                  ([24, 64, 32, 12], [2, 4, 8], 50)])
+def test_bf16_train_step_matches_the_oracle(orc, dg, dims, fanouts, n_seeds):
+    """A bf16 model (bf16 features and matrices, exact in bf16: integers and
+    multiples of 1/16) trains through fp32 copies and fp32 master weights:
+    loss and gradients against the oracle's fp64 step within 2e-2, the
+    update exact on the masters, the bf16 matrices their rounding.  The
+    hidden biases keep every pre-activation far from zero, so that the bf16
+    rounding of the hidden layers cannot flip a ReLU."""
+    import types
+    from gpu_util import margin_biases
+    n = 3000
+    g = exact_graph(n, 51 + len(dims))
+    feats32, w32 = exact_model(dg, n, dims, 52 + dims[1])
+    seeds = dg.permutation(n, 53)[:n_seeds]
+    labels = dg.labels(n, dims[-1], 54)[seeds]
+    key, lr = 55, 0.25
+    ref_blocks = orc.sample_blocks(g.indptr, g.indices, seeds, fanouts, key)
+    X = orc.gather(feats32, ref_blocks[0].src).astype(np.float64)
+    w = types.SimpleNamespace(dims=list(dims), w_self=[bf16_bits(a) for a in w32.w_self],
+                              w_neigh=[bf16_bits(a) for a in w32.w_neigh], bias=w32.bias, dtype="bf16")
+    w.bias = margin_biases(orc, ref_blocks, X, types.SimpleNamespace(
+        bias=w32.bias, as_f64=lambda: w32.as_f64()))
+    w.as_f64 = lambda: ([a.astype(np.float64) for a in w32.w_self], [a.astype(np.float64) for a in w32.w_neigh],
+                        [b.astype(np.float64) for b in w.bias])
+    print(f"bf16 training: dims {dims} fan-outs {fanouts} seeds {n_seeds}", flush=True)
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    master = wt.master()
+    ft = torch.from_numpy(bf16_bits(feats32).view(np.int16)).cuda().view(torch.bfloat16)
+    blocks, host = gpu_blocks(csr, seeds, fanouts, key)
+    assert_blocks_equal(host, ref_blocks)
+    x = gmb.gather_features(blocks, ft)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+    logits = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd)
+    y = torch.from_numpy(labels).cuda()
+    grads, loss = gmb.sage_backward(blocks, x, wt, logits, y, ws_fwd)
+    before = [[t.clone() for t in arrs] for arrs in (master.w_self, master.w_neigh, master.bias)]
+    gmb.sgd_update_bf16(wt, master, grads, lr)
+    torch.cuda.synchronize()
+    compare_train_step_bf16(orc, float(loss.item()), grads, ref_blocks, X, w, labels, lr, before, master, wt)
+    csr.check_status()
+
+
+def test_bf16_sgd_steps_lower_the_loss(dg):
+    """Five bf16 training steps on one batch of Gaussian data: the loss goes
+    down at every step."""
+    n, dims, fanouts = 10000, [32, 64, 64, 10], [5, 10, 15]
+    g = dg.er_directed(n, 12.0, 61)
+    feats = dg.features(n, dims[0], 62, "bf16")
+    w = dg.sage_weights(dims, 63, "bf16")
+    seeds = dg.permutation(n, 64)[:256]
+    labels = torch.from_numpy(dg.labels(n, dims[-1], 65)[seeds]).cuda()
+    csr = csr_on_device(g)
+    wt = to_torch_weights(w)
+    master = wt.master()
+    ft = torch.from_numpy(feats.view(np.int16)).cuda().view(torch.bfloat16)
+    blocks, _ = gpu_blocks(csr, seeds, fanouts, 66)
+    x = gmb.gather_features(blocks, ft)
+    ws_fwd = gmb._aligned_bytes(gmb.forward_workspace_bytes(blocks, wt), ft.device)[1]
+    losses = []
+    for _ in range(6):
+        logits = gmb.sage_forward(blocks, x, wt, workspace=ws_fwd)
+        grads, loss = gmb.sage_backward(blocks, x, wt, logits, labels, ws_fwd)
+        gmb.sgd_update_bf16(wt, master, grads, 0.5)
+        losses.append(float(loss.item()))
+    print("bf16 losses", losses, flush=True)
+    assert all(b < a for a, b in zip(losses, losses[1:])), losses
