@@ -542,6 +542,18 @@ __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes
 constexpr int kScanTile = 1024;
 constexpr int kLongList = 16;   // transpose lists longer than this take a workgroup each
 
+// The embedding update's groups: lanes per row, rows per group, entries per
+// row read in the first batch (tuning macros, -D at build time).
+#ifndef GMB_PULL_UPDATE_G
+#define GMB_PULL_UPDATE_G 32
+#endif
+#ifndef GMB_PULL_UPDATE_R
+#define GMB_PULL_UPDATE_R 4
+#endif
+#ifndef GMB_PULL_UPDATE_E
+#define GMB_PULL_UPDATE_E 2
+#endif
+
 // WG = 0: the scan alone (its own small register and LDS footprint);
 // 1, 2: workgroups past the scan's run the same layer's weight-gradient
 // products (16-byte or scalar loads of H and M), independent of the scan:
@@ -1098,7 +1110,7 @@ hipError_t launch_mean_backward(const int32_t* sizes, const int32_t* indptr, con
   const int chunks = d / 4;
   // each grid ends with kLongGrid workgroups for the long lists
   if (table) {
-    constexpr int kG = 32, kR = 4, kE = 2;
+    constexpr int kG = GMB_PULL_UPDATE_G, kR = GMB_PULL_UPDATE_R, kE = GMB_PULL_UPDATE_E;
     const unsigned rows = grid_of((std::max<int64_t>(cap_src, 1) + kR - 1) / kR * kG, 1 << 30);
     hipLaunchKernelGGL((k_pull_update<kG, kR, kE>), dim3(rows + kLongGrid), dim3(256), 0, s, sizes, off, csc,
                        cap_nnz, dM, dH, d, table, ids, num_nodes, lr, static_cast<int>(rows), scan_state + 1,
