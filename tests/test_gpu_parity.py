@@ -271,6 +271,21 @@ def test_forward_wide_model_f32(orc, dg):
     assert max(errs) <= 5e-6, errs
 
 
+@pytest.mark.parametrize("d_in,d_hid", [(64, 300), (128, 256), (100, 256)])
+def test_forward_large_layer_eight_waves_f32(orc, dg, d_in, d_hid):
+    """A first layer with 17.5k destination rows: the part-product linear
+    on eight waves per workgroup (K = 2 d_in of 128, 256 and 200, the last
+    not a multiple of the 32-wide chunk), ragged rows, and 300 outputs (a
+    ragged fifth column tile); fp32-level accuracy."""
+    g = dg.rmat(16, 60000, 1500000, (0.57, 0.19, 0.19), 91)
+    feats = dg.features(60000, d_in, 92, "f32")
+    w = dg.sage_weights([d_in, d_hid, 8], 93)
+    seeds = dg.permutation(60000, 94)[:8000]
+    # 17,502 destination rows in layer 0: 137 tiles of 128 rows per column tile
+    errs = _forward_case(orc, dg, g, feats, w, seeds, [3, 12], 95, TOL_F32)
+    assert max(errs) <= 5e-6, errs
+
+
 @pytest.mark.parametrize("dims,fanouts", [([8, 300, 20], [6, 3]), ([64, 130, 12], [4, 7]),
                                           ([128, 64, 40, 3], [3, 2, 5])])
 def test_forward_more_shapes_f32(orc, dg, tiny, dims, fanouts):
