@@ -145,6 +145,40 @@ def alg_gather_bytes(n_in: int, dim: int, es: int) -> int:
     return n_in * (2 * dim * es + 4)
 
 
+GATHER_SETS = 16
+
+
+def gather_launch_time(gmb, torch, csr, batches, fanouts, wl, cfg, feats, x_out, K, es, dev):
+    """The gather kernel's average launch duration for the roofline: the
+    first GATHER_SETS batches of the epoch sampled into workspaces of their
+    own (untimed), then K gathers back to back on one stream, cycling over
+    them, between one pair of HIP events on that stream.  The average holds
+    the gap between consecutive kernels but no event per launch (an event
+    pair around every launch, as in the per-stage pass, adds its own
+    dispatch latency of several microseconds).  16 batches' rows are about
+    2 GB on the 2.4M-node workload, far more than the caches hold.  Returns
+    (seconds per launch, algorithmic bytes per launch)."""
+    n = min(GATHER_SETS, len(batches))
+    nbytes = gmb.sample_workspace_bytes(cfg.batch, fanouts, cfg.num_nodes)
+    sets = []
+    for b in range(n):
+        ws = gmb._aligned_bytes(nbytes, dev)[1]
+        blocks = gmb.sample_blocks(csr, batches[b], fanouts, wl.batch_key(b), workspace=ws)
+        sets.append((ws, blocks, alg_gather_bytes(blocks.sizes()[0][1], cfg.feat_dim, es)))
+    for _, blocks, _ in sets:   # warm-up
+        gmb.gather_features(blocks, feats, out=x_out)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(K):
+        gmb.gather_features(sets[i % n][1], feats, out=x_out)
+    ev[1].record()
+    torch.cuda.synchronize()
+    csr.check_status()
+    total = sum(sets[i % n][2] for i in range(K))
+    return ev[0].elapsed_time(ev[1]) / 1e3 / K, total / K
+
+
 def alg_forward_bytes(sizes, dims, es: int) -> int:
     """Per layer: each source row read once, block CSR, mean rows written
     and read, weight matrices, output rows."""
@@ -162,9 +196,11 @@ def linear_flops(sizes, dims) -> int:
 
 def summarize_profile(args):
     """Markdown summary of `rocprofv3 --kernel-trace --stats --output-format
-    csv -- python bench.py ...`: the per-kernel statistics of the whole run,
-    and the gather kernel's average over the launches of pass B (isolated,
-    one stream), which is what `roofline.avg_launch_ms` measures."""
+    csv -- python bench.py ... --cpu-batches 0`: the per-kernel statistics of
+    the whole run, the gather kernel over the launches of pass B (isolated,
+    one stream, per-stage events) and of pass G (the run's last `steps`
+    gathers, back to back on one stream: what `roofline.avg_launch_ms`
+    measures), and pass B's kernels step by step."""
     import csv
     pre = args.summarize_profile
     stats = list(csv.DictReader(open(pre + "_kernel_stats.csv")))
@@ -184,6 +220,13 @@ def summarize_profile(args):
     out.append(f"k_gather launches in the run: {len(g)}; pass B (isolated, launches {lo}..{hi - 1}): "
                f"{len(sel)} launches, average {sum(sel) / max(len(sel), 1) / 1e3:.2f} us, "
                f"min {min(sel) / 1e3:.2f} us, max {max(sel) / 1e3:.2f} us" if sel else "no pass-B launches")
+    gt = [r for r in trace if "k_gather" in r["Kernel_Name"]][-args.steps:]
+    if len(gt) == args.steps:
+        dur = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in gt]
+        span = (int(gt[-1]["End_Timestamp"]) - int(gt[0]["Start_Timestamp"])) / len(gt)
+        out.append(f"pass G (the last {len(gt)} launches, back to back): kernel average {sum(dur) / len(dur) / 1e3:.2f} us, "
+                   f"min {min(dur) / 1e3:.2f} us, max {max(dur) / 1e3:.2f} us; first start to last end "
+                   f"{span / 1e3:.2f} us per launch (kernel plus the gap to the next)")
     # pass B step by step: kernels between the seed kernels that start each
     # step, median duration of each position over the complete steps
     gi = [i for i, r in enumerate(trace) if "k_gather" in r["Kernel_Name"]]
@@ -678,16 +721,18 @@ def main():
                             "runs_seeds_per_s": [seeds_total / t for t in runs_d], "streams": S,
                             "what": "sample_blocks + sage_forward_fused (layer-0 mean from the feature "
                                     "table, only block 0's destination rows gathered)"}
-    # dominant kernel of the path: the feature gather, one launch per step,
-    # timed in the isolated pass (the K launches after warm-up and pass A)
+    # dominant kernel of the path: the feature gather, K launches back to
+    # back on one stream (pass G, after the size pass)
+    t_launch, b_launch = gather_launch_time(gmb, torch, csr, batches, fanouts, wl, cfg, feats, x_buf, K, es, dev)
     traffic, traffic_source = gather_traffic(args.workload)
     res["roofline"] = {"kernel": "k_gather", "bound": "hbm",
-                       "achieved": b_gather / tg / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                       "frac": b_gather / tg / 1e9 / HBM_PEAK_GBPS, "traffic": traffic,
+                       "achieved": b_launch / t_launch / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                       "frac": b_launch / t_launch / 1e9 / HBM_PEAK_GBPS, "traffic": traffic,
                        "traffic_source": traffic_source,
-                       "alg_bytes_per_launch": b_gather / K, "avg_launch_ms": 1e3 * tg / K,
-                       "launches": f"{args.warmup + PASS_A_RUNS * K}..{args.warmup + (PASS_A_RUNS + 1) * K - 1} "
-                                   "(pass B)"}
+                       "alg_bytes_per_launch": b_launch, "avg_launch_ms": 1e3 * t_launch,
+                       "launches": f"the last {K} k_gather launches (pass G: {min(GATHER_SETS, nb)} batches "
+                                   "cycled, back to back on one stream)",
+                       "pass_b_event_bracket_ms": 1e3 * tg / K}
 
     if args.cpu_batches > 0:
         res["cpu_baseline"], res["parity"] = cpu_baseline(args, wl, csr, batches, fanouts, feats,
@@ -894,10 +939,15 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
     # the gather is the one kernel of the iteration bracketed alone by events
     # (in the fused form it runs inside the forward stage: no line)
     if not args.fused:
-        res["roofline"] = {"kernel": "k_gather", "bound": "hbm", "achieved": res["gather_GBps"],
-                           "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": res["gather_GBps"] / HBM_PEAK_GBPS,
-                           "traffic": None, "alg_bytes_per_launch": b_gather / K,
-                           "avg_launch_ms": stage["gather"] / K}
+        es = 2 if master is not None else 4
+        t_launch, b_launch = gather_launch_time(gmb, torch, csr, batches, fanouts, wl, cfg, feats,
+                                                lanes[0]["x"], K, es, dev)
+        res["roofline"] = {"kernel": "k_gather", "bound": "hbm", "achieved": b_launch / t_launch / 1e9,
+                           "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": b_launch / t_launch / 1e9 / HBM_PEAK_GBPS,
+                           "traffic": None, "alg_bytes_per_launch": b_launch, "avg_launch_ms": 1e3 * t_launch,
+                           "launches": f"the last {K} k_gather launches (pass G: {min(GATHER_SETS, nb)} batches "
+                                       "cycled, back to back on one stream)",
+                           "pass_b_event_bracket_ms": stage["gather"] / K}
     else:
         del res["gather_GBps"]   # no gather stage of its own
     if args.cpu_batches > 0:
