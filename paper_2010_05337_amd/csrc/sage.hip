@@ -685,10 +685,10 @@ void launch_slab_for(const int32_t* sizes, const float* hs, const float* ag, con
 // two 16-byte global reads per lane and chunk (d_in % 4 == 0, so a group of
 // four k lies in h_v or in the mean), and cut into parts one chunk ahead of
 // its products.  SPLIT = 1: wave w of WAVES owns R row fragments of 16 rows
-// (16 WAVES R rows per tile) and reuses each B fragment R times; SPLIT = 4
-// (layers with few rows, four waves): the waves share the tile's R
-// fragments, wave w takes the chunks c = w (mod 4), partial sums meet in
-// LDS.  Persistent over row tiles, the next tile's A reads issued as soon
+// (16 WAVES R rows per tile) and reuses each B fragment R times; SPLIT > 1
+// (layers with few rows): the waves share the tile's R fragments, wave w
+// takes the chunks c = w (mod WAVES), partial sums meet in LDS and are added
+// in wave order.  Persistent over row tiles, the next tile's A reads issued as soon
 // as each chunk is cut; loads are unconditional from clamped addresses as
 // in the fp32 slab kernel.
 __device__ __forceinline__ void split3(float x, uint32_t& p0, uint32_t& p1, uint32_t& p2) {
@@ -719,8 +719,8 @@ __device__ __forceinline__ void split8(const float4& lo, const float4& hi, bf16x
   for (int p = 0; p < 3; ++p) part[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
 }
 
-constexpr int parts_lds_bytes(int nch, int j, int r, int split) {
-  return 3 * nch * 4 * 16 * j * 8 * 2 + (split > 1 ? 4 * r * j * 64 * 16 : 16);
+constexpr int parts_lds_bytes(int nch, int j, int r, int split, int waves) {
+  return 3 * nch * 4 * 16 * j * 8 * 2 + (split > 1 ? waves * r * j * 64 * 16 : 16);
 }
 
 template <int NCH, int J, int R, int SPLIT, int WAVES>
@@ -729,15 +729,14 @@ void k_linear_f32_parts(const int32_t* sizes, const float* __restrict__ Hs, cons
                         const float* __restrict__ Ws, const float* __restrict__ Wn,
                         const float* __restrict__ bias, int K, int N, int relu, float* __restrict__ out) {
   constexpr int BN = 16 * J;
-  static_assert(SPLIT == 1 || WAVES == 4, "split K runs four waves");
   constexpr int THREADS = 64 * WAVES;
   constexpr int ROWS = SPLIT > 1 ? 16 * R : 16 * WAVES * R;
-  constexpr int MYCH = SPLIT > 1 ? (NCH + 3) / 4 : NCH;
+  constexpr int MYCH = SPLIT > 1 ? (NCH + WAVES - 1) / WAVES : NCH;
   constexpr int PLANE = NCH * 4 * BN * 8;   // uint16 per plane
   constexpr int ENTRIES = R * J * 64;       // split K: output entries of four rows per tile
-  constexpr int PER_THREAD = SPLIT > 1 ? (ENTRIES + 255) / 256 : 1;
+  constexpr int PER_THREAD = SPLIT > 1 ? (ENTRIES + THREADS - 1) / THREADS : 1;
   __shared__ __attribute__((aligned(16))) uint16_t Bp[3 * PLANE];
-  __shared__ __attribute__((aligned(16))) float Red[SPLIT > 1 ? 4 * ENTRIES * 4 : 4];
+  __shared__ __attribute__((aligned(16))) float Red[SPLIT > 1 ? WAVES * ENTRIES * 4 : 4];
   const int32_t M = load_size(&sizes[kNDst]);
   const int row_tiles = (M + ROWS - 1) / ROWS;
   if (static_cast<int>(blockIdx.x) >= row_tiles) return;
@@ -796,7 +795,7 @@ void k_linear_f32_parts(const int32_t* sizes, const float* __restrict__ Hs, cons
     const int kk = k >= K2 ? 0 : (k < K ? k : k - K);
     return *reinterpret_cast<const float4*>(pick((k >= K) & (k < K2), grow, hrow) + kk);
   };
-  auto chunk_of = [&](int i) { return SPLIT > 1 ? wave + 4 * i : i; };
+  auto chunk_of = [&](int i) { return SPLIT > 1 ? wave + WAVES * i : i; };
   float4 a[R][MYCH][2];
   const float* hr[R];
   const float* gr[R];
@@ -840,7 +839,7 @@ void k_linear_f32_parts(const int32_t* sizes, const float* __restrict__ Hs, cons
     if constexpr (SPLIT > 1) {
 #pragma unroll
       for (int u = 0; u < PER_THREAD; ++u) {
-        const int e = threadIdx.x + 256 * u;
+        const int e = threadIdx.x + THREADS * u;
         if (e < ENTRIES) {
           const int f = e / (J * 64), j = (e / 64) % J, l = e % 64;
           store4(frag_row0(held_rt, f) + 4 * (l >> 4), n0 + j * 16 + (l & 15), held[u][0], bv[j]);
@@ -961,8 +960,8 @@ void k_linear_f32_parts(const int32_t* sizes, const float* __restrict__ Hs, cons
       if (i == MYCH / 2) store_held();
     }
     if constexpr (SPLIT > 1) {
-      // partials of the four waves -> LDS; thread t then holds the entries
-      // e = t + 256 u, each the sum of the four partials
+      // partials of the waves -> LDS; thread t then holds the entries
+      // e = t + THREADS u, each the sum of the partials in wave order
 #pragma unroll
       for (int f = 0; f < R; ++f)
 #pragma unroll
@@ -971,11 +970,11 @@ void k_linear_f32_parts(const int32_t* sizes, const float* __restrict__ Hs, cons
       __syncthreads();
 #pragma unroll
       for (int u = 0; u < PER_THREAD; ++u) {
-        const int e = threadIdx.x + 256 * u;
+        const int e = threadIdx.x + THREADS * u;
         if (e < ENTRIES) {
           floatx4 sum = *reinterpret_cast<const floatx4*>(&Red[e * 4]);
 #pragma unroll
-          for (int w = 1; w < 4; ++w) sum += *reinterpret_cast<const floatx4*>(&Red[(w * ENTRIES + e) * 4]);
+          for (int w = 1; w < WAVES; ++w) sum += *reinterpret_cast<const floatx4*>(&Red[(w * ENTRIES + e) * 4]);
           held[u][0] = sum;
         }
       }
@@ -994,7 +993,7 @@ void k_linear_f32_parts(const int32_t* sizes, const float* __restrict__ Hs, cons
 template <int NCH, int J, int R, int SPLIT, int WAVES>
 void launch_parts(const int32_t* sizes, const float* hs, const float* ag, const float* ws, const float* wn,
                   const float* bias, int K, int N, int relu, float* out, int64_t cap_rows, hipStream_t s) {
-  static_assert(parts_lds_bytes(NCH, J, R, SPLIT) <= 160 * 1024, "slab exceeds the LDS");
+  static_assert(parts_lds_bytes(NCH, J, R, SPLIT, WAVES) <= 160 * 1024, "slab exceeds the LDS");
   constexpr int BN = 16 * J;
   constexpr int ROWS = SPLIT > 1 ? 16 * R : 16 * WAVES * R;
   const int col_tiles = (N + BN - 1) / BN;
@@ -1009,12 +1008,12 @@ void launch_parts(const int32_t* sizes, const float* hs, const float* ag, const 
 
 // Tiling of the part-product kernel, from timings of the three layer shapes
 // of the 3-layer model (39k x 200 -> 256, 4.6k x 512 -> 256, 1k x 512 -> 47):
-// layers with enough 128-row tiles to fill the chip twice run eight waves
-// per workgroup (two per SIMD, one slab: each wave's cutting of its A values
-// then runs beside the other wave's products, since one wave's VALU and
-// matrix-core instructions barely overlap) with 64-column slabs; smaller
-// layers split K over four waves, with 32 columns and two row fragments per
-// wave when there are enough rows, else 16 columns and one.  Returns false
+// eight waves per workgroup (two per SIMD, one slab: each wave's cutting of
+// its A values then runs beside the other wave's products, since one wave's
+// VALU and matrix-core instructions barely overlap).  Layers with enough
+// 128-row tiles to fill the chip twice give each wave its own 16 rows of a
+// 64-column slab; smaller layers split K over the eight waves, on 16-row
+// tiles of 32 columns when there are enough rows, else 16.  Returns false
 // where the fp32 slab kernel is the faster choice (wide K on many rows:
 // the eight-wave tiling would not fit its registers).
 template <int NCH>
@@ -1030,9 +1029,9 @@ bool launch_parts_for(const int32_t* sizes, const float* hs, const float* ag, co
     return false;
   }
   if (cap_rows * N > (int64_t{1} << 18))
-    launch_parts<NCH, 2, 2, 4, 4>(sizes, hs, ag, ws, wn, bias, K, N, relu, out, cap_rows, s);
+    launch_parts<NCH, 2, 1, 4, 8>(sizes, hs, ag, ws, wn, bias, K, N, relu, out, cap_rows, s);
   else
-    launch_parts<NCH, 1, 1, 4, 4>(sizes, hs, ag, ws, wn, bias, K, N, relu, out, cap_rows, s);
+    launch_parts<NCH, 1, 1, 4, 8>(sizes, hs, ag, ws, wn, bias, K, N, relu, out, cap_rows, s);
   return true;
 }
 

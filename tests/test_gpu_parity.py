@@ -264,10 +264,10 @@ def test_forward_wide_model_f32(orc, dg):
     w = dg.sage_weights([100, 256, 256, 47], 23)
     seeds = dg.permutation(30000, 24)[:256]
     errs = _forward_case(orc, dg, g, feats, w, seeds, [15, 10, 5], 25, TOL_F32)
-    # the three layers take the three tilings of the part-product linear
-    # (eight waves on the 64-column slab; split K with two row fragments;
-    # split K on 16 columns): fp32-level accuracy, well inside the tolerance
-    # (about 1e-6 measured; a dropped part product would show as 1e-5 or more)
+    # the layers take the split-K tilings of the part-product linear (32
+    # columns on layer 0, 16 on the smaller two): fp32-level accuracy, well
+    # inside the tolerance (about 1e-6 measured; a dropped part product would
+    # show as 1e-5 or more)
     assert max(errs) <= 5e-6, errs
 
 
