@@ -29,6 +29,7 @@ rocprofv3 output of runs of this script into the tables kept in profiles/.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -138,6 +139,16 @@ def alg_sample_bytes(sizes, wide: bool) -> int:
     for n_dst, n_src, nnz in sizes:
         total += 4 * n_dst + 2 * w * n_dst + 4 * nnz + 4 * (n_dst + 1) + 4 * nnz + 4 * n_src
     return total
+
+
+def quiet_gc() -> None:
+    """The timed passes run with Python's cyclic garbage collector off and
+    the objects made so far frozen out of its scans: a full collection over
+    the generated workload's objects takes tens of milliseconds, and one
+    landing inside a single-run timed loop inflated it several times over."""
+    gc.collect()
+    gc.freeze()
+    gc.disable()
 
 
 def alg_gather_bytes(n_in: int, dim: int, es: int) -> int:
@@ -548,6 +559,7 @@ def main():
                 ev[3].record(st)
         return blocks
 
+    quiet_gc()
     for i in range(args.warmup):
         step(i, S)
     torch.cuda.synchronize()
@@ -715,7 +727,11 @@ def main():
     res["stream_copy_GBps"] = copy_GBps
     peak = BF16_MFMA_PEAK_TFLOPS if bf16 else FP32_MFMA_PEAK_TFLOPS
     res["forward"] = {"alg_bytes": b_fwd, "linear_flops": flops,
-                      "linear_TFLOPs_lower_bound": flops / tf / 1e12, "mfma_peak_TFLOPs": peak}
+                      "linear_TFLOPs_lower_bound": flops / tf / 1e12, "mfma_peak_TFLOPs": peak,
+                      "linear_arithmetic": ("bf16 operands, v_mfma_f32_16x16x32_bf16, fp32 accumulation" if bf16 else
+                                            "fp32 operands cut exactly into three bf16 parts, six part products "
+                                            "per fp32 product on v_mfma_f32_16x16x32_bf16, fp32 accumulation "
+                                            "(K = 2 d_in <= 512; wider layers on many rows: v_mfma_f32_16x16x4_f32)")}
     res["gemm_check"] = gemm_check(torch, dev)
     res["fused_forward"] = {"seeds_per_s": seeds_total / T3, "ms_per_step": 1e3 * T3 / K,
                             "runs_seeds_per_s": [seeds_total / t for t in runs_d], "streams": S,
@@ -841,6 +857,7 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         model(blocks, x, b, i)
         ln["done"].record(comp)
 
+    quiet_gc()
     for i in range(W):
         step(i)
     torch.cuda.synchronize()
