@@ -40,6 +40,7 @@
 
 #include "common.hpp"
 #include "kernels.hpp"
+#include "parts.hpp"
 #include "scan.hpp"
 
 namespace gmb {
@@ -527,6 +528,53 @@ __global__ __launch_bounds__(256) void k_dgrad(const int32_t* __restrict__ sizes
                      (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x,
                      static_cast<int64_t>(gridDim.x) * gridDim.y * blockDim.x,
                      [&](int64_t, int32_t u, int32_t) { atomicAdd(&cnt[u], 1); });
+}
+
+// The same product on the bf16 matrix cores through the exact three-way
+// cut of the operands (parts.hpp), for d_out % 4 == 0 and d_out <= 512: A =
+// dZ, B = the weights' transpose in the slab; then the in-edge count, as
+// above.  The workgroups past the product's row tiles go straight to the
+// count.
+template <int NCH, int J, int R, int SPLIT, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(WAVES / 4, WAVES / 4)))
+void k_dgrad_parts(const int32_t* __restrict__ sizes, parts::DgradOp op, EdgeView ev, int32_t* __restrict__ cnt) {
+  const int32_t M = load_size(&sizes[kNDst]);
+  parts::parts_gemm<parts::DgradOp, NCH, J, R, SPLIT, WAVES>(op, M);
+  for_each_edge_slot(ev, M, load_size(&sizes[kNSrc]),
+                     (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x,
+                     static_cast<int64_t>(gridDim.x) * gridDim.y * blockDim.x,
+                     [&](int64_t, int32_t u, int32_t) { atomicAdd(&cnt[u], 1); });
+}
+
+template <int NCH, int J, int R, int SPLIT, int WAVES>
+void launch_dgrad_parts(const int32_t* sizes, const parts::DgradOp& op, int64_t cap_rows, const EdgeView& ev,
+                        int32_t* cnt, hipStream_t s) {
+  static_assert(parts::parts_lds_bytes(NCH, J, R, SPLIT, WAVES) <= 160 * 1024, "slab exceeds the LDS");
+  hipLaunchKernelGGL((k_dgrad_parts<NCH, J, R, SPLIT, WAVES>), (parts::parts_grid<J, R, SPLIT, WAVES>(cap_rows, op.n())),
+                     dim3(64 * WAVES), 0, s, sizes, op, ev, cnt);
+}
+
+// Tiling as the forward's part-product launches: eight waves per
+// workgroup; many rows: a wave's own 16 rows of a 64-column slab (K up to
+// 256); fewer: split K over the eight waves.  False where the shape has no
+// part-product tiling (the fp32-instruction kernel takes it).
+template <int NCH>
+bool dgrad_parts_for(const int32_t* sizes, const parts::DgradOp& op, int64_t cap_rows, const EdgeView& ev,
+                     int32_t* cnt, hipStream_t s) {
+  const int N = op.n();
+  const int64_t big_tiles = ((cap_rows + 127) / 128) * ((N + 63) / 64);
+  if (big_tiles >= 2 * 256) {
+    if constexpr (NCH <= 8) {
+      launch_dgrad_parts<NCH, 4, 1, 1, 8>(sizes, op, cap_rows, ev, cnt, s);
+      return true;
+    }
+    return false;
+  }
+  if (cap_rows * N > (int64_t{1} << 18))
+    launch_dgrad_parts<NCH, 2, 1, 4, 8>(sizes, op, cap_rows, ev, cnt, s);
+  else
+    launch_dgrad_parts<NCH, 1, 1, 4, 8>(sizes, op, cap_rows, ev, cnt, s);
+  return true;
 }
 
 // ---- mean backward: the block's transpose -----------------------------------
@@ -1046,6 +1094,21 @@ hipError_t launch_dgrad(const int32_t* sizes, const float* dZ, int ldz, int d_ou
                         const float* wn, int d_in, float* dH, float* dM, int64_t cap_rows,
                         const int32_t* indptr, const int32_t* local, int64_t cap_nnz, int32_t fanout, int32_t* cnt,
                         hipStream_t s) {
+  const EdgeView ev0{indptr, local, cap_nnz, fanout};
+  const uintptr_t align = reinterpret_cast<uintptr_t>(dZ) | reinterpret_cast<uintptr_t>(ws) |
+                          reinterpret_cast<uintptr_t>(wn);
+  const int nch32 = (d_out + 31) / 32;
+  if (d_out % 4 == 0 && ldz % 4 == 0 && align % 16 == 0 && nch32 <= 16) {
+    const parts::DgradOp op{dZ, ws, wn, ldz, d_out, d_in, dH, dM};
+    bool done;
+#define GMB_DPARTS(C) done = dgrad_parts_for<C>(sizes, op, cap_rows, ev0, cnt, s)
+    if (nch32 <= 2) GMB_DPARTS(2);
+    else if (nch32 <= 4) GMB_DPARTS(4);
+    else if (nch32 <= 8) GMB_DPARTS(8);
+    else GMB_DPARTS(16);
+#undef GMB_DPARTS
+    if (done) return hipGetLastError();
+  }
   const int nch = (d_out + 15) / 16;
   const int col_tiles = (2 * d_in + 63) / 64;
   int64_t rows = (cap_rows + 63) / 64;
