@@ -46,7 +46,8 @@
 //                 contiguous range of edges), samples them as above and
 //                 writes its edges and its destinations, grouped by owner,
 //                 into its own region of the pair array, with the group
-//                 offsets (fan-outs above 64: k_sample_wide, then k_route)
+//                 offsets (fan-outs above 64: k_sample_wide_wave, a wave
+//                 per destination, or k_sample_wide above 256, then k_route)
 //   k_owner(h)    one workgroup per owner: gathers its pairs from every
 //                 router's region, dedups them in an LDS hash table and
 //                 writes each edge's answer (known local id, first
@@ -338,7 +339,89 @@ __global__ __launch_bounds__(256) void k_sample_table(CsrArgs ga, const int32_t*
   if (seed_old < kEdgeTag) raise_status(status, GMB_STATUS_EDUP);
 }
 
-// Fan-outs above 64: one thread per destination; the block's output row
+// Fan-outs from 65 to 64 I: one wave per destination (grid-stride), I
+// draws per lane (draw q on lane q % 64, slot q / 64).  Floyd's rule is
+// resolved in draw order: draw q keeps its value unless a draw r < q holds
+// it (one ballot over the values held so far), else it takes j_q = d - f + q;
+// each value's rank (the count of smaller values) is its place in the row,
+// which is so written in slot order.  The same draws and the same rule as
+// the one-thread form below, hence the same rows.  The deferred local ids
+// of the previous hop are copied by the grid's threads (grid-stride).
+template <int I>
+__global__ __launch_bounds__(256) void k_sample_wide_wave(CsrArgs ga, const int32_t* ids, const int32_t* sizes,
+                                                          const int32_t* blk_indptr, int32_t* nbr, uint32_t* status,
+                                                          int fanout, int layer, uint32_t k0, uint32_t k1,
+                                                          int check_seeds, DeferredArgs fix) {
+  const CsrView g = view(ga);
+  const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t nthreads = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t e = gid; e < fix.cap; e += nthreads) {
+    DeferredItem it = deferred_read(fix, e);
+    deferred_fetch(fix, it);
+    deferred_store(fix, e, it);
+  }
+  const int32_t n_dst = load_size(&sizes[kNDst]);
+  const int lane = threadIdx.x & 63;
+  const uint32_t f = static_cast<uint32_t>(fanout);
+  for (int64_t p = gid / 64; p < n_dst; p += nthreads / 64) {   // uniform per wave
+    const int32_t v = ids[p];
+    if (!valid_vertex(v, g.num_nodes)) {
+      if (check_seeds && lane == 0) raise_status(status, GMB_STATUS_ERANGE);
+      continue;
+    }
+    int64_t begin, end;
+    row_range(g, v, begin, end);
+    const int64_t d = end - begin;
+    const int32_t off = blk_indptr[p];
+    if (d <= fanout) {
+      for (int64_t s = lane; s < d; s += 64)
+        emit_edge(off + static_cast<int32_t>(s), g.indices[begin + s], nbr, g.num_nodes, status);
+      continue;
+    }
+    const uint32_t base = static_cast<uint32_t>(d - fanout);
+    uint32_t t[I], x[I];
+#pragma unroll
+    for (int i = 0; i < I; ++i) {
+      const uint32_t q = static_cast<uint32_t>(lane + 64 * i);
+      t[i] = q < f ? draw_below(k0, k1, static_cast<uint32_t>(v), static_cast<uint32_t>(layer), q, base + q + 1) : 0u;
+      x[i] = t[i];
+    }
+    for (uint32_t q = 1; q < f; ++q) {
+      const int qi = static_cast<int>(q >> 6), ql = static_cast<int>(q & 63);
+      uint32_t mine = t[0];
+#pragma unroll
+      for (int i = 1; i < I; ++i) mine = i == qi ? t[i] : mine;
+      const uint32_t tq = __shfl(mine, ql, 64);
+      bool hit = false;
+#pragma unroll
+      for (int i = 0; i < I; ++i) hit |= (static_cast<uint32_t>(lane + 64 * i) < q) & (x[i] == tq);
+      if (__ballot(hit) != 0 && lane == ql) {   // the ballot is uniform
+#pragma unroll
+        for (int i = 0; i < I; ++i)
+          if (i == qi) x[i] = base + q;
+      }
+    }
+    uint32_t rank[I];
+#pragma unroll
+    for (int i = 0; i < I; ++i) rank[i] = 0;
+    for (uint32_t q = 0; q < f; ++q) {
+      const int qi = static_cast<int>(q >> 6), ql = static_cast<int>(q & 63);
+      uint32_t mine = x[0];
+#pragma unroll
+      for (int i = 1; i < I; ++i) mine = i == qi ? x[i] : mine;
+      const uint32_t xq = __shfl(mine, ql, 64);
+#pragma unroll
+      for (int i = 0; i < I; ++i) rank[i] += xq < x[i] ? 1u : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < I; ++i) {
+      const uint32_t q = static_cast<uint32_t>(lane + 64 * i);
+      if (q < f) emit_edge(off + static_cast<int32_t>(rank[i]), g.indices[begin + x[i]], nbr, g.num_nodes, status);
+    }
+  }
+}
+
+// Fan-outs above 64 I_max (256): one thread per destination; the block's output row
 // holds the chosen slots while Floyd runs, is sorted in place, then mapped
 // to vertex ids.
 __global__ __launch_bounds__(256) void k_sample_wide(CsrArgs ga, const int32_t* ids, const int32_t* sizes,
@@ -1252,6 +1335,19 @@ hipError_t launch_assign(const AssignArgs& a, int num_values, const CsrArgs& g, 
 
 hipError_t launch_sample(const CsrArgs& g, const int32_t* ids, const HopArgs& h, uint32_t* status, uint32_t k0,
                          uint32_t k1, int first_hop, const DeferredArgs& fix, hipStream_t s) {
+  if (h.fanout <= 256) {
+    // a wave per destination (grid-stride over the destinations and the
+    // deferred ids, at most 16384 workgroups)
+    const int64_t threads = std::max<int64_t>(64 * std::max<int64_t>(h.cap_dst, 1), fix.cap);
+    const unsigned grid = std::min<unsigned>(grid_for(threads), 16384u);
+    if (h.fanout <= 128)
+      hipLaunchKernelGGL(k_sample_wide_wave<2>, dim3(grid), dim3(256), 0, s, g, ids, h.sizes, h.indptr, h.nbr,
+                         status, h.fanout, h.layer, k0, k1, first_hop, fix);
+    else
+      hipLaunchKernelGGL(k_sample_wide_wave<4>, dim3(grid), dim3(256), 0, s, g, ids, h.sizes, h.indptr, h.nbr,
+                         status, h.fanout, h.layer, k0, k1, first_hop, fix);
+    return hipGetLastError();
+  }
   auto threads = std::max(h.cap_dst, fix.cap);
   hipLaunchKernelGGL(k_sample_wide, dim3(grid_for(threads)), dim3(256), 0, s, g, ids, h.sizes, h.indptr, h.nbr,
                      status, h.fanout, h.layer, k0, k1, first_hop, fix);

@@ -86,8 +86,9 @@ def test_sampling_rmat_hubs_bitexact(orc, dg, wide):
 
 
 def test_sampling_wide_fanouts_on_hubs(orc, dg):
-    """Fan-outs above 64 (the one-thread-per-destination sampler, whose
-    slots are sorted in place) on rows far longer than the fan-out, and a
+    """Fan-outs above 64 on rows far longer than the fan-out: 65 to 128 (a
+    wave per destination, two draws per lane), 129 to 256 (four per lane),
+    above 256 (one thread per destination, slots sorted in place), and a
     fan-out of exactly 64 (the widest lane group)."""
     g = dg.rmat(14, 16000, 240000, (0.57, 0.19, 0.19), 17)
     g = dg.inject_hubs(g, 4, 5000, 18)
@@ -95,7 +96,8 @@ def test_sampling_wide_fanouts_on_hubs(orc, dg):
     seeds = np.concatenate([g.hubs, dg.permutation(16000, 19)[:400]]).astype(np.int64)
     seeds = seeds[np.sort(np.unique(seeds, return_index=True)[1])]
     deg = g.degrees()
-    for fo, key in [([100], 21), ([70, 3], 22), ([64], 23)]:
+    for fo, key in [([100], 21), ([70, 3], 22), ([64], 23), ([128], 24), ([129], 25), ([200], 26),
+                    ([256], 27), ([300], 28), ([65, 2], 29)]:
         _, host = gpu_blocks(csr, seeds, fo, key)
         ref = orc.sample_blocks(g.indptr, g.indices, seeds, fo, key)
         assert_blocks_equal(host, ref, f"fanouts {fo}")
