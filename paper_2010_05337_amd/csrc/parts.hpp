@@ -191,7 +191,7 @@ __device__ __forceinline__ void parts_gemm(const Op& op, int32_t M) {
   const int row_tiles = (M + ROWS - 1) / ROWS;
   if (static_cast<int>(blockIdx.x) >= row_tiles) return;
   const int n0 = blockIdx.y * BN;
-  const int K2 = op.k2(), N = op.n();
+  const int N = op.n();
   // slab fill: item (c, q, n) reads B[32c + 8q .. +7][n0 + n] (the
   // policy's eight loads), cuts them into parts and writes one 16-byte word
   // per plane; a thread issues the loads of all its items before the first

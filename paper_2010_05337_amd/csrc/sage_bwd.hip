@@ -599,7 +599,7 @@ constexpr int kLongList = 16;   // transpose lists longer than this take a workg
 #define GMB_PULL_UPDATE_R 4
 #endif
 #ifndef GMB_PULL_UPDATE_E
-#define GMB_PULL_UPDATE_E 2
+#define GMB_PULL_UPDATE_E 1
 #endif
 
 // WG = 0: the scan alone (its own small register and LDS footprint);
@@ -833,22 +833,25 @@ __global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ s
     // the layer below's output does not depend on the gradient: read first
     const float4 o = *reinterpret_cast<const float4*>(out + at);
     float4 acc = self ? *reinterpret_cast<const float4*>(dH + at) : make_float4(0.f, 0.f, 0.f, 0.f);
-    int32_t s = s0;
-    for (; s + 1 < s1; s += 2) {
-      const int2 e0 = csc[s], e1 = csc[s + 1];
-      const bool ok0 = e0.x >= 0 && e0.x < n_dst, ok1 = e1.x >= 0 && e1.x < n_dst;
-      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
-      const float4 g1 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok1 ? e1.x : 0) * d + 4 * c);
-      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f, w1 = ok1 ? __int_as_float(e1.y) : 0.f;
-      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
-      acc.x += w1 * g1.x; acc.y += w1 * g1.y; acc.z += w1 * g1.z; acc.w += w1 * g1.w;
-    }
-    if (s < s1) {
-      const int2 e0 = csc[s];
-      const bool ok0 = e0.x >= 0 && e0.x < n_dst;
-      const float4 g0 = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok0 ? e0.x : 0) * d + 4 * c);
-      const float w0 = ok0 ? __int_as_float(e0.y) : 0.f;
-      acc.x += w0 * g0.x; acc.y += w0 * g0.y; acc.z += w0 * g0.z; acc.w += w0 * g0.w;
+    // four entries per round of reads (the sum still runs in entry order)
+    for (int32_t s = s0; s < s1; s += 4) {
+      int2 x[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = s + q < s1 ? csc[s + q] : make_int2(-1, 0);
+      float4 g[4];
+      float w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool ok = x[q].x >= 0 && x[q].x < n_dst;
+        w[q] = ok ? __int_as_float(x[q].y) : 0.f;
+        g[q] = ok ? *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(x[q].x) * d + 4 * c)
+                  : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (s + q >= s1) break;
+        acc.x += w[q] * g[q].x; acc.y += w[q] * g[q].y; acc.z += w[q] * g[q].z; acc.w += w[q] * g[q].w;
+      }
     }
     acc.x = o.x > 0.f ? acc.x : 0.f;
     acc.y = o.y > 0.f ? acc.y : 0.f;
@@ -948,15 +951,29 @@ __global__ __launch_bounds__(256) void k_pull_update(const int32_t* __restrict__
         acc[r].z += w[r][j] * g[r][j].z;
         acc[r].w += w[r][j] * g[r][j].w;
       }
-    // the rest of the longer lists
+    // the rest of the longer lists, four entries per round of reads (the
+    // sum still runs in entry order)
 #pragma unroll
     for (int r = 0; r < R; ++r)
-      for (int32_t j = E; j < cnt[r]; ++j) {
-        const int2 x = csc[s0[r] + j];
-        const bool ok = x.x >= 0 && x.x < n_dst;
-        const float4 gx = *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(ok ? x.x : 0) * d + 4 * c);
-        const float wx = ok ? __int_as_float(x.y) : 0.f;
-        acc[r].x += wx * gx.x; acc[r].y += wx * gx.y; acc[r].z += wx * gx.z; acc[r].w += wx * gx.w;
+      for (int32_t j = E; j < cnt[r]; j += 4) {
+        int2 x[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) x[q] = j + q < cnt[r] ? csc[s0[r] + j + q] : make_int2(-1, 0);
+        float4 gx[4];
+        float wx[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const bool ok = x[q].x >= 0 && x[q].x < n_dst;
+          wx[q] = ok ? __int_as_float(x[q].y) : 0.f;
+          gx[q] = ok ? *reinterpret_cast<const float4*>(dM + static_cast<int64_t>(x[q].x) * d + 4 * c)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (j + q >= cnt[r]) break;
+          acc[r].x += wx[q] * gx[q].x; acc[r].y += wx[q] * gx[q].y;
+          acc[r].z += wx[q] * gx[q].z; acc[r].w += wx[q] * gx[q].w;
+        }
       }
     if (c0 >= chunks) continue;
 #pragma unroll
