@@ -5,19 +5,23 @@
 //   k_xent         softmax cross-entropy per target row (one wave per row):
 //                  dZ = (softmax(z) - e_y) / B, and the row's loss term; also
 //                  clears the per-source edge counters of the transposes
-//   k_wgrad        [dW_self; dW_neigh] = [H | M]^T dZ and db = sum of dZ rows:
-//                  v_mfma_f32_16x16x4_f32 with the rows of the block as the
+//   k_wgrad_parts  [dW_self; dW_neigh] = [H | M]^T dZ and db = sum of dZ rows
+//                  on the bf16 matrix cores through the exact three-way cut
+//                  of the operands (parts.hpp), the rows of the block as the
 //                  reduction dimension; a workgroup owns a 64 x 64 tile of
-//                  the output and a range of rows, its four waves split the
-//                  rows and are summed through LDS, and every workgroup
-//                  writes its partial sums (no atomics: the same result on
-//                  every run)
+//                  the output and a range of rows, its eight waves (two per
+//                  SIMD) split the rows and are summed through LDS, and every
+//                  workgroup writes its partial sums (no atomics: the same
+//                  result on every run).  The same products in fp32
+//                  (v_mfma_f32_16x16x4_f32, wgrad_block) ride in the
+//                  transpose scan's launch on the layers with an input
+//                  gradient
 //   k_wgrad_reduce sums the partials in a fixed order into the gradients;
 //                  on the last layer one more workgroup sums the loss terms
 //                  into the mean loss (fixed order).  On a layer whose input
 //                  gradient runs, the reduction's workgroups ride at the end
 //                  of that layer's k_csc_fill grid, and (for a small scan)
-//                  k_wgrad's at the end of its k_csc_scan grid, instead of
+//                  the products' at the end of its k_csc_scan grid, instead of
 //                  launches of their own (the input gradient then goes
 //                  first)
 //   k_dgrad        [dH_self | dM] = dZ [W_self; W_neigh]^T: the weights'
@@ -279,12 +283,201 @@ __device__ __forceinline__ void wgrad_block(const int32_t* __restrict__ sizes, c
   }
 }
 
-template <bool VEC>
-__global__ __launch_bounds__(256)
-__attribute__((amdgpu_waves_per_eu(kWgradDepth <= 4 ? 2 : 1, kWgradDepth <= 4 ? 2 : 1)))
-void k_wgrad(const int32_t* __restrict__ sizes, const float* __restrict__ H, const float* __restrict__ M, int d_in,
-             const float* __restrict__ dZ, int ldz, int ldp, float* __restrict__ partial) {
-  wgrad_block<VEC>(sizes, H, M, d_in, dZ, ldz, ldp, partial, blockIdx.x, blockIdx.y, blockIdx.z, gridDim.x);
+// The same gradient on the bf16 matrix cores through the exact three-way
+// cut of the operands (parts.hpp: six part products, fp32 accumulation),
+// for the layers whose weight gradient has a launch of its own: the same
+// workgroups (p, y, z), 64 x 64 tiles, row ranges, partials and reduction
+// as above.  The block rows are the reduction dimension: per 32-row chunk,
+// lane (g, i) = (l / 16, l % 16) supplies A[i][8g .. +7] = X[row 8g .. +7]
+// [64 z' + 16 b + i] and B[8g .. +7][i] = dZ[row 8g .. +7][64 y + 16 b' + i]
+// of v_mfma_f32_16x16x32_bf16 for the four column blocks b, b' of the tile
+// (eight 4-byte loads per column: the sixteen lanes of a row read 64
+// consecutive bytes), cuts them in registers and holds C[4g + r][i] of the
+// 4 x 4 blocks.  Wave w of W takes the chunks w, w + W, ... of the range;
+// rows past the range read its last row and their dZ is zeroed (also in
+// the bias sums); columns past the arrays read column 0 and feed only
+// outputs that are never written.  The W waves' tiles meet in LDS and are
+// added in wave order.  The cut costs about as many VALU issue cycles as
+// the products take on the matrix core, and a wave does not overlap the
+// two by itself: two waves per SIMD (W = 8, the loads of a chunk issued
+// just before its products) measured 35 us on the 100 -> 256 layer of a
+// 39k-row block, against 46 us for four waves with the next chunk's loads
+// in flight (depth 2; depth 3 and 4: 50 us) and 47 us for the fp32 products.
+#ifndef GMB_WGRAD_PARTS_DEPTH
+#define GMB_WGRAD_PARTS_DEPTH 1
+#endif
+#ifndef GMB_WGRAD_PARTS_WAVES
+#define GMB_WGRAD_PARTS_WAVES 8
+#endif
+constexpr int kWgradPartsDepth = GMB_WGRAD_PARTS_DEPTH;   // chunks in flight per wave
+constexpr int kWgradPartsWaves = GMB_WGRAD_PARTS_WAVES;   // waves per workgroup, two per SIMD at 8
+
+__global__ __launch_bounds__(64 * kWgradPartsWaves)
+__attribute__((amdgpu_waves_per_eu(kWgradPartsWaves / 4, kWgradPartsWaves / 4)))
+void k_wgrad_parts(const int32_t* __restrict__ sizes, const float* __restrict__ H, const float* __restrict__ M,
+                   int d_in, const float* __restrict__ dZ, int ldz, int ldp, float* __restrict__ partial) {
+  using parts::bf16x8;
+  constexpr int W = kWgradPartsWaves;
+  constexpr int kPad = 68;   // LDS row stride of the waves' tiles
+  __shared__ __attribute__((aligned(16))) float red[W][64 * kPad];
+  __shared__ float red_db[W][64];
+  const int32_t n = load_size(&sizes[kNDst]);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, li = lane & 15;
+  const int p = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  const int K2 = 2 * d_in;
+  const int TI = (d_in + 63) / 64;
+  const bool from_m = bz >= TI;
+  const int zc = from_m ? bz - TI : bz;
+  const char* X = reinterpret_cast<const char*>(from_m ? M : H);   // uniform per workgroup
+  const char* Zb = reinterpret_cast<const char*>(dZ);
+  const uint32_t xrow = static_cast<uint32_t>(d_in) * 4u, zrow = static_cast<uint32_t>(ldz) * 4u;
+  uint32_t xo[4], zo[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int c = zc * 64 + 16 * b + li, o = by * 64 + 16 * b + li;
+    xo[b] = static_cast<uint32_t>(c < d_in ? c : 0) * 4u;
+    zo[b] = static_cast<uint32_t>(o < ldz ? o : 0) * 4u;
+  }
+  const int gx = gridDim.x;
+  const int rows_per_part = ((n + gx - 1) / gx + 15) / 16 * 16;
+  const int r0 = min(p * rows_per_part, n);
+  const int r1 = min(r0 + rows_per_part, n);
+  floatx4 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float dbs[4] = {0.f, 0.f, 0.f, 0.f};
+
+  auto load = [&](int k0, float (&xa)[4][8], float (&zb)[4][8]) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int row = k0 + 8 * g + e;
+      const uint32_t rc = static_cast<uint32_t>(row < r1 ? row : r1 - 1);
+      const uint32_t xr = rc * xrow, zr = rc * zrow;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        xa[b][e] = *reinterpret_cast<const float*>(X + (xr + xo[b]));
+        zb[b][e] = *reinterpret_cast<const float*>(Zb + (zr + zo[b]));
+      }
+    }
+  };
+  auto compute = [&](int k0, float (&xa)[4][8], float (&zb)[4][8]) {
+    if (k0 + 32 > r1) {   // uniform: the range's last chunk of this wave
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (k0 + 8 * g + e >= r1) {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) zb[b][e] = 0.f;
+        }
+    }
+    if (bz == 0) {   // uniform: the bias sums ride on the first column tile
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dbs[b] += zb[b][e];
+    }
+    bf16x8 bp[4][3];
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      parts::split8(make_float4(zb[b][0], zb[b][1], zb[b][2], zb[b][3]),
+                    make_float4(zb[b][4], zb[b][5], zb[b][6], zb[b][7]), bp[b]);
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      bf16x8 ap[3];
+      parts::split8(make_float4(xa[a][0], xa[a][1], xa[a][2], xa[a][3]),
+                    make_float4(xa[a][4], xa[a][5], xa[a][6], xa[a][7]), ap);
+      // the smallest part products first
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap[0], bp[b][2], acc[a][b], 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap[1], bp[b][1], acc[a][b], 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap[2], bp[b][0], acc[a][b], 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap[0], bp[b][1], acc[a][b], 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap[1], bp[b][0], acc[a][b], 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap[0], bp[b][0], acc[a][b], 0, 0, 0);
+    }
+  };
+
+  // loads run D - 1 chunks ahead of the products; the body is unrolled D
+  // times so that every buffer keeps its registers, the chunk count is
+  // rounded up to a multiple of D and a chunk past the range adds zero
+  constexpr int D = kWgradPartsDepth, STRIDE = 32 * W;
+  int k0 = r0 + 32 * wave;
+  const int nsteps = __builtin_amdgcn_readfirstlane(k0 < r1 ? (r1 - k0 + STRIDE - 1) / STRIDE : 0);
+  float xs[D][4][8], zs[D][4][8];
+  if (nsteps > 0) {
+#pragma unroll
+    for (int b = 0; b + 1 < D; ++b) load(k0 + STRIDE * b, xs[b], zs[b]);
+  }
+  for (int it = 0; it < nsteps; it += D) {
+#pragma unroll
+    for (int b = 0; b < D; ++b) {
+      load(k0 + STRIDE * (b + D - 1), xs[(b + D - 1) % D], zs[(b + D - 1) % D]);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(k0 + STRIDE * b, xs[b], zs[b]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    k0 += STRIDE * D;
+  }
+  // the bias sums over the lane's rows, then over g
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    dbs[b] += __shfl_xor(dbs[b], 16, 64);
+    dbs[b] += __shfl_xor(dbs[b], 32, 64);
+  }
+  float* mine = red[wave];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mine[(16 * a + 4 * g + r) * kPad + 16 * b + li] = acc[a][b][r];
+  if (g == 0) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) red_db[wave][16 * b + li] = dbs[b];
+  }
+  __syncthreads();
+  // thread t of the 64 W: tile row t / W, the 64 / W columns from
+  // (64 / W) (t % W); the waves' sums added in wave order
+  constexpr int kPer = 64 / W;
+  float* part = partial + static_cast<int64_t>(p) * (K2 + 1) * ldp;
+  const int m = threadIdx.x / W, n0 = kPer * (threadIdx.x % W);
+  const int c = zc * 64 + m;
+  if (c < d_in) {
+    float* dst = part + static_cast<int64_t>(from_m ? d_in + c : c) * ldp;
+#pragma unroll
+    for (int s4 = 0; s4 < kPer / 4; ++s4) {
+      const int o = by * 64 + n0 + 4 * s4;
+      if (o >= ldp) break;
+      float4 v = *reinterpret_cast<const float4*>(&red[0][m * kPad + n0 + 4 * s4]);
+#pragma unroll
+      for (int w = 1; w < W; ++w) {
+        const float4 x = *reinterpret_cast<const float4*>(&red[w][m * kPad + n0 + 4 * s4]);
+        v.x += x.x; v.y += x.y; v.z += x.z; v.w += x.w;
+      }
+      *reinterpret_cast<float4*>(dst + o) = v;
+    }
+  }
+  if (bz == 0 && threadIdx.x < 16) {
+    const int o = by * 64 + 4 * threadIdx.x;
+    if (o < ldp) {
+      float v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int cc = 4 * threadIdx.x + j;
+        v[j] = red_db[0][cc];
+#pragma unroll
+        for (int w = 1; w < W; ++w) v[j] += red_db[w][cc];
+      }
+      *reinterpret_cast<float4*>(part + static_cast<int64_t>(K2) * ldp + o) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  }
 }
 
 // One float4 of output per thread group of four: group g sums the parts
@@ -1095,10 +1288,9 @@ hipError_t launch_wgrad(const int32_t* sizes, const float* H, const float* M, in
   if (defer) {
     *defer = WgradArgs{sizes, H, M, d_in, dZ, ldz, ldp, partial, parts, static_cast<int>(grid.y),
                        static_cast<int>(grid.z), vec ? 1 : 0};
-  } else if (vec) {
-    hipLaunchKernelGGL(k_wgrad<true>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
   } else {
-    hipLaunchKernelGGL(k_wgrad<false>, grid, dim3(256), 0, s, sizes, H, M, d_in, dZ, ldz, ldp, partial);
+    hipLaunchKernelGGL(k_wgrad_parts, grid, dim3(64 * kWgradPartsWaves), 0, s, sizes, H, M, d_in, dZ, ldz, ldp,
+                       partial);
   }
   if (fold)
     *fold = r;
