@@ -763,9 +763,14 @@ bool dgrad_parts_for(const int32_t* sizes, const parts::DgradOp& op, int64_t cap
     }
     return false;
   }
-  if (cap_rows * N > (int64_t{1} << 18))
-    launch_dgrad_parts<NCH, 2, 1, 4, 8>(sizes, op, cap_rows, ev, cnt, s);
-  else
+  if (cap_rows * N > (int64_t{1} << 18)) {
+    // 64 columns a workgroup where the slab allows it: twice the workgroups
+    // per column tile, half the row tiles each walks
+    if constexpr (NCH <= 8)
+      launch_dgrad_parts<NCH, 4, 1, 4, 8>(sizes, op, cap_rows, ev, cnt, s);
+    else
+      launch_dgrad_parts<NCH, 2, 1, 4, 8>(sizes, op, cap_rows, ev, cnt, s);
+  } else
     launch_dgrad_parts<NCH, 1, 1, 4, 8>(sizes, op, cap_rows, ev, cnt, s);
   return true;
 }
