@@ -827,11 +827,12 @@ int check_grads(const gmb_sage_grads* g, const gmb_sage_weights* w) {
   return GMB_OK;
 }
 
-// Transpose scans of at most this many tiles take the weight gradient's
-// products into their launch (a larger scan's own workgroups would hold
-// the CUs while the products wait behind them: measured slower on the
-// 1032-tile scan of layer 0 with learnable embeddings).
-constexpr int64_t kFoldScanTiles = 256;
+// Transpose scans over at most this many sources take the weight
+// gradient's products into their launch (a larger scan's own workgroups
+// would hold the CUs while the products wait behind them: measured slower
+// on the 1.06M-source scan of layer 0 with learnable embeddings, whose
+// products take the part-product kernel of their own launch).
+constexpr int64_t kFoldScanSources = 262144;
 
 // The backward from the loss down; with table != NULL layer 0's input
 // gradient is applied to the embedding rows of block 0's sources.
@@ -936,7 +937,7 @@ int run_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights
     // gradient)
     const bool top = l == L - 1;
     const bool below = l > 0 || embed;
-    const bool beside_scan = below && gmb::csc_scan_tiles(bk.cap_src) <= kFoldScanTiles;
+    const bool beside_scan = below && bk.cap_src <= kFoldScanSources;
     gmb::WgradArgs defer{};
     gmb::ReduceArgs fold{};
     e = gmb::launch_wgrad(bk.sizes, h_in, m, d_in, cur, p.ldz[l], d_out, std::max<int64_t>(bk.cap_dst, 1), part,
