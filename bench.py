@@ -946,6 +946,10 @@ def run_train(args, wl, csr, ip, ix, feats, weights, batches, t_gen):
         "forward_linear_TFLOPs_lower_bound": fwd_flops / tf / 1e12,
         "backward_products_TFLOPs_lower_bound": bwd_flops / tb / 1e12,
         "mfma_peak_TFLOPs": FP32_MFMA_PEAK_TFLOPS,
+        "products_arithmetic": "fp32 operands cut exactly into three bf16 parts, six part products per fp32 "
+                               "product on v_mfma_f32_16x16x32_bf16, fp32 accumulation (forward linear, input "
+                               "gradients, and the weight gradient of layers with a launch of their own); the "
+                               "weight gradients of layers with an input gradient on v_mfma_f32_16x16x4_f32",
         "gemm_check": gemm_check(torch, dev),
         "stream_copy_GBps": stream_copy(torch, dev),
         "gather_GBps": None if args.fused else b_gather / (stage["gather"] / 1e3) / 1e9,
