@@ -355,7 +355,11 @@ size_t gmb_backward_workspace_bytes(const gmb_blocks* blocks, const gmb_sage_wei
  * vertex from a transpose of the block whose entries take their slots by
  * atomic counters, so each source's terms are summed in an order that can
  * change between runs, and the gradients of the layers below the last can
- * differ in their last bits. */
+ * differ in their last bits.  The transpose's offsets come from a
+ * single-pass scan whose tiles wait for their predecessors in a bounded
+ * loop (about 4M short sleeps); only a GPU that stalls a running tile for
+ * that long makes a wait give up, and then the input gradients of that
+ * call are wrong (the call reports no status for it). */
 int gmb_sage_backward(const gmb_blocks* blocks, const void* x, const gmb_sage_weights* weights,
                       const float* logits, const int32_t* labels, const void* fwd_ws, size_t fwd_ws_bytes,
                       const gmb_sage_grads* grads, float* loss, void* ws, size_t ws_bytes, void* stream);
