@@ -1096,12 +1096,14 @@ __global__ __launch_bounds__(256) void k_pull_mean(const int32_t* __restrict__ s
 // g_u = (u < n_dst ? dH[u] : 0) + sum over u's transpose entries (v, w) of
 // w * dM[v], as a plain read-modify-write (the rows of one mini-batch are
 // distinct; mini-batches in flight together update without locks, as
-// Hogwild does; an id outside [0, num_nodes) skips its row).  The update is
-// bound by the latency of three dependent rounds of reads per row (offsets
-// and ids; table row, self part and the first entries; the entries' dM
-// rows), so each G-lane group takes R rows and issues every round for all
-// of them at once; entries past the first E of a row (few rows have them)
-// follow one by one.  Lane c covers the float4 columns c, c + G, ...
+// Hogwild does; an id outside [0, num_nodes) skips its row).  Each row
+// takes dependent rounds of reads (offsets and ids; table row, self part
+// and the first E entries; the entries' dM rows; then the rest of a longer
+// list, four entries per round), and every round is issued for the R rows
+// of a G-lane group at once.  What bounds the kernel is the rate of its
+// scattered 400-byte row accesses (table rows and dM rows), not the
+// rounds' latency: one round fewer per row measured no faster.  Lane c
+// covers the float4 columns c, c + G, ...
 template <int G, int R, int E>
 __global__ __launch_bounds__(256) void k_pull_update(const int32_t* __restrict__ sizes,
                                                      const int32_t* __restrict__ off,
