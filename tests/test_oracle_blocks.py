@@ -131,6 +131,12 @@ def test_gather_is_a_bit_copy(orc, dg):
     assert np.array_equal(orc.gather(b16, ids), b16[ids])
     with pytest.raises(orc.OracleError):
         orc.gather(f32, [500])
+    # rows that carry their own index: entry (r, c) = r * 16 + c, exact in
+    # fp32, so every gathered row decodes to the id it was asked for
+    own = np.arange(500 * 16, dtype=np.float32).reshape(500, 16)
+    got = orc.gather(own, ids)
+    assert np.array_equal(got[:, 0].astype(np.int64) // 16, ids)
+    assert np.array_equal(got - got[:, :1], np.tile(np.arange(16, dtype=np.float32), (len(ids), 1)))
 
 
 def test_mean_aggregate_matches_dense(orc, dg, tiny):

@@ -58,6 +58,19 @@ MUTANTS = {
     # backward: loss gradient not divided by the batch size
     "bwd_xent_not_mean": ("dz[v * C + c] = (p - (c == y[v] ? 1.0 : 0.0)) / (double)n;",
                           "dz[v * C + c] = (p - (c == y[v] ? 1.0 : 0.0));"),
+    # gather: the row before the named one
+    "gather_wrong_row": ("(const char*)feats + ids[i] * row_bytes",
+                         "(const char*)feats + (ids[i] > 0 ? ids[i] - 1 : 0) * row_bytes"),
+    # seeds: a repeated seed accepted instead of refused
+    "seed_duplicate_accepted": ("if (map[s] != 0) { free(front);", "if (0) { free(front);"),
+    # sampling: the drawn slots left in Floyd's order instead of ascending
+    "sample_slots_unsorted": ("qsort(slots, k, sizeof(uint32_t), cmp_u32);", "(void)cmp_u32;"),
+    # sampling: a row of degree <= fan-out taken back to front
+    "sample_small_row_reversed": ("for (int64_t s = 0; s < d; ++s) slots[s] = (uint32_t)s;",
+                                  "for (int64_t s = 0; s < d; ++s) slots[s] = (uint32_t)(d - 1 - s);"),
+    # SAGE: the ReLU applied on every layer, the last one too
+    "sage_relu_everywhere": ("out[v * d_out + o] = (relu && z < 0.0) ? 0.0 : z;",
+                             "out[v * d_out + o] = (z < 0.0) ? 0.0 : z;"),
     # backward: neighbour weight gradient taken from the self input
     "bwd_neigh_from_self": ("const double hc = H[v * d_in + c], mc = m[v * d_in + c];",
                             "const double hc = H[v * d_in + c], mc = H[v * d_in + c];"),
@@ -99,11 +112,12 @@ def _build_mutant(tmpdir, name):
 
 
 def _fails(fn):
-    """True when the pin rejects the mutant (an assertion fails).  Any other
+    """True when the pin rejects the mutant: an assertion fails, or a
+    pytest.raises in it sees no error where one is due.  Any other
     exception does not count as a catch."""
     try:
         fn()
-    except AssertionError:
+    except (AssertionError, pytest.fail.Exception):
         return True
     except Exception:
         return False
@@ -120,6 +134,8 @@ def test_pins_catch_mutant(name, tmp_path, dg):
         "floyd": lambda: ts.test_floyd_brute_force_exact_uniformity(mut, 5),
         "chi2": lambda: ts.test_keyed_subsets_uniform_over_keys(pins, 8, 3, 200000),
         "blocks": lambda: tb.test_tiny_blocks_invariants(mut, dg, tiny),
+        "errors": lambda: tb.test_error_statuses(mut, tiny),
+        "gather": lambda: tb.test_gather_is_a_bit_copy(mut, dg),
         "rmat": lambda: tb.test_rmat_blocks_invariants_with_hubs(mut, dg),
         "mean": lambda: tb.test_mean_aggregate_matches_dense(mut, dg, tiny),
         "dense": lambda: tb.test_full_neighbourhood_equals_dense_sage(mut, dg, 2),
