@@ -71,6 +71,17 @@ MUTANTS = {
     # SAGE: the ReLU applied on every layer, the last one too
     "sage_relu_everywhere": ("out[v * d_out + o] = (relu && z < 0.0) ? 0.0 : z;",
                              "out[v * d_out + o] = (z < 0.0) ? 0.0 : z;"),
+    # mean: a row without edges divided by its count as well (0 / 0)
+    "mean_empty_row_divided": ("    if (k > 0)\n      for (int64_t c = 0; c < d; ++c) row[c] = row[c] / (double)k;",
+                               "    for (int64_t c = 0; c < d; ++c) row[c] = row[c] / (double)k;"),
+    # loss: the label's class shifted by one
+    "xent_label_shifted": ("loss += -(row[y[v]] - mx - log(sum));", "loss += -(row[(y[v] + 1) % C] - mx - log(sum));"),
+    # backward: the bias gradient summed over one row only
+    "bwd_bias_one_row": ("for (int64_t v = 0; v < n; ++v) s += dZ[v * d_out + o];", "s += dZ[o];"),
+    # backward: the ReLU mask letting the clamped units through
+    "bwd_relu_mask_at_zero": ("dZ[i] = out[i] > 0.0 ? dOut[i] : 0.0;", "dZ[i] = out[i] >= 0.0 ? dOut[i] : 0.0;"),
+    # backward: the mean's gradient sent to the destination instead of the source
+    "bwd_mean_to_destination": ("double* h = dH + local[e] * d;", "double* h = dH + v * d;"),
     # backward: neighbour weight gradient taken from the self input
     "bwd_neigh_from_self": ("const double hc = H[v * d_in + c], mc = m[v * d_in + c];",
                             "const double hc = H[v * d_in + c], mc = H[v * d_in + c];"),
