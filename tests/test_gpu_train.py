@@ -115,14 +115,18 @@ def test_train_step_matches_the_oracle(orc, dg, dims, fanouts, n_seeds):
     csr.check_status()
 
 
-def test_repeated_backward(orc, dg):
+@pytest.mark.parametrize("dims,fanouts,n_seeds", [([16, 32, 32, 6], [4, 4, 8], 120),
+                                                  ([100, 47], [8], 600)])
+def test_repeated_backward(orc, dg, dims, fanouts, n_seeds):
     """The last layer's gradients are summed in a fixed order: identical bits
     on every run; the layers below take the fp32 atomic adds of the mean's
-    backward and agree within the tolerance."""
-    n, dims, fanouts = 3000, [16, 32, 32, 6], [4, 4, 8]
+    backward and agree within the tolerance.  The one-layer case puts the
+    last layer's products in a launch of their own (the part-product weight
+    gradient: two column tiles, several row ranges)."""
+    n = 3000
     g = exact_graph(n, 21)
     feats, w = exact_model(dg, n, dims, 22)
-    seeds = dg.permutation(n, 23)[:120]
+    seeds = dg.permutation(n, 23)[:n_seeds]
     labels = torch.from_numpy(dg.labels(n, dims[-1], 24)[seeds]).cuda()
     csr = csr_on_device(g)
     wt = to_torch_weights(w)
