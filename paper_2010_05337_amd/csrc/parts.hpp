@@ -99,6 +99,9 @@ struct LinearOp {
   const float* bias_v;
   int K, N, relu;
   float* out;
+  int quad_b;   // N % 4 == 0 and 16-byte aligned matrices: the slab takes load_b8x4
+  static constexpr bool kQuadCapable = true;
+  static constexpr bool kEarlyA = true;   // the first tile's A loads overlap the slab's
   __host__ __device__ int k2() const { return 2 * K; }
   __host__ __device__ int n() const { return N; }
   __host__ __device__ int64_t ldo() const { return N; }
@@ -125,6 +128,23 @@ struct LinearOp {
       w[s8] = pick_ptr(in[s8] & (k >= K), Wn, Ws)[static_cast<int64_t>(kr) * N + (in[s8] ? gn : 0)];
     }
   }
+  // B[k0 .. k0 + 7][gn .. gn + 3] (quad_b set, gn % 4 == 0): eight 16-byte
+  // loads, one per row, w[j][s] = B[k0 + s][gn + j]; in[s] false where row
+  // k0 + s lies outside B or the quad past N (its load reads W_self's first
+  // values).  K N < 2^31, so an element offset fits in 32 bits.
+  __device__ void load_b8x4(bool item, int k0, int gn, float (&w)[4][8], bool (&in)[8]) const {
+    const bool cols = item & (gn < N);
+    const uint32_t gc = cols ? static_cast<uint32_t>(gn) : 0u;
+#pragma unroll
+    for (int s8 = 0; s8 < 8; ++s8) {
+      const int k = k0 + s8;
+      in[s8] = cols & (k < 2 * K);
+      const bool hi = in[s8] & (k >= K);
+      const uint32_t kr = in[s8] ? static_cast<uint32_t>(hi ? k - K : k) : 0u;
+      const float4 x = *reinterpret_cast<const float4*>(pick_ptr(hi, Wn, Ws) + (kr * static_cast<uint32_t>(N) + gc));
+      w[0][s8] = x.x; w[1][s8] = x.y; w[2][s8] = x.z; w[3][s8] = x.w;
+    }
+  }
   __device__ float bias(int col) const { return bias_v[col < N ? col : N - 1]; }
   __device__ float act(float z) const { return relu ? (z > 0.f ? z : 0.f) : z; }
   __device__ float* out_at(int64_t row, int col) const { return out + row * N + col; }
@@ -134,6 +154,8 @@ struct LinearOp {
 // W_neigh]^T (B[k][nn] = W[nn][k], 2 d_in columns), the result's columns
 // nn < d_in to dH and the others to dM (row stride d_in each).
 struct DgradOp {
+  static constexpr bool kQuadCapable = false;   // its eight k are one contiguous run already
+  static constexpr bool kEarlyA = false;        // (the largest tiling has no registers to spare for it)
   const float* dZ;
   const float* Ws;
   const float* Wn;
@@ -192,11 +214,79 @@ __device__ __forceinline__ void parts_gemm(const Op& op, int32_t M) {
   if (static_cast<int>(blockIdx.x) >= row_tiles) return;
   const int n0 = blockIdx.y * BN;
   const int N = op.n();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, r16 = lane & 15;
+  // first row of fragment f of row tile rt (SPLIT = 1: wave w owns
+  // fragments w R .. w R + R - 1; split K: every wave takes all R)
+  auto frag_row0 = [&](int rt, int f) { return rt * ROWS + (SPLIT > 1 ? f : wave * R + f) * 16; };
+  auto frag_rows = [&](int rt, int f, const float*& hrow, const float*& grow) {
+    const int row = frag_row0(rt, f) + r16;
+    op.a_rows(row < M ? row : M - 1, hrow, grow);   // a row past the end reads row M-1
+  };
+  auto load4 = [&](const float* hrow, const float* grow, int k) -> float4 { return op.load_a4(hrow, grow, k); };
+  auto chunk_of = [&](int i) { return SPLIT > 1 ? wave + WAVES * i : i; };
+  float4 a[R][MYCH][2];
+  const float* hr[R];
+  const float* gr[R];
+  // the first tile's A values, issued between the slab's loads and their
+  // use, so that the two round trips overlap
+  auto issue_first_a = [&]() {
+#pragma unroll
+    for (int f = 0; f < R; ++f) {
+      frag_rows(blockIdx.x, f, hr[f], gr[f]);
+#pragma unroll
+      for (int i = 0; i < MYCH; ++i) {
+        const int k = chunk_of(i) * 32 + 8 * q;
+        a[f][i][0] = load4(hr[f], gr[f], k);
+        a[f][i][1] = load4(hr[f], gr[f], k + 4);
+      }
+    }
+  };
   // slab fill: item (c, q, n) reads B[32c + 8q .. +7][n0 + n] (the
   // policy's eight loads), cuts them into parts and writes one 16-byte word
-  // per plane; a thread issues the loads of all its items before the first
-  // use (one round trip to the L2 instead of one per item)
-  {
+  // per plane; where the policy can (the forward's row-major matrices with N
+  // % 4 == 0), an item takes four adjacent columns with eight 16-byte loads
+  // instead (a quarter of the load instructions and their address work).  A
+  // thread issues the loads of all its items before the first use (one
+  // round trip to the L2 instead of one per item), and with kEarlyA the
+  // first tile's A loads go out behind them
+  bool quad = false;
+  if constexpr (Op::kQuadCapable) quad = op.quad_b != 0;
+  if (quad) {
+    // four adjacent columns per item: eight 16-byte loads, four words per plane
+    if constexpr (Op::kQuadCapable) {
+      constexpr int kQuads = NCH * 4 * BN / 4, kPer = (kQuads + THREADS - 1) / THREADS;
+      float w[kPer][4][8];
+      bool in[kPer][8];
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int it = threadIdx.x + THREADS * u;
+        const int n4 = it % (BN / 4), cq = it / (BN / 4);
+        op.load_b8x4(it < kQuads, cq * 8, n0 + 4 * n4, w[u], in[u]);
+      }
+      if constexpr (Op::kEarlyA) issue_first_a();
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int it = threadIdx.x + THREADS * u;
+        if (it >= kQuads) continue;
+        const int n4 = it % (BN / 4), cq = it / (BN / 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+          for (int s8 = 0; s8 < 8; ++s8) {
+            opaque(w[u][j][s8]);
+            w[u][j][s8] = in[u][s8] ? w[u][j][s8] : 0.f;
+          }
+          bf16x8 part[3];
+          split8(make_float4(w[u][j][0], w[u][j][1], w[u][j][2], w[u][j][3]),
+                 make_float4(w[u][j][4], w[u][j][5], w[u][j][6], w[u][j][7]), part);
+#pragma unroll
+          for (int p = 0; p < 3; ++p)
+            *reinterpret_cast<bf16x8*>(&Bp[p * PLANE + (cq * BN + 4 * n4 + j) * 8]) = part[p];
+        }
+      }
+    }
+  } else {
     constexpr int kItems = NCH * 4 * BN, kPer = (kItems + THREADS - 1) / THREADS;
     float w[kPer][8];
     bool in[kPer][8];
@@ -206,6 +296,7 @@ __device__ __forceinline__ void parts_gemm(const Op& op, int32_t M) {
       const int n = it % BN, cq = it / BN;
       op.load_b8(it < kItems, cq * 8, n0 + n, w[u], in[u]);
     }
+    if constexpr (Op::kEarlyA) issue_first_a();
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       const int it = threadIdx.x + THREADS * u;
@@ -223,30 +314,7 @@ __device__ __forceinline__ void parts_gemm(const Op& op, int32_t M) {
     }
   }
   __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int q = lane >> 4, r16 = lane & 15;
-  // first row of fragment f of row tile rt (SPLIT = 1: wave w owns
-  // fragments w R .. w R + R - 1; split K: every wave takes all R)
-  auto frag_row0 = [&](int rt, int f) { return rt * ROWS + (SPLIT > 1 ? f : wave * R + f) * 16; };
-  auto frag_rows = [&](int rt, int f, const float*& hrow, const float*& grow) {
-    const int row = frag_row0(rt, f) + r16;
-    op.a_rows(row < M ? row : M - 1, hrow, grow);   // a row past the end reads row M-1
-  };
-  auto load4 = [&](const float* hrow, const float* grow, int k) -> float4 { return op.load_a4(hrow, grow, k); };
-  auto chunk_of = [&](int i) { return SPLIT > 1 ? wave + WAVES * i : i; };
-  float4 a[R][MYCH][2];
-  const float* hr[R];
-  const float* gr[R];
-#pragma unroll
-  for (int f = 0; f < R; ++f) {
-    frag_rows(blockIdx.x, f, hr[f], gr[f]);
-#pragma unroll
-    for (int i = 0; i < MYCH; ++i) {
-      const int k = chunk_of(i) * 32 + 8 * q;
-      a[f][i][0] = load4(hr[f], gr[f], k);
-      a[f][i][1] = load4(hr[f], gr[f], k + 4);
-    }
-  }
+  if constexpr (!Op::kEarlyA) issue_first_a();
   // bias of this lane's columns n0 + 16 j + lane % 16 (fixed over the tiles;
   // with split K the thread's stored entries have the same lane % 16)
   float bv[J];

@@ -673,7 +673,8 @@ template <int NCH, int J, int R, int SPLIT, int WAVES>
 void launch_parts(const int32_t* sizes, const float* hs, const float* ag, const float* ws, const float* wn,
                   const float* bias, int K, int N, int relu, float* out, int64_t cap_rows, hipStream_t s) {
   static_assert(parts::parts_lds_bytes(NCH, J, R, SPLIT, WAVES) <= 160 * 1024, "slab exceeds the LDS");
-  const parts::LinearOp op{hs, ag, ws, wn, bias, K, N, relu, out};
+  const bool quad = N % 4 == 0 && (reinterpret_cast<uintptr_t>(ws) | reinterpret_cast<uintptr_t>(wn)) % 16 == 0;
+  const parts::LinearOp op{hs, ag, ws, wn, bias, K, N, relu, out, quad ? 1 : 0};
   hipLaunchKernelGGL((k_linear_f32_parts<NCH, J, R, SPLIT, WAVES>), (parts::parts_grid<J, R, SPLIT, WAVES>(cap_rows, N)),
                      dim3(64 * WAVES), 0, s, sizes, op);
 }
