@@ -271,7 +271,12 @@ def summarize_profile(args):
 
 
 COPY_BYTES = 1 << 30   # the plain copy that calibrates bandwidth and HBM counters
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gather_products2m_traffic.json")
+
+
+def traffic_file(workload: str) -> str:
+    """Stored counter summary of the gather kernel on one workload."""
+    return os.path.join(ROOT, "profiles", f"k_gather_{workload}_traffic.json")
+
 GATHER_SOURCE = os.path.join(ROOT, "paper_2010_05337_amd", "csrc", "gather.hip")
 
 
@@ -293,9 +298,9 @@ def _pmc_per_dispatch(d: str, counter: str):
                 continue
             name = r["Kernel_Name"].replace("gmb::(anonymous namespace)::", "").replace("void ", "")
             per = acc.setdefault(name, {})
-            key = r.get("Dispatch_Id", str(len(per)))
+            key = int(r.get("Dispatch_Id", len(per)))
             per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
-    return {k: list(v.values()) for k, v in acc.items()}
+    return {k: [v[i] for i in sorted(v)] for k, v in acc.items()}   # in dispatch order
 
 
 SIMDS = 256 * 4          # MI355X: 256 CUs of 4 SIMDs
@@ -400,16 +405,21 @@ def summarize_pmc(args):
     """HBM bytes per launch of the gather kernel from FETCH_SIZE and
     WRITE_SIZE (KiB per dispatch), each scaled by the factor that makes the
     same counter read the known size of the plain copy (COPY_BYTES read,
-    COPY_BYTES written) in the same run.  The copy's dispatches are the
-    copy-kernel dispatches within 20% of the largest."""
+    COPY_BYTES written) in the same run.  The gather's dispatches are the
+    run's last `--steps` ones: pass G, the launches `roofline` divides its
+    algorithmic bytes over (the earlier passes hold smaller batches too).
+    The copy's dispatches are the copy-kernel dispatches within 20% of the
+    largest."""
     fetch = _pmc_per_dispatch(args.summarize_pmc[0], "FETCH_SIZE")
     write = _pmc_per_dispatch(args.summarize_pmc[1], "WRITE_SIZE")
 
     def gather(tab):
         ks = [k for k in tab if "k_gather" in k]
-        if not ks:
-            raise SystemExit("no gather dispatches in the counter files")
-        v = [x for k in ks for x in tab[k]]
+        if len(ks) != 1:
+            raise SystemExit(f"expected one gather kernel in the counter files, found {len(ks)}")
+        v = tab[ks[0]][-args.steps:]
+        if len(v) < args.steps:
+            raise SystemExit(f"{len(v)} gather dispatches, fewer than --steps {args.steps}")
         return ks[0].split("(")[0], sum(v) / len(v), len(v)
 
     def copy(tab):
@@ -434,7 +444,9 @@ def summarize_pmc(args):
     # the benchmark line of the FETCH_SIZE run, if saved next to its CSV
     try:
         with open(os.path.join(args.summarize_pmc[0], "bench.json")) as f:
-            alg = json.loads(f.read().strip().splitlines()[-1])["roofline"]["alg_bytes_per_launch"]
+            line = json.loads(f.read().strip().splitlines()[-1])
+        alg = line["roofline"]["alg_bytes_per_launch"]
+        out["workload"] = line["config"]["workload"].split(":")[0]
         out["alg_bytes_per_launch"] = alg
         out["traffic_over_alg"] = out["traffic_bytes_per_launch"] / alg
     except (OSError, ValueError, KeyError, IndexError):
@@ -444,20 +456,23 @@ def summarize_pmc(args):
 
 def gather_traffic(workload: str):
     """Measured HBM bytes per gather launch and where they come from: the
-    stored counter summary of the products2m workload, if it was taken on the
-    current gather kernel (digest of its source); otherwise (None, reason)."""
-    if workload != "products2m":
-        return None, f"no counter run stored for the {workload} workload"
+    stored counter summary of this workload, if it was taken on the current
+    gather kernel (digest of its source); otherwise (None, reason)."""
+    path = traffic_file(workload)
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             t = json.load(f)
-    except (OSError, ValueError):
-        return None, "no stored counter summary"
+    except OSError:
+        return None, f"no counter run stored for the {workload} workload"
+    except ValueError:
+        return None, f"unreadable counter summary {os.path.relpath(path, ROOT)}"
+    if t.get("workload", "products2m") != workload:
+        return None, f"{os.path.relpath(path, ROOT)} was taken on another workload"
     digest = _source_digest(GATHER_SOURCE)
     if t.get("gather_source_sha256_16") != digest:
         return None, "the stored counter summary predates the current gather kernel"
     return t["traffic_bytes_per_launch"], (
-        f"not measured in this run: {os.path.relpath(TRAFFIC_FILE, ROOT)}, two rocprofv3 --pmc runs "
+        f"not measured in this run: {os.path.relpath(path, ROOT)}, two rocprofv3 --pmc runs "
         f"(FETCH_SIZE, WRITE_SIZE) of the command recorded there, calibrated by a 1 GiB copy; "
         f"gather.hip digest {digest} matches")
 
