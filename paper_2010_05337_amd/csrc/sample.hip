@@ -1051,8 +1051,13 @@ __global__ __launch_bounds__(kScanBlock) void k_rank(RankArgs a, CsrArgs ga, int
   __shared__ int s_tile;
   __shared__ int32_t s_excl[NV];
   __shared__ int32_t s_wave[NV * (kScanBlock / 64)];
-  __shared__ int32_t s_key[T];
-  __shared__ int32_t s_res[T];   // the answers; then the new vertices' local ids
+  // edge j of the router at slot(j): one pad word after every ITEMS
+  // entries, so that a thread's ITEMS consecutive entries start ITEMS + 1
+  // words after its neighbour's (an odd stride: no two lanes of a wave on
+  // one bank)
+  auto slot = [](int32_t j) { return j + j / ITEMS; };
+  __shared__ int32_t s_key[T + T / ITEMS];
+  __shared__ int32_t s_res[T + T / ITEMS];   // the answers; then the new vertices' local ids
   const CsrView g = view(ga);
   int32_t basev[NV];
 #pragma unroll
@@ -1081,8 +1086,8 @@ __global__ __launch_bounds__(kScanBlock) void k_rank(RankArgs a, CsrArgs ga, int
       const int32_t i = threadIdx.x + k * kScanBlock;
       const int32_t j = static_cast<int32_t>(pr[k].y & ~kEdgeTag) - r.e0;
       if (i < M && (pr[k].y & kEdgeTag) && j >= 0 && j < E) {
-        s_key[j] = static_cast<int32_t>(pr[k].x);
-        s_res[j] = an[k];
+        s_key[slot(j)] = static_cast<int32_t>(pr[k].x);
+        s_res[slot(j)] = an[k];
       }
     }
   }
@@ -1092,8 +1097,8 @@ __global__ __launch_bounds__(kScanBlock) void k_rank(RankArgs a, CsrArgs ga, int
 #pragma unroll
   for (int q = 0; q < ITEMS; ++q) {
     const bool in = base + q < E;
-    u[q] = in ? s_key[base + q] : -1;
-    ans[q] = in ? s_res[base + q] : 0;
+    u[q] = in ? s_key[slot(base + q)] : -1;
+    ans[q] = in ? s_res[slot(base + q)] : 0;
   }
   uint32_t flags = 0;
 #pragma unroll
@@ -1143,7 +1148,7 @@ __global__ __launch_bounds__(kScanBlock) void k_rank(RankArgs a, CsrArgs ga, int
     if ((flags >> q) & 1u) {
       ids[rk] = u[q];
       a.local[r.e0 + base + q] = rk;
-      s_res[base + q] = rk;
+      s_res[slot(base + q)] = rk;
 #pragma unroll
       for (int v = 1; v < NV; ++v) {
         a.indptr[v][rk] = run[v];
@@ -1159,7 +1164,7 @@ __global__ __launch_bounds__(kScanBlock) void k_rank(RankArgs a, CsrArgs ga, int
     int32_t loc = ans[q];   // a known vertex's local id
     if (loc < 0) {
       const int32_t e0 = -(loc + 1);   // the first occurrence, earlier than this edge
-      if (e0 >= r.e0 && e0 < r.e1) loc = s_res[e0 - r.e0];
+      if (e0 >= r.e0 && e0 < r.e1) loc = s_res[slot(e0 - r.e0)];
     }
     a.local[r.e0 + base + q] = loc;
   }
