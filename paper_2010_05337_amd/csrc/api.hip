@@ -127,8 +127,17 @@ int plan_sampling(int32_t num_seeds, const int32_t* fanouts, int32_t num_layers,
         return fail(GMB_EINVAL, "hop %d: %lld destinations need %lld routers, above %d", h,
                     static_cast<long long>(hp.cap_dst), static_cast<long long>(routers), gmb::kMaxRouters);
       hp.routers = static_cast<int32_t>(routers);
-      hp.owners = static_cast<int32_t>(std::min<int64_t>(
-          gmb::kMaxOwners, std::max<int64_t>(1, (hp.cap_nnz + hp.cap_dst + gmb::kOwnerPairs - 1) / gmb::kOwnerPairs)));
+      const int64_t pairs = hp.cap_nnz + hp.cap_dst;
+      int64_t owners = std::max<int64_t>(1, (pairs + gmb::kOwnerPairs - 1) / gmb::kOwnerPairs);
+      // one owner per CU at a time: a count just past a multiple of the CU
+      // count would run its last owners as a wave of their own, doubling
+      // the kernel; take the multiple below while each owner's share at full
+      // capacity still fits three quarters of its table
+      if (owners > gmb::kComputeUnits) {
+        const int64_t lower = (owners - 1) / gmb::kComputeUnits * gmb::kComputeUnits;
+        if ((pairs + lower - 1) / lower <= gmb::kOwnerSlots * 3 / 4) owners = lower;
+      }
+      hp.owners = static_cast<int32_t>(std::min<int64_t>(gmb::kMaxOwners, owners));
       hp.tile_stride = hp.routers;
     }
     hp.tiles_word = zero_words;

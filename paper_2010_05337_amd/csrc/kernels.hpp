@@ -85,6 +85,9 @@ constexpr int kMaxSpan = 1024;
 constexpr int kOwnerSlots = 8192;
 // pairs per owner the plan aims at, at full capacity (half the table)
 constexpr int64_t kOwnerPairs = 4096;
+// compute units of the MI355X (gfx950); an owner's LDS table takes most of
+// a CU's LDS, so one owner workgroup runs per CU at a time
+constexpr int kComputeUnits = 256;
 
 // Sampling arguments of one hop (fan-out f, model layer `layer`); the
 // first hop also checks the seeds (check_seeds).  fix: the previous hop's
